@@ -1,0 +1,98 @@
+/* Flash Swin attention forward for AMD MI355X (gfx950) -- C ABI.
+ *
+ * Operation (HRSAM, arXiv 2407.02109):
+ *   Eq. 1 (Sec. 3.2) scaled dot-product attention, evaluated independently inside each
+ *   shifted window of Sec. 3.3 ("Flash Swin"), with the KV-only padding of Sec. 3.4 /
+ *   App. B as an option.  Window partition, cyclic shift, border padding and masking all
+ *   happen inside one kernel launch; no reordered copy of q, k, v or out is made.
+ *
+ * Semantics.  Tokens sit on an Hgrid x Wgrid grid in raster order (token j at row
+ * j / Wgrid, column j % Wgrid; Sec. 3.3's vanilla map).  Along each axis, coordinate c
+ * belongs to region floor((c - shift) / window) (floor division).  This is the paper's
+ * construction -- window - shift virtual tokens in front of the axis, unshifted windows on
+ * the padded canvas, virtual tokens dropped -- extended to any 0 <= shift < window and to
+ * grids that are not a multiple of the window (then the last windows are cut off by the
+ * grid border, like the first ones).  For every query token (b, y, x) and head h:
+ *
+ *   R      = { tokens (y', x') of the grid : same row region as y, same column region as x }
+ *   z_j    = <q[b, y*W + x, h, :], k[b, j, h, :]> / sqrt(head_dim)          (j in R)
+ *   out    = sum_j softmax(z)_j * v[b, j, h, :]                       (FLA_PAD_MASK)
+ *
+ * FLA_PAD_KVTOKEN (Sec. 3.4, App. B): every key slot of the query's window x window
+ * canvas square that is not a grid token reads the learnable pad token stored at row
+ * L = Hgrid*Wgrid of k and v; it enters the softmax once per such slot, i.e. with
+ * multiplicity n_pad = window^2 - |R|.  Queries are never padded.
+ *
+ * Layout.  q and out: [B, Hgrid*Wgrid, heads, head_dim], contiguous, row-major.
+ * k and v: the same, or [B, Hgrid*Wgrid + 1, heads, head_dim] in FLA_PAD_KVTOKEN mode
+ * (row L is the pad token of each batch entry and head).  All four are device pointers
+ * owned by the caller; the library never allocates, frees, copies or synchronises.
+ * q, k and v may alias each other; out must not overlap any of them.
+ *
+ * Errors.  Each entry point checks its arguments in the order of the status codes below
+ * (after the size checks) and returns the first failure without launching anything and
+ * without touching out.  An empty problem (B, heads, Hgrid or Wgrid equal to 0) returns
+ * FLA_OK at once and ignores the pointers.  Launches are asynchronous on `stream`
+ * (a hipStream_t; NULL = the null stream): a fault during execution surfaces at the
+ * caller's next synchronisation, not here.  The library is stateless apart from a
+ * per-device architecture probe and is safe to call from several threads.
+ */
+#ifndef FLA_SWIN_H
+#define FLA_SWIN_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FLA_PAD_MASK = 0,     /* virtual / out-of-grid key slots are excluded from the softmax */
+    FLA_PAD_KVTOKEN = 1   /* virtual key slots read the pad token at row L of k and v       */
+} fla_pad_mode;
+
+typedef enum {
+    FLA_OK = 0,
+    FLA_ERR_SHAPE = 1,     /* B, heads, Hgrid or Wgrid negative                            */
+    FLA_ERR_NULL = 2,      /* a pointer is NULL on a non-empty problem                     */
+    FLA_ERR_ALIGN = 3,     /* a pointer is not 16-byte aligned                             */
+    FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (this build: 64)                   */
+    FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
+    FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
+    FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */
+    FLA_ERR_ALIAS = 8,     /* out overlaps q, k or v                                       */
+    FLA_ERR_TOO_LARGE = 9, /* a tensor has 2^40 elements or more, or the grid is too big   */
+    FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
+    FLA_ERR_LAUNCH = 11    /* the HIP runtime refused the kernel launch                    */
+} fla_status;
+
+/* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
+ * Q.K^T and P.V run on bf16 matrix cores with fp32 accumulation; softmax in fp32;
+ * P is rounded to bf16 before P.V.  Returns an fla_status. */
+int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out,
+                      int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                      int window, int shift, int pad_mode, void* stream);
+
+/* fp32 forward: same operation and layout with float tensors, computed entirely in
+ * fp32 (used for tight-tolerance checks on small grids).  Returns an fla_status. */
+int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out,
+                          int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                          int window, int shift, int pad_mode, void* stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* fla_status_string(int status);
+
+/* Algorithmic work of one call, host arithmetic only (no device access):
+ *   *flops = 4 * head_dim * heads * B * (sum over windows of n^2), plus one pad key per
+ *            query of a window with virtual slots in FLA_PAD_KVTOKEN mode; n is the number
+ *            of grid tokens in the window (Q.K^T and P.V, masked pairs not counted);
+ *   *bytes = elem_bytes * heads * head_dim * B * (4 * Hgrid * Wgrid (+2 pad rows)):
+ *            q, k, v read once and out written once.
+ * Either output pointer may be NULL.  Returns FLA_OK or the argument status code. */
+int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                       int window, int shift, int pad_mode, int elem_bytes,
+                       double* flops, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLA_SWIN_H */

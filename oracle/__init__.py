@@ -1,0 +1,22 @@
+"""Plain fp64 CPU oracle for Flash Swin attention (HRSAM, arXiv 2407.02109, Sec. 3.3-3.4, App. A-B).
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check in
+``__graft_entry__`` and the CPU-baseline leg of ``bench.py`` may import this package.
+The GPU library never imports it and shares no code, table or helper with it.
+
+Every function here is a slow, obviously-correct restatement of the paper's
+definitions in float64 NumPy; see ``swin_oracle`` for the four forms.
+"""
+from .swin_oracle import (  # noqa: F401
+    PAD_MASK,
+    PAD_KVTOKEN,
+    swin_attention_textbook,
+    swin_attention_canvas,
+    swin_attention_fla,
+    swin_attention_bruteforce,
+    swin_attention_at,
+    fla_shift_window_indices,
+    fla_kv_padding_indices,
+    window_sizes,
+    work_counts,
+)

@@ -1,0 +1,18 @@
+"""Flash Swin attention for AMD MI355X (gfx950).
+
+The compute lives in the HIP library ``libfla_swin.so`` built from ``csrc/``; this
+package only marshals arguments to its C ABI (see ``binding``).  Importing the package
+does not load the library; the first call does, and fails loudly if it is missing.
+"""
+from .binding import (  # noqa: F401
+    FLA_PAD_MASK,
+    FLA_PAD_KVTOKEN,
+    FlaError,
+    fla_swin_attn_fwd,
+    fla_swin_attn_fwd_f32,
+    fla_status_string,
+    fla_swin_attn_work,
+    swin_attn,
+    library_path,
+    load_library,
+)

@@ -1,0 +1,124 @@
+"""Seeded synthetic inputs for Flash Swin attention.
+
+This module draws random numbers and nothing else: it holds none of the attention
+arithmetic, so both the GPU tests and the fp64 oracle can consume its output.
+
+Workloads are token grids shaped like the paper's ViT-B encoder inputs (16x16 patches,
+12 heads of 64 channels, window 16, shift 8; Sec. 3.3, Sec. 4.1 and App. D): 1024^2,
+2048^2 and 4096^2 images give 64x64, 128x128 and 256x256 token grids.  Values are
+i.i.d. N(0, 1) from a seeded CPU generator, scaled by exact powers of two and rounded
+to the storage dtype (round-to-nearest-even), so the oracle sees exactly the values the
+GPU sees.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+
+import torch
+
+PAD_MASK = 0
+PAD_KVTOKEN = 1
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    heads: int
+    H: int
+    W: int
+    head_dim: int
+    window: int
+    shift: int
+    dtype: str                 # "bf16" | "f32"
+    seed: int
+    pad_mode: int = PAD_MASK
+    scale: float = 1.0         # exact power of two applied to q, k and v before rounding
+    stress_keys: float = 0.0   # fraction of (token, head) key rows multiplied by 8
+    note: str = field(default="", compare=False)
+
+    @property
+    def L(self) -> int:
+        return self.H * self.W
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+WORKLOADS = {
+    "tiny_s0": Workload("tiny_s0", 1, 1, 32, 32, 64, 8, 0, "f32", seed=0,
+                        note="32x32 grid, window 8, no shift, fp32"),
+    "tiny_s4": Workload("tiny_s4", 1, 1, 32, 32, 64, 8, 4, "f32", seed=0,
+                        note="32x32 grid, window 8, shift 4, fp32"),
+    "img1024": Workload("img1024", 1, 12, 64, 64, 64, 16, 8, "bf16", seed=1, scale=0.125,
+                        note="1024^2 image: 64x64 tokens, 12 heads x 64, window 16, shift 8"),
+    "img2048": Workload("img2048", 1, 12, 128, 128, 64, 16, 8, "bf16", seed=2,
+                        note="2048^2 image: 128x128 tokens, 12 heads x 64, window 16, shift 8"),
+    "img4096": Workload("img4096", 1, 12, 256, 256, 64, 16, 8, "bf16", seed=3, stress_keys=0.01,
+                        note="4096^2 image: 256x256 tokens, 12 heads x 64, window 16, shift 8, "
+                             "1% of key rows x8"),
+    "ragged150x203": Workload("ragged150x203", 4, 12, 150, 203, 64, 16, 8, "bf16", seed=4,
+                              note="non-divisible 150x203 grid, B=4, 12 heads x 64, window 16, "
+                                   "shift 8, padded keys masked"),
+}
+
+
+def make_inputs(wl: Workload, device: str | torch.device = "cpu"):
+    """Return (q, k, v) as contiguous [B, L(+1), heads, head_dim] tensors of wl's dtype.
+
+    In KV-token mode k and v carry one extra row (index L), the pad token, drawn like the
+    others.  Generation always happens on the CPU generator so every device sees the same
+    bytes."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(wl.seed)
+    rows_kv = wl.L + (1 if wl.pad_mode == PAD_KVTOKEN else 0)
+    q = torch.randn(wl.B, wl.L, wl.heads, wl.head_dim, generator=g, dtype=torch.float32)
+    k = torch.randn(wl.B, rows_kv, wl.heads, wl.head_dim, generator=g, dtype=torch.float32)
+    v = torch.randn(wl.B, rows_kv, wl.heads, wl.head_dim, generator=g, dtype=torch.float32)
+    if wl.scale != 1.0:
+        q.mul_(wl.scale)
+        k.mul_(wl.scale)
+        v.mul_(wl.scale)
+    if wl.stress_keys > 0:
+        n_rows = wl.B * wl.L * wl.heads
+        n_hot = int(round(wl.stress_keys * n_rows))
+        hot = torch.randperm(n_rows, generator=g)[:n_hot]
+        kv = k[:, : wl.L].reshape(n_rows, wl.head_dim)   # view over the real key rows
+        kv[hot] *= 8.0
+    dt = wl.torch_dtype
+    out = []
+    for t in (q, k, v):
+        t = t.to(dt).contiguous()
+        out.append(t.to(device) if str(device) != "cpu" else t)
+    return tuple(out)
+
+
+def to_f64_numpy(t):
+    """Exact float64 copy of a CPU/GPU tensor (bf16 and fp32 embed exactly in fp64)."""
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def random_queries(wl: Workload, n: int, seed: int):
+    """n random (b, y, x) query positions, plus every corner of the grid (the windows
+    that the shift splits), as an int64 tensor [S, 3]."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    b = torch.randint(0, wl.B, (n,), generator=g)
+    y = torch.randint(0, wl.H, (n,), generator=g)
+    x = torch.randint(0, wl.W, (n,), generator=g)
+    pts = [torch.stack([b, y, x], dim=1)]
+    corners = []
+    for bb in {0, wl.B - 1}:
+        for yy in {0, wl.H - 1}:
+            for xx in {0, wl.W - 1}:
+                corners.append((bb, yy, xx))
+    pts.append(torch.tensor(corners, dtype=torch.int64))
+    return torch.cat(pts, dim=0)
