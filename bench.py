@@ -1,0 +1,182 @@
+#!/usr/bin/env python3
+"""Flash Swin attention benchmark on one MI355X.
+
+One step = one ``fla_swin_attn_fwd`` call: a whole shifted-window attention layer over
+every batch entry and head of the workload (window partition, shift, border handling,
+masking, Q.K^T, online softmax, P.V and the scatter back to token order, all inside the
+kernel).  Inputs are synthetic (seeded N(0,1), see paper_2407_02109_amd/synth.py) and
+resident in HBM before timing starts.
+
+Prints one JSON line: microseconds per layer (the headline), TFLOP/s and the fraction of
+the bf16 matrix-core peak, the HBM roofline of the kernel, and the fp64 CPU oracle timed
+on this host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+KERNEL_SOURCES = ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
+                  "paper_2407_02109_amd/csrc/fla_swin_internal.h"]
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
+    or None when it is missing or was taken on another version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_hash") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, q, k, v, budget_s: float):
+    """Time the fp64 oracle (textbook Plain Swin form) on this host's cores."""
+    import oracle
+    from paper_2407_02109_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    # bounded sample: whole layers of the workload when one fits the budget, else a
+    # subset of heads (every head is the same amount of work), scaled to a layer
+    heads = wl.heads
+    q64, k64, v64 = (synth.to_f64_numpy(t) for t in (q, k, v))
+    t0 = time.perf_counter()
+    oracle.swin_attention_textbook(q64[:, :, :1], k64[:, :, :1], v64[:, :, :1],
+                                   wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
+    per_head = time.perf_counter() - t0
+    use_heads = int(max(1, min(heads, budget_s / 3.0 / max(per_head, 1e-6))))
+    times = []
+    while len(times) < 3:
+        t0 = time.perf_counter()
+        oracle.swin_attention_textbook(q64[:, :, :use_heads], k64[:, :, :use_heads],
+                                       v64[:, :, :use_heads], wl.H, wl.W, wl.window, wl.shift,
+                                       wl.pad_mode)
+        times.append((time.perf_counter() - t0) * heads / use_heads)
+    return {"value": statistics.median(times) * 1e6, "unit": "us/layer", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "fp64 textbook oracle on %d of %d heads of the %s layer, median of 3, "
+                      "scaled to the whole layer; host %s with %d usable cores"
+                      % (use_heads, heads, wl.name, os.uname().machine, len(os.sched_getaffinity(0)))}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="img4096",
+                    help="img1024 | img2048 | img4096 | ragged150x203 (default: img4096)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the Flash Swin layer has no cross-GPU step in "
+              "this build (windows, heads and batch entries are independent); run with --gpus 1",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2407_02109_amd import binding, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    wl = synth.WORKLOADS[args.workload]
+    if wl.dtype != "bf16":
+        print("bench.py times the bf16 path; %s is an fp32 parity case" % wl.name, file=sys.stderr)
+        return 2
+    binding.load_library()
+    print("[bench] workload %s: generating inputs" % wl.name, file=sys.stderr, flush=True)
+    q, k, v = synth.make_inputs(wl)
+    dev = torch.device("cuda:0")
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    out = torch.empty_like(qd)
+    flops, nbytes = binding.fla_swin_attn_work(wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                               wl.window, wl.shift, wl.pad_mode, wl.elem_bytes)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        binding.fla_swin_attn_fwd(qd, kd, vd, out, wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                  wl.window, wl.shift, wl.pad_mode, stream)
+
+    print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    gpu_ms = ev0.elapsed_time(ev1)
+    us = gpu_ms * 1e3 / args.steps
+    tflops = flops / (us * 1e-6) / 1e12
+    gbs = nbytes / (us * 1e-6) / 1e9
+    assert torch.isfinite(out[:, :64].float()).all()
+
+    traffic = measured_traffic(wl.name)
+    rec = {
+        "metric": "us per Flash-Swin attention layer and TFLOP/s (fraction of MFMA peak)",
+        "value": round(us, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "heads": wl.heads, "grid": [wl.H, wl.W],
+                   "head_dim": wl.head_dim, "window": wl.window, "shift": wl.shift,
+                   "pad_mode": wl.pad_mode, "parallelism": "none (1 GPU)"},
+        "tflops": round(tflops, 2),
+        "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": traffic},
+        "alg_flops": flops,
+        "alg_bytes": nbytes,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -58,8 +58,9 @@ typedef enum {
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
     FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */
-    FLA_ERR_ALIAS = 8,     /* out overlaps q, k or v                                       */
-    FLA_ERR_TOO_LARGE = 9, /* a tensor has 2^40 elements or more, or the grid is too big   */
+    FLA_ERR_TOO_LARGE = 8, /* a tensor has 2^40 elements or more, or the launch would need
+                              2^24 workgroups or more                                      */
+    FLA_ERR_ALIAS = 9,     /* out overlaps q, k or v                                       */
     FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
     FLA_ERR_LAUNCH = 11    /* the HIP runtime refused the kernel launch                    */
 } fla_status;

@@ -1,0 +1,217 @@
+// C ABI of the Flash Swin attention library: argument checks, launch geometry,
+// architecture probe, status strings and algorithmic work counts.
+// The operation and the argument contract are stated in include/fla_swin.h.
+#include "fla_swin.h"
+
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "fla_swin_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxElems = int64_t(1) << 40;
+constexpr int64_t kMaxGroups = (int64_t(1) << 24) - 1;   // grid.x * 256 threads < 2^32
+
+struct Geometry {
+    int origin, nwy, nwx, nqb;
+    int64_t n_groups;
+};
+
+// Windows per axis and the largest window: the canvas has `origin` virtual tokens in
+// front; window i covers canvas [i*window, (i+1)*window) = grid [i*window - origin, ...).
+Geometry geometry(int B, int heads, int H, int W, int window, int shift) {
+    Geometry g;
+    g.origin = (window - shift) % window;
+    const int64_t nwy = (int64_t(H) + g.origin + window - 1) / window;
+    const int64_t nwx = (int64_t(W) + g.origin + window - 1) / window;
+    g.nwy = (int)nwy;
+    g.nwx = (int)nwx;
+    const int64_t max_rows = window < H ? window : H;
+    const int64_t max_cols = window < W ? window : W;
+    const int64_t nmax = max_rows * max_cols;
+    g.nqb = (int)((nmax + fla::kQueryBlock - 1) / fla::kQueryBlock);
+    g.n_groups = int64_t(B) * heads * nwy * nwx * g.nqb;
+    return g;
+}
+
+bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + uint64_t(b_bytes) && b0 < a0 + uint64_t(a_bytes);
+}
+
+// Size checks shared by every entry point.  Returns FLA_OK and sets *empty when there is
+// nothing to compute.
+int check_sizes(int B, int heads, int H, int W, bool* empty) {
+    *empty = false;
+    if (B < 0 || heads < 0 || H < 0 || W < 0) return FLA_ERR_SHAPE;
+    *empty = B == 0 || heads == 0 || H == 0 || W == 0;
+    return FLA_OK;
+}
+
+int check_scalars(int head_dim, int window, int shift, int pad_mode) {
+    if (head_dim != fla::kHeadDim) return FLA_ERR_HEAD_DIM;
+    if (window < 1) return FLA_ERR_WINDOW;
+    if (shift < 0 || shift >= window) return FLA_ERR_SHIFT;
+    if (pad_mode != FLA_PAD_MASK && pad_mode != FLA_PAD_KVTOKEN) return FLA_ERR_PAD_MODE;
+    return FLA_OK;
+}
+
+// 0 = not probed yet, 1 = gfx950, 2 = something else
+std::atomic<int> g_arch_state[64];
+
+int check_arch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+        (void)hipGetLastError();
+        return FLA_ERR_ARCH;
+    }
+    if (dev < 64) {
+        const int st = g_arch_state[dev].load(std::memory_order_acquire);
+        if (st != 0) return st == 1 ? FLA_OK : FLA_ERR_ARCH;
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return FLA_ERR_ARCH;
+    }
+    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (dev < 64) g_arch_state[dev].store(ok ? 1 : 2, std::memory_order_release);
+    return ok ? FLA_OK : FLA_ERR_ARCH;
+}
+
+int forward(const void* q, const void* k, const void* v, void* out, int B, int heads, int H,
+            int W, int head_dim, int window, int shift, int pad_mode, void* stream,
+            int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t)) {
+    bool empty = false;
+    int st = check_sizes(B, heads, H, W, &empty);
+    if (st != FLA_OK || empty) return st;
+    if (!q || !k || !v || !out) return FLA_ERR_NULL;
+    const uintptr_t mis = (reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) |
+                           reinterpret_cast<uintptr_t>(v) | reinterpret_cast<uintptr_t>(out)) & 15u;
+    if (mis) return FLA_ERR_ALIGN;
+    st = check_scalars(head_dim, window, shift, pad_mode);
+    if (st != FLA_OK) return st;
+
+    // sizes, in an order that cannot overflow int64 before the bound check
+    const int64_t L = int64_t(H) * W;
+    const int64_t tok = int64_t(heads) * head_dim;
+    const int64_t kv_rows = L + (pad_mode == FLA_PAD_KVTOKEN ? 1 : 0);
+    if (kv_rows >= kMaxElems || tok >= kMaxElems || kv_rows > kMaxElems / tok) return FLA_ERR_TOO_LARGE;
+    if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
+    const Geometry geo = geometry(B, heads, H, W, window, shift);
+    if (geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
+
+    const int64_t q_bytes = int64_t(B) * L * tok * elem_bytes;
+    const int64_t kv_bytes = int64_t(B) * kv_rows * tok * elem_bytes;
+    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, k, kv_bytes) ||
+        overlaps(out, q_bytes, v, kv_bytes))
+        return FLA_ERR_ALIAS;
+
+    st = check_arch();
+    if (st != FLA_OK) return st;
+
+    fla::SwinArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = out;
+    a.B = B;
+    a.heads = heads;
+    a.H = H;
+    a.W = W;
+    a.window = window;
+    a.shift = shift;
+    a.origin = geo.origin;
+    a.nwy = geo.nwy;
+    a.nwx = geo.nwx;
+    a.nqb = geo.nqb;
+    a.pad_mode = pad_mode;
+    a.tok_stride = tok;
+    a.q_batch_stride = L * tok;
+    a.kv_batch_stride = kv_rows * tok;
+    a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
+    a.n_groups = geo.n_groups;
+    if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
+        (void)hipGetLastError();
+        return FLA_ERR_LAUNCH;
+    }
+    return FLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
+                      int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
+                      void* stream) {
+    return forward(q, k, v, out, B, heads, Hgrid, Wgrid, head_dim, window, shift, pad_mode,
+                   stream, 2, fla::launch_swin_fwd_bf16);
+}
+
+int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
+                          int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                          int pad_mode, void* stream) {
+    return forward(q, k, v, out, B, heads, Hgrid, Wgrid, head_dim, window, shift, pad_mode,
+                   stream, 4, fla::launch_swin_fwd_f32);
+}
+
+const char* fla_status_string(int status) {
+    switch (status) {
+        case FLA_OK: return "ok";
+        case FLA_ERR_SHAPE: return "B, heads, Hgrid and Wgrid must be >= 0";
+        case FLA_ERR_NULL: return "q, k, v and out must be non-NULL";
+        case FLA_ERR_ALIGN: return "q, k, v and out must be 16-byte aligned";
+        case FLA_ERR_HEAD_DIM: return "head_dim must be 64";
+        case FLA_ERR_WINDOW: return "window must be >= 1";
+        case FLA_ERR_SHIFT: return "shift must satisfy 0 <= shift < window";
+        case FLA_ERR_PAD_MODE: return "pad_mode must be FLA_PAD_MASK (0) or FLA_PAD_KVTOKEN (1)";
+        case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements or 2^24 workgroups)";
+        case FLA_ERR_ALIAS: return "out overlaps q, k or v";
+        case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
+        case FLA_ERR_LAUNCH: return "kernel launch failed";
+        default: return "unknown status";
+    }
+}
+
+int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
+                       int shift, int pad_mode, int elem_bytes, double* flops, double* bytes) {
+    bool empty = false;
+    int st = check_sizes(B, heads, Hgrid, Wgrid, &empty);
+    if (st != FLA_OK) return st;
+    if (window < 1) return FLA_ERR_WINDOW;
+    if (shift < 0 || shift >= window) return FLA_ERR_SHIFT;
+    if (pad_mode != FLA_PAD_MASK && pad_mode != FLA_PAD_KVTOKEN) return FLA_ERR_PAD_MODE;
+    if (head_dim < 1 || elem_bytes < 1) return FLA_ERR_HEAD_DIM;
+    double pairs = 0.0;
+    if (!empty) {
+        // window (i, j) holds rows_i * cols_j tokens; rows_i from the canvas geometry
+        const int origin = (window - shift) % window;
+        const int64_t nwy = (int64_t(Hgrid) + origin + window - 1) / window;
+        const int64_t nwx = (int64_t(Wgrid) + origin + window - 1) / window;
+        auto extent = [&](int64_t i, int64_t len) -> double {
+            int64_t s0 = i * window - origin, s1 = s0 + window;
+            if (s0 < 0) s0 = 0;
+            if (s1 > len) s1 = len;
+            return double(s1 - s0);
+        };
+        const double full = double(window) * double(window);
+        for (int64_t i = 0; i < nwy; ++i) {
+            const double a = extent(i, Hgrid);
+            for (int64_t j = 0; j < nwx; ++j) {
+                const double n = a * extent(j, Wgrid);
+                pairs += n * n;
+                if (pad_mode == FLA_PAD_KVTOKEN && n < full) pairs += n;
+            }
+        }
+    }
+    const double rows = empty ? 0.0 : 4.0 * double(Hgrid) * Wgrid + (pad_mode == FLA_PAD_KVTOKEN ? 2.0 : 0.0);
+    if (flops) *flops = 4.0 * head_dim * double(heads) * B * pairs;
+    if (bytes) *bytes = rows * B * double(heads) * head_dim * elem_bytes;
+    return FLA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,190 @@
+"""CPU tests of the C ABI: exported symbols, argument checks, work counts.
+
+No kernel is launched here: every call either fails an argument check before any device
+access, or (with no GPU present) stops at the architecture probe."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import oracle as O
+from paper_2407_02109_amd import binding as fb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fla_swin.h")
+
+
+def _header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fla_\w+)\s*\(", text)))
+
+
+def _header_enum(name):
+    text = open(HEADER).read()
+    return {k: int(v) for k, v in re.findall(r"\b(%s_\w+)\s*=\s*(\d+)" % name, text)}
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fb.library_path()):
+        pytest.skip("libfla_swin.so not built")
+    return fb.load_library()
+
+
+def test_header_declares_the_entry_points():
+    assert _header_functions() == ["fla_status_string", "fla_swin_attn_fwd",
+                                   "fla_swin_attn_fwd_f32", "fla_swin_attn_work"]
+
+
+def test_library_exports_every_header_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", fb.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s+(\w+)", out))
+    for name in _header_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+    # nothing else with the library prefix leaks out
+    assert {s for s in exported if s.startswith("fla_")} == set(_header_functions())
+
+
+def test_status_strings_cover_every_code(lib):
+    codes = _header_enum("FLA")
+    st = {k: v for k, v in codes.items() if k.startswith("FLA_ERR") or k == "FLA_OK"}
+    assert sorted(st.values()) == list(range(len(st)))
+    seen = set()
+    for name, code in st.items():
+        s = fb.fla_status_string(code)
+        assert s and s != "unknown status", name
+        seen.add(s)
+    assert len(seen) == len(st)
+    assert fb.fla_status_string(999) == "unknown status"
+    assert fb.fla_status_string(-1) == "unknown status"
+
+
+# fake, 256-byte aligned, non-overlapping device addresses: never dereferenced on failure
+Q, K, V, OUT = 0x10000000, 0x20000000, 0x30000000, 0x40000000
+GOOD = dict(B=1, heads=12, Hgrid=64, Wgrid=64, head_dim=64, window=16, shift=8, pad_mode=0)
+
+
+def _call(fn, q=Q, k=K, v=V, out=OUT, **kw):
+    a = dict(GOOD)
+    a.update(kw)
+    return fn(q, k, v, out, a["B"], a["heads"], a["Hgrid"], a["Wgrid"], a["head_dim"],
+              a["window"], a["shift"], a["pad_mode"], 0, check=False)
+
+
+CASES = [
+    ("FLA_ERR_SHAPE", dict(B=-1)), ("FLA_ERR_SHAPE", dict(heads=-3)),
+    ("FLA_ERR_SHAPE", dict(Hgrid=-1)), ("FLA_ERR_SHAPE", dict(Wgrid=-64)),
+    ("FLA_ERR_NULL", dict(q=0)), ("FLA_ERR_NULL", dict(k=0)), ("FLA_ERR_NULL", dict(v=0)),
+    ("FLA_ERR_NULL", dict(out=0)),
+    ("FLA_ERR_ALIGN", dict(q=Q + 8)), ("FLA_ERR_ALIGN", dict(out=OUT + 2)),
+    ("FLA_ERR_ALIGN", dict(v=V + 4)), ("FLA_ERR_ALIGN", dict(k=K + 1)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=32)), ("FLA_ERR_HEAD_DIM", dict(head_dim=0)),
+    ("FLA_ERR_WINDOW", dict(window=0)), ("FLA_ERR_WINDOW", dict(window=-4, shift=0)),
+    ("FLA_ERR_SHIFT", dict(shift=16)), ("FLA_ERR_SHIFT", dict(shift=-1)),
+    ("FLA_ERR_SHIFT", dict(window=1, shift=1)),
+    ("FLA_ERR_PAD_MODE", dict(pad_mode=2)), ("FLA_ERR_PAD_MODE", dict(pad_mode=-1)),
+    ("FLA_ERR_TOO_LARGE", dict(Hgrid=1 << 20, Wgrid=1 << 20)),
+    ("FLA_ERR_TOO_LARGE", dict(B=1 << 20, Hgrid=1024, Wgrid=1024)),
+    ("FLA_ERR_TOO_LARGE", dict(B=2**31 - 1, heads=2**31 - 1, Hgrid=2**31 - 1, Wgrid=2**31 - 1)),
+    ("FLA_ERR_ALIAS", dict(out=Q)), ("FLA_ERR_ALIAS", dict(out=Q + 64 * 64 * 12 * 64)),
+    ("FLA_ERR_ALIAS", dict(out=K - 256)), ("FLA_ERR_ALIAS", dict(out=V + 1024)),
+]
+
+
+@pytest.mark.parametrize("fn", [fb.fla_swin_attn_fwd, fb.fla_swin_attn_fwd_f32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("status,kw", CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(CASES)])
+def test_argument_checks(lib, fn, status, kw):
+    codes = _header_enum("FLA")
+    kw = dict(kw)
+    if fn is fb.fla_swin_attn_fwd_f32 and status == "FLA_ERR_ALIAS" and kw.get("out") == Q + 64 * 64 * 12 * 64:
+        kw["out"] = Q + 64 * 64 * 12 * 64 * 2      # still inside q: fp32 elements are 4 bytes
+    assert _call(fn, **kw) == codes[status]
+
+
+def test_first_failing_check_wins(lib):
+    codes = _header_enum("FLA")
+    # NULL and bad shift: NULL is reported (checks run in status-code order)
+    assert _call(fb.fla_swin_attn_fwd, q=0, shift=99) == codes["FLA_ERR_NULL"]
+    # bad head_dim and bad shift: head_dim first
+    assert _call(fb.fla_swin_attn_fwd, head_dim=48, shift=99) == codes["FLA_ERR_HEAD_DIM"]
+    # negative size beats everything
+    assert _call(fb.fla_swin_attn_fwd, B=-1, q=0, head_dim=1) == codes["FLA_ERR_SHAPE"]
+
+
+def test_adjacent_buffers_do_not_alias(lib):
+    n = 1 * 64 * 64 * 12 * 64 * 2
+    st = _call(fb.fla_swin_attn_fwd, q=Q, k=Q + n, v=Q + 2 * n, out=Q + 3 * n)
+    assert st != _header_enum("FLA")["FLA_ERR_ALIAS"]
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(heads=0), dict(Hgrid=0), dict(Wgrid=0, q=0, out=0)])
+def test_empty_problem_is_ok_and_ignores_pointers(lib, kw):
+    kw = dict(kw)
+    kw.setdefault("q", 0)
+    assert _call(fb.fla_swin_attn_fwd, **kw) == 0
+    assert _call(fb.fla_swin_attn_fwd_f32, **kw) == 0
+
+
+def test_kvtoken_alias_range_includes_pad_row(lib):
+    codes = _header_enum("FLA")
+    L = 64 * 64
+    tok = 12 * 64 * 2
+    # k occupies L+1 rows in KV-token mode: out starting right after L rows of k overlaps
+    assert _call(fb.fla_swin_attn_fwd, k=K, out=K + L * tok, pad_mode=1) == codes["FLA_ERR_ALIAS"]
+    assert _call(fb.fla_swin_attn_fwd, k=K, out=K + L * tok, pad_mode=0) != codes["FLA_ERR_ALIAS"]
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_no_device_reports_arch(lib):
+    assert _call(fb.fla_swin_attn_fwd) == _header_enum("FLA")["FLA_ERR_ARCH"]
+    assert _call(fb.fla_swin_attn_fwd_f32) == _header_enum("FLA")["FLA_ERR_ARCH"]
+
+
+@pytest.mark.parametrize("B,heads,H,W,k,s,pm", [
+    (1, 12, 64, 64, 16, 8, 0), (1, 12, 256, 256, 16, 8, 0), (4, 12, 150, 203, 16, 8, 0),
+    (1, 1, 32, 32, 8, 4, 0), (1, 1, 32, 32, 8, 0, 0), (2, 3, 20, 13, 8, 4, 1),
+    (1, 2, 7, 5, 16, 3, 1), (1, 1, 1, 1, 1, 0, 1), (3, 2, 40, 24, 64, 0, 0), (1, 12, 64, 64, 32, 16, 1)])
+def test_work_counts_match_oracle(lib, B, heads, H, W, k, s, pm):
+    for eb in (2, 4):
+        f, b = fb.fla_swin_attn_work(B, heads, H, W, 64, k, s, pm, eb)
+        f0, b0 = O.work_counts(B, heads, H, W, 64, k, s, pm, eb)
+        assert f == f0 and b == b0
+
+
+def test_work_counts_errors(lib):
+    assert lib.fla_swin_attn_work(1, 1, 8, 8, 64, 0, 0, 0, 2, None, None) == _header_enum("FLA")["FLA_ERR_WINDOW"]
+    assert lib.fla_swin_attn_work(1, 1, 8, 8, 64, 4, 4, 0, 2, None, None) == _header_enum("FLA")["FLA_ERR_SHIFT"]
+    assert lib.fla_swin_attn_work(-1, 1, 8, 8, 64, 4, 0, 0, 2, None, None) == _header_enum("FLA")["FLA_ERR_SHAPE"]
+    f = ctypes.c_double(-1)
+    assert lib.fla_swin_attn_work(0, 1, 8, 8, 64, 4, 0, 0, 2, ctypes.byref(f), None) == 0
+    assert f.value == 0.0
+
+
+def test_product_code_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2407_02109_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in text and "from oracle" not in text, fn
+                assert "swin_oracle" not in text, fn
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(fb, "_lib", None)
+    monkeypatch.setattr(fb, "library_path", lambda: str(tmp_path / "libfla_swin.so"))
+    with pytest.raises(fb.FlaError):
+        fb.load_library()
