@@ -58,8 +58,10 @@ typedef enum {
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
     FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */
-    FLA_ERR_TOO_LARGE = 8, /* a tensor has 2^40 elements or more, or the launch would need
-                              2^24 workgroups or more                                      */
+    FLA_ERR_TOO_LARGE = 8, /* a tensor has 2^40 elements or more, the launch would need
+                              2^24 workgroups or more, the rows of one window span 2 GiB or
+                              more (min(window, Hgrid) * Wgrid * heads * head_dim * element
+                              bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
     FLA_ERR_ALIAS = 9,     /* out overlaps q, k or v                                       */
     FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
     FLA_ERR_LAUNCH = 11    /* the HIP runtime refused the kernel launch                    */

@@ -103,6 +103,12 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
     const Geometry geo = geometry(B, heads, H, W, window, shift);
     if (geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    // the kernels address a window with 32-bit byte offsets from its first token, and
+    // split a window-local index into (row, col) with a 32-bit multiply-high
+    const int64_t win_rows = window < H ? window : H;
+    const int64_t win_cols = window < W ? window : W;
+    if (win_rows * W * tok * elem_bytes >= (int64_t(1) << 31)) return FLA_ERR_TOO_LARGE;
+    if (win_rows * win_cols * win_cols > (int64_t(1) << 32)) return FLA_ERR_TOO_LARGE;
 
     const int64_t q_bytes = int64_t(B) * L * tok * elem_bytes;
     const int64_t kv_bytes = int64_t(B) * kv_rows * tok * elem_bytes;
@@ -169,7 +175,7 @@ const char* fla_status_string(int status) {
         case FLA_ERR_WINDOW: return "window must be >= 1";
         case FLA_ERR_SHIFT: return "shift must satisfy 0 <= shift < window";
         case FLA_ERR_PAD_MODE: return "pad_mode must be FLA_PAD_MASK (0) or FLA_PAD_KVTOKEN (1)";
-        case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements or 2^24 workgroups)";
+        case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements, 2^24 workgroups or a 2 GiB window span)";
         case FLA_ERR_ALIAS: return "out overlaps q, k or v";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";

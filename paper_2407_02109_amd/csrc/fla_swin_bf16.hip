@@ -4,22 +4,25 @@
 // window's rectangle comes from integer arithmetic on the shifted-window geometry
 // (HRSAM Sec. 3.3 / App. A): no index table, no reordered copy.  Its real tokens are
 // taken in row-major order inside the rectangle (Eq. nonshift), so the key set is dense:
-// n = rows * cols keys, no masked slots except the MFMA tail of the last key tile.
+// n = rows * cols keys, no masked slots except the tail of the last key tile.
 //
 // Per workgroup:
-//   1. K rows of the window -> LDS row-major (row stride 144 B);
-//      V rows -> LDS transposed (V^T, one row per channel), so that P.V can take V as the
-//      A operand with keys along the reduction dimension.
-//   2. Each of the 4 waves owns 64 queries.  Q stays in registers as the B operand.
-//      For every tile of 64 keys:  S^T = K . Q^T  (v_mfma_f32_16x16x32_bf16, fp32 acc),
-//      scale into the exp2 domain, mask the key tail, online softmax per query column
-//      (cross-lane max over the 4 lane groups), P^T rounded to bf16 stays in registers in
-//      exactly the layout the next MFMA reads as its B operand, O^T += V^T . P^T.
+//   1. K rows of the window -> LDS row-major; V rows -> LDS transposed (V^T, one row per
+//      channel) so that P.V can take V as the A operand with keys along the reduction.
+//   2. Each of the 4 waves owns 64 queries; Q stays in registers as the B operand.
+//      For every tile of 64 keys:  S^T = K . Q^T on v_mfma_f32_32x32x16_bf16 (fp32
+//      accumulation).  Each lane then holds 32 keys of one query column and the partner
+//      lane (l ^ 32) the other 32, so the column max needs one v_permlane32_swap.
+//      p = exp2(s * log2(e)/sqrt(d) - m) is a single FMA + v_exp_f32; P^T is rounded to
+//      bf16 in the exact register layout the next MFMA reads as its B operand, and the
+//      row sum adds the rounded values with v_dot2_f32_bf16.  O^T += V^T . P^T.
+//      The running max is raised only when a tile exceeds it by more than 2^8 (in the
+//      exp2 domain), so the O^T rescale runs on a handful of tiles, not on every one.
 //   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.
 //
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
-// the window and its logit is raised by log2(n_pad), so it carries the weight of the
-// n_pad = window^2 - n virtual slots it stands for.
+// the window and its logit is raised by log2(n_pad)/scale, so in the softmax it carries
+// the weight of the n_pad = window^2 - n virtual slots it stands for.
 #include "fla_swin_internal.h"
 
 namespace fla {
@@ -27,40 +30,150 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 
 constexpr int D = kHeadDim;     // 64 channels per head
 constexpr int THREADS = 256;    // 4 waves of 64
 constexpr int KC = 256;         // keys staged in LDS at a time
 constexpr int KT = 64;          // keys per inner tile
 constexpr int KS = D + 8;       // K row stride in LDS, bf16 elements (144 B)
-constexpr int VS = KC + 8;      // V^T row stride in LDS, bf16 elements (528 B)
+constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
+constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
 
-__device__ __forceinline__ uint4 ld_global16(const uint16_t* p) {
-    return *reinterpret_cast<const uint4*>(p);
+// max / sum over lanes l and l ^ 32 (the two halves holding the same query column)
+__device__ __forceinline__ float xhalf_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ float wave_max_groups(float x) {
-    // max over the 4 lanes {l, l^16, l^32, l^48}: same query column, different key rows
-    x = fmaxf(x, __shfl_xor(x, 16));
-    x = fmaxf(x, __shfl_xor(x, 32));
-    return x;
+// ---- global memory through buffer resources: 32-bit byte offsets from the window's first
+//      token, and hardware range checks (a load outside the resource returns 0, a store
+//      outside it is dropped), so no access can leave the tensor it belongs to.
+constexpr unsigned kOutside = 0x80000000u;   // offset that is always out of range
+constexpr int kMaxRecords = 0x7fffffff;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long long bytes) {
+    const int n = bytes < kMaxRecords ? (int)bytes : kMaxRecords;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, unsigned off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
-__device__ __forceinline__ float wave_sum_groups(float x) {
-    x += __shfl_xor(x, 16);
-    x += __shfl_xor(x, 32);
-    return x;
+// Byte offset of window-local index t (t = row * cols + col, row-major in the window's
+// rectangle) from the window's first token.  row = t / cols is a multiply-high by
+// ceil(2^32 / cols), exact for t * cols < 2^32 (the host guarantees n * cols <= 2^32);
+// cols == 1 uses magic 0 and adds t through one_mask.
+struct WindowAddr {
+    unsigned row_bytes;   // bytes between grid rows: W * heads * head_dim * 2
+    unsigned tok_bytes;   // bytes between adjacent tokens of a row: heads * head_dim * 2
+    unsigned magic, one_mask, cols;
+
+    __device__ __forceinline__ void init(int c, unsigned rowb, unsigned tokb) {
+        cols = (unsigned)c;
+        magic = c > 1 ? (unsigned)(((1ull << 32) + c - 1) / c) : 0u;
+        one_mask = c > 1 ? 0u : 0xffffffffu;
+        row_bytes = rowb;
+        tok_bytes = tokb;
+    }
+    __device__ __forceinline__ unsigned operator()(int t) const {
+        const unsigned r = __umulhi((unsigned)t, magic) + ((unsigned)t & one_mask);
+        const unsigned c = (unsigned)t - r * cols;
+        return r * row_bytes + c * tok_bytes;
+    }
+};
+
+__device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, const uint16_t* __restrict__ Vt,
+                                            bool masked, int t0, int kc0, int nk, int n, float pad_bias_raw,
+                                            const bf16x8 (&qop)[2][4], floatx16 (&o)[2][2],
+                                            float (&m_run)[2], float (&l_run)[2], float c_log2,
+                                            int lane) {
+    const int li = lane & 31;
+    const int h = lane >> 5;
+    // ---- S^T = K . Q^T for 64 keys x 64 queries; s[kb][qb][r] holds
+    //      key 32*kb + 8*(r/4) + 4*h + r%4 of query 32*qb + li
+    floatx16 s[2][2];
+    for (int kb = 0; kb < 2; ++kb) {
+        const uint16_t* krow = Ks + (t0 + 32 * kb + li) * KS + 8 * h;
+        bf16x8 ka[4];
+        for (int st = 0; st < 4; ++st) ka[st] = *reinterpret_cast<const bf16x8*>(krow + 16 * st);
+        for (int qb = 0; qb < 2; ++qb) {
+            floatx16 acc = {};
+            for (int st = 0; st < 4; ++st)
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qop[qb][st], acc, 0, 0, 0);
+            s[kb][qb] = acc;
+        }
+    }
+    if (masked) {   // wave-uniform: only the last tile of a window
+        // keys past the window -> -inf; the pad token gets its multiplicity as a bias
+        for (int kb = 0; kb < 2; ++kb)
+            for (int r = 0; r < 16; ++r) {
+                const int key = kc0 + t0 + 32 * kb + 8 * (r >> 2) + 4 * h + (r & 3);
+                const float bias = key == n ? pad_bias_raw : 0.f;
+                for (int qb = 0; qb < 2; ++qb)
+                    s[kb][qb][r] = key < nk ? s[kb][qb][r] + bias : -INFINITY;
+            }
+    }
+    for (int qb = 0; qb < 2; ++qb) {
+        // ---- column max, lazily folded into the running max
+        float mx = fmaxf(s[0][qb][0], s[1][qb][0]);
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][qb][r], s[1][qb][r]));
+        mx = xhalf_max(mx);
+        const bool raise = mx > m_run[qb] + kLazyThreshold / c_log2;
+        if (__builtin_amdgcn_ballot_w64(raise)) {
+            const float m_new = raise ? mx : m_run[qb];
+            const float alpha = __builtin_amdgcn_exp2f((m_run[qb] - m_new) * c_log2);
+            m_run[qb] = m_new;
+            l_run[qb] *= alpha;
+            for (int db = 0; db < 2; ++db) o[db][qb] *= alpha;
+        }
+        const float neg_mc = -m_run[qb] * c_log2;
+        // ---- p = exp2(s*c - m*c), rounded to bf16 as the B operand of P.V
+        bf16x8 pb[4];
+        for (int sg = 0; sg < 4; ++sg) {
+            const int kb = sg >> 1, r0 = (sg & 1) * 8;
+            bf16x8 v8;
+            for (int j = 0; j < 8; ++j)
+                v8[j] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][r0 + j], c_log2, neg_mc));
+            pb[sg] = v8;
+        }
+        // ---- row sum of the rounded P (what P.V actually weights)
+        const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+        float lsum[4] = {l_run[qb], 0.f, 0.f, 0.f};
+        for (int sg = 0; sg < 4; ++sg)
+            for (int j = 0; j < 8; j += 2) {
+                const bf16x2 pr = {pb[sg][j], pb[sg][j + 1]};
+                lsum[sg] = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum[sg], false);
+            }
+        l_run[qb] = (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
+        // ---- O^T += V^T . P^T; step sg covers keys 16*sg + {0..3, 8..11} + 4*h
+        for (int sg = 0; sg < 4; ++sg) {
+            for (int db = 0; db < 2; ++db) {
+                const uint16_t* vrow = Vt + (32 * db + li) * VS + t0 + 16 * sg + 4 * h;
+                const bf16x4 va = *reinterpret_cast<const bf16x4*>(vrow);
+                const bf16x4 vb = *reinterpret_cast<const bf16x4*>(vrow + 8);
+                const bf16x8 vA = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+                o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pb[sg], o[db][qb], 0, 0, 0);
+            }
+        }
+    }
 }
 
-// 2 waves per SIMD: the register budget (256) matches what the 70 KB of LDS allows (2 workgroups per CU).
+// 2 waves per SIMD: the register budget (256) matches what the LDS footprint allows
+// (2 workgroups per CU).
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void swin_fwd_bf16_kernel(SwinArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * KS];
     __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
 
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
-    //      12 workgroups of one window read adjacent 128-byte pieces of the same rows
+    //      workgroups of one window read adjacent 128-byte pieces of the same token rows
     long long id = blockIdx.x;
     const int head = (int)(id % a.heads);
     id /= a.heads;
@@ -78,177 +191,148 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const long long n_pad = (long long)a.window * a.window - n;
     const bool has_pad = a.pad_mode == 1 && n_pad > 0;
     const int nk = n + (has_pad ? 1 : 0);
-    const float pad_bias = has_pad ? log2f((float)n_pad) : 0.f;
+    const float pad_bias_raw = has_pad ? log2f((float)n_pad) / a.scale_log2 : 0.f;
 
-    const uint16_t* qg = static_cast<const uint16_t*>(a.q) + (long long)b * a.q_batch_stride + head * D;
-    const uint16_t* kg = static_cast<const uint16_t*>(a.k) + (long long)b * a.kv_batch_stride + head * D;
-    const uint16_t* vg = static_cast<const uint16_t*>(a.v) + (long long)b * a.kv_batch_stride + head * D;
-    uint16_t* og = static_cast<uint16_t*>(a.out) + (long long)b * a.q_batch_stride + head * D;
+    // ---- buffer resources based at the window's first token (y0, x0) of head `head`
     const long long L = (long long)a.H * a.W;
+    const long long win_elems = ((long long)wr.y0 * a.W + wr.x0) * a.tok_stride + head * D;
+    const long long q_base = (long long)b * a.q_batch_stride + win_elems;
+    const long long kv_base = (long long)b * a.kv_batch_stride + win_elems;
+    const long long q_total = (long long)a.B * a.q_batch_stride;
+    const long long kv_total = (long long)a.B * a.kv_batch_stride;
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + q_base;
+    const uint16_t* kp = static_cast<const uint16_t*>(a.k) + kv_base;
+    const uint16_t* vp = static_cast<const uint16_t*>(a.v) + kv_base;
+    uint16_t* op = static_cast<uint16_t*>(a.out) + q_base;
+    const __amdgpu_buffer_rsrc_t qr = make_rsrc(qp, (q_total - q_base) * 2);
+    const __amdgpu_buffer_rsrc_t orr = make_rsrc(op, (q_total - q_base) * 2);
+    const __amdgpu_buffer_rsrc_t kr = make_rsrc(kp, (kv_total - kv_base) * 2);
+    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vp, (kv_total - kv_base) * 2);
+    // the pad token of KV-token mode: row L of this batch entry and head, 128 bytes
+    const long long pad_elems = (long long)b * a.kv_batch_stride + L * a.tok_stride + head * D;
+    const __amdgpu_buffer_rsrc_t kpr = make_rsrc(static_cast<const uint16_t*>(a.k) + pad_elems, has_pad ? D * 2 : 0);
+    const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, has_pad ? D * 2 : 0);
 
-    // token row (in elements, relative to the per-(b, head) base) of window-local index t
-    auto token_off = [&](int t) -> long long {
-        if (t >= n) return L * a.tok_stride;          // the pad token (KV-token mode only)
-        const int r = t / wr.cols;
-        const int c = t - r * wr.cols;
-        return ((long long)(wr.y0 + r) * a.W + (wr.x0 + c)) * a.tok_stride;
-    };
+    WindowAddr addr;
+    addr.init(wr.cols, (unsigned)((long long)a.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int g = lane >> 4;        // lane group: MFMA reduction slice / output row quad
-    const int li = lane & 15;       // MFMA row (A) / column (B, output)
+    const int li = lane & 31;
+    const int h = lane >> 5;
 
     const int wq0 = q_begin + wave * 64;
-    const int nq = min(64, n - wq0);   // queries of this wave (<= 0: wave only loads)
+    const int nq = min(64, n - wq0);   // queries of this wave (<= 0: the wave only loads)
 
-    // ---- Q in registers, B-operand layout: lane holds q[query 16*j + li][32*c + 8*g .. +8]
-    bf16x8 qop[4][2];
+    // ---- Q in registers, B-operand layout: lane holds q[query 32*qb + li][16*st + 8*h .. +8]
+    bf16x8 qop[2][4];
     if (nq > 0) {
-        for (int j = 0; j < 4; ++j) {
-            const int t = min(wq0 + 16 * j + li, n - 1);
-            const uint16_t* row = qg + token_off(t);
-            for (int c = 0; c < 2; ++c)
-                qop[j][c] = __builtin_bit_cast(bf16x8, ld_global16(row + 32 * c + 8 * g));
+        for (int qb = 0; qb < 2; ++qb) {
+            const unsigned row = addr(min(wq0 + 32 * qb + li, n - 1));
+            for (int st = 0; st < 4; ++st)
+                qop[qb][st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
         }
     }
 
-    float m_run[4], l_run[4];
-    floatx4 o[4][4];   // O^T: [channel block][query block]
-    for (int j = 0; j < 4; ++j) {
-        m_run[j] = -INFINITY;
-        l_run[j] = 0.f;
-        for (int db = 0; db < 4; ++db) o[db][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
+    float m_run[2] = {-INFINITY, -INFINITY};
+    float l_run[2] = {0.f, 0.f};
+    floatx16 o[2][2];   // O^T: [channel block][query block]
+    for (int db = 0; db < 2; ++db)
+        for (int qb = 0; qb < 2; ++qb) o[db][qb] = floatx16{};
 
     for (int kc0 = 0; kc0 < nk; kc0 += KC) {
         const int ck = min(KC, nk - kc0);
-        const int ck_pad = (ck + KT - 1) / KT * KT;
         if (kc0 > 0) __syncthreads();   // previous chunk fully consumed
 
-        // ---- K chunk -> LDS (row-major).  8 threads per 128-byte row: coalesced.
-        for (int i = tid; i < ck_pad * 8; i += THREADS) {
-            const int key = i >> 3, part = i & 7;
-            uint4 val = make_uint4(0u, 0u, 0u, 0u);
-            if (key < ck) val = ld_global16(kg + token_off(kc0 + key) + part * 8);
-            *reinterpret_cast<uint4*>(&Ks[key * KS + part * 8]) = val;
+        // ---- issue every global load of the chunk before the first LDS write, so a
+        //      workgroup waits for one round trip to HBM, not one per load.
+        //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 32*it.
+        //      V: a thread takes 4 keys x 8 channels (job i = tid + 256*it).
+        uint4 kreg[KC / 32];
+        uint4 vreg[2][4];
+        const int part = tid & 7;
+#pragma unroll
+        for (int it = 0; it < KC / 32; ++it) {
+            const int key = (tid >> 3) + 32 * it;
+            const int t = kc0 + key;   // keys past the window (and the pad slot) read 0
+            kreg[it] = bload16(kr, (t < n ? addr(t) : kOutside) + part * 16);
         }
-        // ---- V chunk -> LDS transposed.  A thread takes 4 keys x 8 channels, swaps
-        //      16-bit halves in registers and writes 8 rows of V^T, 4 keys each.
-        const int n_quads = ck_pad / 4;
-        for (int i = tid; i < n_quads * 8; i += THREADS) {
-            const int quad = (i & 7) + ((i >> 6) << 3);
-            const int part = (i >> 3) & 7;
-            uint4 r[4];
+        const int vpart = (tid >> 3) & 7;
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int quad = (tid & 7) + (((tid >> 6) + 4 * it) << 3);
+#pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int key = quad * 4 + u;
-                r[u] = make_uint4(0u, 0u, 0u, 0u);
-                if (key < ck) r[u] = ld_global16(vg + token_off(kc0 + key) + part * 8);
+                const int t = kc0 + key;
+                vreg[it][u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
             }
-            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&r[0]);
-            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&r[1]);
-            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&r[2]);
-            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&r[3]);
+        }
+        // ---- K -> LDS row-major
+#pragma unroll
+        for (int it = 0; it < KC / 32; ++it) {
+            const int key = (tid >> 3) + 32 * it;
+            *reinterpret_cast<uint4*>(&Ks[key * KS + part * 8]) = kreg[it];
+        }
+        // ---- V -> LDS transposed: swap 16-bit halves of 4 keys in registers and write 8
+        //      rows of V^T (channels vpart*8 .. +7), 4 keys each
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int quad = (tid & 7) + (((tid >> 6) + 4 * it) << 3);
+            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[it][0]);
+            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[it][1]);
+            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[it][2]);
+            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[it][3]);
+#pragma unroll
             for (int m = 0; m < 4; ++m) {
                 uint2 lo, hi;   // channel 2m and 2m+1 of keys quad*4 .. +3
                 lo.x = (w0[m] & 0xffffu) | (w1[m] << 16);
                 lo.y = (w2[m] & 0xffffu) | (w3[m] << 16);
                 hi.x = (w0[m] >> 16) | (w1[m] & 0xffff0000u);
                 hi.y = (w2[m] >> 16) | (w3[m] & 0xffff0000u);
-                const int ch = part * 8 + 2 * m;
+                const int ch = vpart * 8 + 2 * m;
                 *reinterpret_cast<uint2*>(&Vt[ch * VS + quad * 4]) = lo;
                 *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + quad * 4]) = hi;
+            }
+        }
+        if (has_pad && n - kc0 < KC) {
+            // the pad token is key n of the window: its slot was zero-filled above; after
+            // the barrier, 8 threads put its K row and its V^T column in place
+            __syncthreads();
+            const int slot = n - kc0;
+            if (tid < 8) {
+                *reinterpret_cast<uint4*>(&Ks[slot * KS + tid * 8]) = bload16(kpr, tid * 16);
+                const uint4 vv = bload16(vpr, tid * 16);
+                const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
+                for (int e = 0; e < 8; ++e) Vt[(tid * 8 + e) * VS + slot] = ve[e];
             }
         }
         __syncthreads();
 
         if (nq > 0) {
             for (int t0 = 0; t0 < ck; t0 += KT) {
-                // ---- S^T tile: 64 keys x 64 queries, lane holds keys 16*kb + 4*g + r
-                floatx4 s[4][4];
-                for (int kb = 0; kb < 4; ++kb) {
-                    const uint16_t* krow = &Ks[(t0 + 16 * kb + li) * KS + 8 * g];
-                    const bf16x8 ka0 = *reinterpret_cast<const bf16x8*>(krow);
-                    const bf16x8 ka1 = *reinterpret_cast<const bf16x8*>(krow + 32);
-                    for (int j = 0; j < 4; ++j) {
-                        floatx4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            ka0, qop[j][0], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                        s[kb][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka1, qop[j][1], acc, 0, 0, 0);
-                    }
-                }
-                // ---- scale to the exp2 domain, mask keys past the window, pad-token weight
-                const int key_base = kc0 + t0 + 4 * g;
-                for (int kb = 0; kb < 4; ++kb) {
-                    for (int r = 0; r < 4; ++r) {
-                        const int key = key_base + 16 * kb + r;
-                        const bool valid = key < nk;
-                        const float bias = (has_pad && key == n) ? pad_bias : 0.f;
-                        for (int j = 0; j < 4; ++j) {
-                            const float x = s[kb][j][r] * a.scale_log2 + bias;
-                            s[kb][j][r] = valid ? x : -INFINITY;
-                        }
-                    }
-                }
-                // ---- online softmax per query column
-                bf16x8 pb[4][2];
-                for (int j = 0; j < 4; ++j) {
-                    float mx = -INFINITY;
-                    for (int kb = 0; kb < 4; ++kb)
-                        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[kb][j][r]);
-                    mx = wave_max_groups(mx);
-                    const float m_new = fmaxf(m_run[j], mx);   // finite: key 0 of a tile is valid
-                    const float alpha = __builtin_amdgcn_exp2f(m_run[j] - m_new);
-                    m_run[j] = m_new;
-                    l_run[j] *= alpha;
-                    for (int db = 0; db < 4; ++db) o[db][j] *= alpha;
-                    float p[4][4];
-                    float lsum = 0.f;
-                    for (int kb = 0; kb < 4; ++kb)
-                        for (int r = 0; r < 4; ++r) {
-                            p[kb][r] = __builtin_amdgcn_exp2f(s[kb][j][r] - m_new);
-                            lsum += p[kb][r];
-                        }
-                    l_run[j] += lsum;
-                    // B operand of P.V: slots 0..3 = key block 2c, slots 4..7 = key block 2c+1
-                    for (int c = 0; c < 2; ++c) {
-                        bf16x8 v8;
-                        for (int r = 0; r < 4; ++r) {
-                            v8[r] = (__bf16)p[2 * c][r];
-                            v8[4 + r] = (__bf16)p[2 * c + 1][r];
-                        }
-                        pb[j][c] = v8;
-                    }
-                }
-                // ---- O^T += V^T . P^T; A operand: channel 16*db + li, the same 8 keys
-                for (int c = 0; c < 2; ++c) {
-                    for (int db = 0; db < 4; ++db) {
-                        const uint16_t* vrow = &Vt[(16 * db + li) * VS + t0 + 32 * c + 4 * g];
-                        const bf16x4 va = *reinterpret_cast<const bf16x4*>(vrow);
-                        const bf16x4 vb = *reinterpret_cast<const bf16x4*>(vrow + 16);
-                        const bf16x8 vA = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
-                        for (int j = 0; j < 4; ++j)
-                            o[db][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA, pb[j][c], o[db][j], 0, 0, 0);
-                    }
-                }
+                // a tile needs masking only if it runs past the keys or holds the pad token
+                attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run,
+                            l_run, a.scale_log2, lane);
             }
         }
     }
 
-    // ---- epilogue: normalise, round to bf16 (RNE), store at the query's own token
+    // ---- epilogue: normalise, round to bf16 (RNE), store at the query's own token.
+    //      Lane holds channels 32*db + 8*(r/4) + 4*h + r%4 of query 32*qb + li.
     if (nq > 0) {
-        for (int j = 0; j < 4; ++j) {
-            const float l_tot = wave_sum_groups(l_run[j]);
-            const float inv = 1.f / l_tot;
-            const int qi = 16 * j + li;
-            if (qi < nq) {
-                uint16_t* row = og + token_off(wq0 + qi);
-                for (int db = 0; db < 4; ++db) {
+        for (int qb = 0; qb < 2; ++qb) {
+            const float inv = 1.f / xhalf_sum(l_run[qb]);
+            const int qi = 32 * qb + li;
+            const unsigned row = qi < nq ? addr(wq0 + qi) : kOutside;   // tail rows: dropped
+            for (int db = 0; db < 2; ++db)
+                for (int rg = 0; rg < 4; ++rg) {
                     bf16x4 r4;
-                    for (int r = 0; r < 4; ++r) r4[r] = (__bf16)(o[db][j][r] * inv);
-                    *reinterpret_cast<bf16x4*>(row + 16 * db + 4 * g) = r4;
+                    for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][qb][4 * rg + u] * inv);
+                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, r4), orr,
+                                                          row + 2 * (32 * db + 8 * rg + 4 * h), 0, 0);
                 }
-            }
         }
     }
 }

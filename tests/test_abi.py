@@ -91,6 +91,8 @@ CASES = [
     ("FLA_ERR_TOO_LARGE", dict(Hgrid=1 << 20, Wgrid=1 << 20)),
     ("FLA_ERR_TOO_LARGE", dict(B=1 << 20, Hgrid=1024, Wgrid=1024)),
     ("FLA_ERR_TOO_LARGE", dict(B=2**31 - 1, heads=2**31 - 1, Hgrid=2**31 - 1, Wgrid=2**31 - 1)),
+    ("FLA_ERR_TOO_LARGE", dict(Hgrid=4, Wgrid=1 << 21, window=8, shift=0)),   # window rows span 3 GiB
+    ("FLA_ERR_TOO_LARGE", dict(heads=1, Hgrid=2048, Wgrid=2048, window=2048, shift=0)),  # n*cols = 2^33
     ("FLA_ERR_ALIAS", dict(out=Q)), ("FLA_ERR_ALIAS", dict(out=Q + 64 * 64 * 12 * 64)),
     ("FLA_ERR_ALIAS", dict(out=K - 256)), ("FLA_ERR_ALIAS", dict(out=V + 1024)),
 ]
