@@ -52,6 +52,84 @@ def measured_traffic(workload: str):
     return rec.get("bytes_per_launch")
 
 
+def copy_calibration(nbytes: int = 512 << 20, reps: int = 3):
+    """Plain device-to-device copies of a known size, run inside the profiled process so
+    that FETCH_SIZE / WRITE_SIZE can be scaled by what they read for a known byte count."""
+    import torch
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+
+
+def summarize(prof_dir: str, workload: str, command: str):
+    """Turn rocprofv3 CSV output (kernel trace + FETCH_SIZE + WRITE_SIZE passes) into the
+    committed summaries under profiles/: a markdown table and traffic_<workload>.json."""
+    import csv
+    import glob
+    import statistics as st
+
+    def rows(pattern):
+        out = []
+        for path in glob.glob(os.path.join(prof_dir, pattern), recursive=True):
+            with open(path) as f:
+                out.extend(csv.DictReader(f))
+        return out
+
+    trace = rows("trace/**/*kernel_trace.csv")
+    durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace
+            if "swin_fwd_bf16" in r["Kernel_Name"]]
+    stats = rows("trace/**/*kernel_stats.csv")
+    counters = {}
+    copies = {}
+    for name in ("FETCH_SIZE", "WRITE_SIZE"):
+        per_dispatch, per_copy = {}, {}
+        for r in rows("%s/**/*counter_collection.csv" % name.lower()):
+            if r["Counter_Name"] != name:
+                continue
+            key = r["Dispatch_Id"]
+            if "swin_fwd_bf16" in r["Kernel_Name"]:
+                per_dispatch[key] = per_dispatch.get(key, 0.0) + float(r["Counter_Value"])
+            elif "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= 65536:
+                # the 512 MiB calibration copies (small copies elsewhere have tiny grids)
+                per_copy[key] = per_copy.get(key, 0.0) + float(r["Counter_Value"])
+        counters[name] = st.median(per_dispatch.values()) if per_dispatch else None
+        copies[name] = st.median(per_copy.values()) if per_copy else None
+    copy_bytes = 512 << 20
+    fetch_scale = copy_bytes / (copies["FETCH_SIZE"] * 1024) if copies["FETCH_SIZE"] else None
+    write_scale = copy_bytes / (copies["WRITE_SIZE"] * 1024) if copies["WRITE_SIZE"] else None
+    traffic = None
+    if counters["FETCH_SIZE"] and counters["WRITE_SIZE"] and fetch_scale and write_scale:
+        traffic = (counters["FETCH_SIZE"] * 1024 * fetch_scale + counters["WRITE_SIZE"] * 1024 * write_scale)
+    lines = ["# rocprofv3 summary: swin_fwd_bf16_kernel, workload %s" % workload, "",
+             "Command (run from the repository root on the GPU host):", "", "```", command, "```", ""]
+    if durs:
+        lines += ["Kernel trace: %d dispatches, duration avg %.2f us, median %.2f us, min %.2f us, max %.2f us"
+                  % (len(durs), st.mean(durs) / 1e3, st.median(durs) / 1e3, min(durs) / 1e3, max(durs) / 1e3), ""]
+    if stats:
+        lines += ["| kernel | calls | total ns | average ns | percentage |", "|---|---|---|---|---|"]
+        for r in stats:
+            lines.append("| %s | %s | %s | %s | %s |" % (r["Name"][:70], r["Calls"], r["TotalDurationNs"],
+                                                          r["AverageNs"], r["Percentage"]))
+        lines.append("")
+    lines += ["HBM counters (KiB per dispatch, median): FETCH_SIZE %s, WRITE_SIZE %s" % (counters["FETCH_SIZE"], counters["WRITE_SIZE"]),
+              "Copy calibration (512 MiB device copy, KiB per dispatch): FETCH_SIZE %s, WRITE_SIZE %s" % (copies["FETCH_SIZE"], copies["WRITE_SIZE"]),
+              "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (fetch_scale, write_scale),
+              "Traffic per launch (scaled): %s bytes" % (None if traffic is None else int(traffic)),
+              "Kernel source hash: %s" % kernel_hash(), ""]
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", "swin_fwd_bf16_%s.md" % workload), "w") as f:
+        f.write("\n".join(lines))
+    if traffic is not None:
+        with open(os.path.join(ROOT, "profiles", "traffic_%s.json" % workload), "w") as f:
+            json.dump({"workload": workload, "kernel_hash": kernel_hash(), "bytes_per_launch": int(traffic),
+                       "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],
+                       "fetch_scale": fetch_scale, "write_scale": write_scale,
+                       "avg_duration_us": st.mean(durs) / 1e3 if durs else None}, f, indent=1)
+    print("\n".join(lines))
+
+
 def cpu_baseline(wl, q, k, v, budget_s: float):
     """Time the fp64 oracle (textbook Plain Swin form) on this host's cores."""
     import oracle
@@ -93,11 +171,20 @@ def main() -> int:
                     help="img1024 | img2048 | img4096 | ragged150x203 (default: img4096)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run 512 MiB device copies (for scaling HBM counters)")
+    ap.add_argument("--summarize", metavar="PROF_DIR",
+                    help="summarise rocprofv3 CSV output into profiles/ and exit (no GPU needed)")
+    ap.add_argument("--command", default="", help="profiling command recorded by --summarize")
     args = ap.parse_args()
 
+    if args.summarize:
+        summarize(args.summarize, args.workload, args.command)
+        return 0
+
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the Flash Swin layer has no cross-GPU step in "
-              "this build (windows, heads and batch entries are independent); run with --gpus 1",
+        print("bench.py measures one GPU only: a Flash Swin layer needs no cross-GPU step "
+              "(windows, heads and batch entries are independent); run with --gpus 1",
               file=sys.stderr)
         return 2
 
@@ -171,6 +258,8 @@ def main() -> int:
         "alg_flops": flops,
         "alg_bytes": nbytes,
     }
+    if args.copy_calibration:
+        copy_calibration()
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_budget)

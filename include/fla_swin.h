@@ -54,7 +54,7 @@ typedef enum {
     FLA_ERR_SHAPE = 1,     /* B, heads, Hgrid or Wgrid negative                            */
     FLA_ERR_NULL = 2,      /* a pointer is NULL on a non-empty problem                     */
     FLA_ERR_ALIGN = 3,     /* a pointer is not 16-byte aligned                             */
-    FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (this build: 64)                   */
+    FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (supported: 64)                      */
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
     FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */

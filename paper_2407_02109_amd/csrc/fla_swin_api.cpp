@@ -59,26 +59,32 @@ int check_scalars(int head_dim, int window, int shift, int pad_mode) {
     return FLA_OK;
 }
 
-// 0 = not probed yet, 1 = gfx950, 2 = something else
-std::atomic<int> g_arch_state[64];
+// Per-device probe result: 0 = not probed yet, -1 = not gfx950, > 0 = gfx950 with that
+// many compute units.
+std::atomic<int> g_device_cus[64];
 
-int check_arch() {
+int check_arch(int* cus) {
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
         (void)hipGetLastError();
         return FLA_ERR_ARCH;
     }
     if (dev < 64) {
-        const int st = g_arch_state[dev].load(std::memory_order_acquire);
-        if (st != 0) return st == 1 ? FLA_OK : FLA_ERR_ARCH;
+        const int st = g_device_cus[dev].load(std::memory_order_acquire);
+        if (st != 0) {
+            *cus = st;
+            return st > 0 ? FLA_OK : FLA_ERR_ARCH;
+        }
     }
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_ARCH;
     }
-    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-    if (dev < 64) g_arch_state[dev].store(ok ? 1 : 2, std::memory_order_release);
+    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 && prop.multiProcessorCount > 0;
+    const int st = ok ? prop.multiProcessorCount : -1;
+    if (dev < 64) g_device_cus[dev].store(st, std::memory_order_release);
+    *cus = st;
     return ok ? FLA_OK : FLA_ERR_ARCH;
 }
 
@@ -116,7 +122,8 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
         overlaps(out, q_bytes, v, kv_bytes))
         return FLA_ERR_ALIAS;
 
-    st = check_arch();
+    int cus = 0;
+    st = check_arch(&cus);
     if (st != FLA_OK) return st;
 
     fla::SwinArgs a;
@@ -140,6 +147,7 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     a.kv_batch_stride = kv_rows * tok;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
     a.n_groups = geo.n_groups;
+    a.n_cus = cus;
     if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;

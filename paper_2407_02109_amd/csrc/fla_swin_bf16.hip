@@ -18,6 +18,9 @@
 //      row sum adds the rounded values with v_dot2_f32_bf16.  O^T += V^T . P^T.
 //      The running max is raised only when a tile exceeds it by more than 2^8 (in the
 //      exp2 domain), so the O^T rescale runs on a handful of tiles, not on every one.
+//      A wave raises its issue priority (s_setprio) while it issues MFMAs, so that the
+//      two waves sharing a SIMD (two workgroups per CU) drift into opposite phases: one
+//      feeds the matrix cores while the other runs its softmax on the vector ALU.
 //   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.
 //
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
@@ -103,6 +106,9 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         const uint16_t* krow = Ks + (t0 + 32 * kb + li) * KS + 8 * h;
         bf16x8 ka[4];
         for (int st = 0; st < 4; ++st) ka[st] = *reinterpret_cast<const bf16x8*>(krow + 16 * st);
+        // raise this wave's issue priority while it feeds the matrix cores, so that the
+        // other wave on the SIMD runs its softmax (vector ALU) meanwhile
+        __builtin_amdgcn_s_setprio(1);
         for (int qb = 0; qb < 2; ++qb) {
             floatx16 acc = {};
             for (int st = 0; st < 4; ++st)
@@ -110,6 +116,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
             s[kb][qb] = acc;
         }
     }
+    __builtin_amdgcn_s_setprio(0);
     if (masked) {   // wave-uniform: only the last tile of a window
         // keys past the window -> -inf; the pad token gets its multiplicity as a bias
         for (int kb = 0; kb < 2; ++kb)
@@ -152,6 +159,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
                 lsum[sg] = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum[sg], false);
             }
         l_run[qb] = (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
+        __builtin_amdgcn_s_setprio(1);
         // ---- O^T += V^T . P^T; step sg covers keys 16*sg + {0..3, 8..11} + 4*h
         for (int sg = 0; sg < 4; ++sg) {
             for (int db = 0; db < 2; ++db) {
@@ -162,6 +170,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
                 o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pb[sg], o[db][qb], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
     }
 }
 

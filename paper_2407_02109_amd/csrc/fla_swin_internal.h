@@ -6,7 +6,7 @@
 
 namespace fla {
 
-constexpr int kHeadDim = 64;    // head_dim supported by this build
+constexpr int kHeadDim = 64;    // head_dim supported by the kernels
 constexpr int kQueryBlock = 256; // queries of one window handled by one workgroup
 
 // Everything a kernel needs, computed once on the host per call.
@@ -25,7 +25,8 @@ struct SwinArgs {
     int64_t q_batch_stride;     // elements between batch entries of q / out: L * tok_stride
     int64_t kv_batch_stride;    // same for k / v (L or L + 1 rows)
     float scale_log2;           // log2(e) / sqrt(head_dim): logits go straight to exp2
-    int64_t n_groups;           // workgroups in the grid
+    int64_t n_groups;           // workgroups: B * heads * windows * query blocks
+    int n_cus;                  // compute units of the device
 };
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);

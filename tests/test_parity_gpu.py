@@ -1,8 +1,8 @@
 """GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
 
-Tolerances: bf16 max-abs 2e-2 and mean-abs 2e-3; fp32 max-abs 1e-5 (fixed by the
-task's statement of the target; the bf16 bound covers one bf16 rounding of outputs up
-to |o| ~ 8 plus the rounding of P to bf16 before P.V).  Outputs are pre-filled with NaN
+Tolerances: bf16 max-abs 2e-2 and mean-abs 2e-3; fp32 max-abs 1e-5 (the parity target;
+the bf16 bound covers one bf16 rounding of outputs up to |o| ~ 8 plus the rounding of P
+to bf16 before P.V).  Outputs are pre-filled with NaN
 so that an unwritten row fails, and every full-size run is repeated to check that the
 kernel is deterministic (it has no atomics)."""
 import numpy as np
