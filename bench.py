@@ -165,8 +165,9 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=5000,
+                    help="untimed steps first; about half a second of them lets the clocks settle")
     ap.add_argument("--workload", default="img4096",
                     help="img1024 | img2048 | img4096 | ragged150x203 (default: img4096)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

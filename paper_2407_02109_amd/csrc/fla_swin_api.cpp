@@ -148,6 +148,10 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
     a.n_groups = geo.n_groups;
     a.n_cus = cus;
+    a.div_heads = fla::FastDiv::make((unsigned)heads);
+    a.div_nqb = fla::FastDiv::make((unsigned)geo.nqb);
+    a.div_nwin = fla::FastDiv::make((unsigned)(geo.nwy * geo.nwx));
+    a.div_nwx = fla::FastDiv::make((unsigned)geo.nwx);
     if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;

@@ -6,21 +6,22 @@
 // taken in row-major order inside the rectangle (Eq. nonshift), so the key set is dense:
 // n = rows * cols keys, no masked slots except the tail of the last key tile.
 //
-// Per workgroup:
+// Per workgroup (512 threads = 8 waves):
 //   1. K rows of the window -> LDS row-major; V rows -> LDS transposed (V^T, one row per
 //      channel) so that P.V can take V as the A operand with keys along the reduction.
-//   2. Each of the 4 waves owns 64 queries; Q stays in registers as the B operand.
-//      For every tile of 64 keys:  S^T = K . Q^T on v_mfma_f32_32x32x16_bf16 (fp32
-//      accumulation).  Each lane then holds 32 keys of one query column and the partner
-//      lane (l ^ 32) the other 32, so the column max needs one v_permlane32_swap.
+//      Every global load of a 256-key chunk is issued before the first LDS write.
+//   2. Each wave owns 32 queries; Q stays in registers as the B operand.
+//      For every tile of 32 keys:  S^T = K . Q^T on v_mfma_f32_32x32x16_bf16 (fp32
+//      accumulation).  Each lane then holds 16 keys of one query column and the partner
+//      lane (l ^ 32) the other 16, so the column max needs one v_permlane32_swap.
 //      p = exp2(s * log2(e)/sqrt(d) - m) is a single FMA + v_exp_f32; P^T is rounded to
 //      bf16 in the exact register layout the next MFMA reads as its B operand, and the
 //      row sum adds the rounded values with v_dot2_f32_bf16.  O^T += V^T . P^T.
 //      The running max is raised only when a tile exceeds it by more than 2^8 (in the
 //      exp2 domain), so the O^T rescale runs on a handful of tiles, not on every one.
-//      A wave raises its issue priority (s_setprio) while it issues MFMAs, so that the
-//      two waves sharing a SIMD (two workgroups per CU) drift into opposite phases: one
-//      feeds the matrix cores while the other runs its softmax on the vector ALU.
+//      The kernel is held to 128 VGPRs so that 4 waves share each SIMD (2 workgroups per
+//      CU): while one wave waits on the matrix core, another runs its softmax on the
+//      vector ALU, which is the busier of the two units.
 //   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.
 //
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
@@ -38,9 +39,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef int v2i __attribute__((ext_vector_type(2)));
 
 constexpr int D = kHeadDim;     // 64 channels per head
-constexpr int THREADS = 256;    // 4 waves of 64
+constexpr int THREADS = 512;    // 8 waves of 64
+constexpr int QW = 32;          // queries per wave
 constexpr int KC = 256;         // keys staged in LDS at a time
-constexpr int KT = 64;          // keys per inner tile
+constexpr int KT = 32;          // keys per inner tile
 constexpr int KS = D + 8;       // K row stride in LDS, bf16 elements (144 B)
 constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
 constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
@@ -94,103 +96,83 @@ struct WindowAddr {
 
 __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, const uint16_t* __restrict__ Vt,
                                             bool masked, int t0, int kc0, int nk, int n, float pad_bias_raw,
-                                            const bf16x8 (&qop)[2][4], floatx16 (&o)[2][2],
-                                            float (&m_run)[2], float (&l_run)[2], float c_log2,
-                                            int lane) {
+                                            const bf16x8 (&qop)[4], floatx16 (&o)[2],
+                                            float& m_run, float& l_run, float c_log2, int lane) {
     const int li = lane & 31;
     const int h = lane >> 5;
-    // ---- S^T = K . Q^T for 64 keys x 64 queries; s[kb][qb][r] holds
-    //      key 32*kb + 8*(r/4) + 4*h + r%4 of query 32*qb + li
-    floatx16 s[2][2];
-    for (int kb = 0; kb < 2; ++kb) {
-        const uint16_t* krow = Ks + (t0 + 32 * kb + li) * KS + 8 * h;
-        bf16x8 ka[4];
-        for (int st = 0; st < 4; ++st) ka[st] = *reinterpret_cast<const bf16x8*>(krow + 16 * st);
-        // raise this wave's issue priority while it feeds the matrix cores, so that the
-        // other wave on the SIMD runs its softmax (vector ALU) meanwhile
-        __builtin_amdgcn_s_setprio(1);
-        for (int qb = 0; qb < 2; ++qb) {
-            floatx16 acc = {};
-            for (int st = 0; st < 4; ++st)
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[st], qop[qb][st], acc, 0, 0, 0);
-            s[kb][qb] = acc;
+    // ---- S^T = K . Q^T for 32 keys x 32 queries: s[r] holds key 8*(r/4) + 4*h + r%4
+    //      of query li
+    const uint16_t* krow = Ks + (t0 + li) * KS + 8 * h;
+    floatx16 s = {};
+    for (int st = 0; st < 4; ++st)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * st),
+                                                    qop[st], s, 0, 0, 0);
+    if (masked) {
+        // entry r holds key base + 8*(r/4) + r%4 with base = kc0 + t0 + 4*h
+        const int lim = nk - (kc0 + t0 + 4 * h);    // entries below lim are keys of the window
+        const int pad = n - (kc0 + t0 + 4 * h);     // the entry that is the pad token (if any)
+        for (int r = 0; r < 16; ++r) {
+            const int off = 8 * (r >> 2) + (r & 3);
+            const float x = off == pad ? s[r] + pad_bias_raw : s[r];
+            s[r] = off < lim ? x : -INFINITY;
         }
     }
-    __builtin_amdgcn_s_setprio(0);
-    if (masked) {   // wave-uniform: only the last tile of a window
-        // keys past the window -> -inf; the pad token gets its multiplicity as a bias
-        for (int kb = 0; kb < 2; ++kb)
-            for (int r = 0; r < 16; ++r) {
-                const int key = kc0 + t0 + 32 * kb + 8 * (r >> 2) + 4 * h + (r & 3);
-                const float bias = key == n ? pad_bias_raw : 0.f;
-                for (int qb = 0; qb < 2; ++qb)
-                    s[kb][qb][r] = key < nk ? s[kb][qb][r] + bias : -INFINITY;
-            }
+    float mx = fmaxf(s[0], s[1]);
+    for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(s[r], s[r + 1]));
+    mx = xhalf_max(mx);
+    const bool raise = mx > m_run + kLazyThreshold / c_log2;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+        const float m_new = raise ? mx : m_run;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
+        m_run = m_new;
+        l_run *= alpha;
+        o[0] *= alpha;
+        o[1] *= alpha;
     }
-    for (int qb = 0; qb < 2; ++qb) {
-        // ---- column max, lazily folded into the running max
-        float mx = fmaxf(s[0][qb][0], s[1][qb][0]);
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][qb][r], s[1][qb][r]));
-        mx = xhalf_max(mx);
-        const bool raise = mx > m_run[qb] + kLazyThreshold / c_log2;
-        if (__builtin_amdgcn_ballot_w64(raise)) {
-            const float m_new = raise ? mx : m_run[qb];
-            const float alpha = __builtin_amdgcn_exp2f((m_run[qb] - m_new) * c_log2);
-            m_run[qb] = m_new;
-            l_run[qb] *= alpha;
-            for (int db = 0; db < 2; ++db) o[db][qb] *= alpha;
-        }
-        const float neg_mc = -m_run[qb] * c_log2;
-        // ---- p = exp2(s*c - m*c), rounded to bf16 as the B operand of P.V
-        bf16x8 pb[4];
-        for (int sg = 0; sg < 4; ++sg) {
-            const int kb = sg >> 1, r0 = (sg & 1) * 8;
-            bf16x8 v8;
-            for (int j = 0; j < 8; ++j)
-                v8[j] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][qb][r0 + j], c_log2, neg_mc));
-            pb[sg] = v8;
-        }
-        // ---- row sum of the rounded P (what P.V actually weights)
-        const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
-        float lsum[4] = {l_run[qb], 0.f, 0.f, 0.f};
-        for (int sg = 0; sg < 4; ++sg)
-            for (int j = 0; j < 8; j += 2) {
-                const bf16x2 pr = {pb[sg][j], pb[sg][j + 1]};
-                lsum[sg] = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum[sg], false);
-            }
-        l_run[qb] = (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
-        __builtin_amdgcn_s_setprio(1);
-        // ---- O^T += V^T . P^T; step sg covers keys 16*sg + {0..3, 8..11} + 4*h
-        for (int sg = 0; sg < 4; ++sg) {
-            for (int db = 0; db < 2; ++db) {
-                const uint16_t* vrow = Vt + (32 * db + li) * VS + t0 + 16 * sg + 4 * h;
-                const bf16x4 va = *reinterpret_cast<const bf16x4*>(vrow);
-                const bf16x4 vb = *reinterpret_cast<const bf16x4*>(vrow + 8);
-                const bf16x8 vA = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
-                o[db][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pb[sg], o[db][qb], 0, 0, 0);
-            }
-        }
-        __builtin_amdgcn_s_setprio(0);
+    const float neg_mc = -m_run * c_log2;
+    bf16x8 pb[2];
+    for (int sg = 0; sg < 2; ++sg) {
+        bf16x8 v8;
+        for (int j = 0; j < 8; ++j)
+            v8[j] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * sg + j], c_log2, neg_mc));
+        pb[sg] = v8;
     }
+    const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+    float l0 = l_run, l1 = 0.f;
+    for (int j = 0; j < 8; j += 2) {
+        l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[0][j], pb[0][j + 1]}, ones, l0, false);
+        l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[1][j], pb[1][j + 1]}, ones, l1, false);
+    }
+    l_run = l0 + l1;
+    for (int sg = 0; sg < 2; ++sg)
+        for (int db = 0; db < 2; ++db) {
+            const uint16_t* vrow = Vt + (32 * db + li) * VS + t0 + 16 * sg + 4 * h;
+            const bf16x4 va = *reinterpret_cast<const bf16x4*>(vrow);
+            const bf16x4 vb = *reinterpret_cast<const bf16x4*>(vrow + 8);
+            const bf16x8 vA = {va[0], va[1], va[2], va[3], vb[0], vb[1], vb[2], vb[3]};
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vA, pb[sg], o[db], 0, 0, 0);
+        }
 }
 
-// 2 waves per SIMD: the register budget (256) matches what the LDS footprint allows
-// (2 workgroups per CU).
-__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// 4 waves per SIMD: at most 128 VGPRs, and the LDS footprint (2 x 69 KB) admits the two
+// workgroups per CU that this takes.
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void swin_fwd_bf16_kernel(SwinArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * KS];
     __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
 
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
-    //      workgroups of one window read adjacent 128-byte pieces of the same token rows
-    long long id = blockIdx.x;
-    const int head = (int)(id % a.heads);
-    id /= a.heads;
-    const int qblk = (int)(id % a.nqb);
-    id /= a.nqb;
+    //      workgroups of one window read adjacent 128-byte pieces of the same token rows.
+    //      The divisions are multiply-high by constants the host prepared.
+    const unsigned id0 = blockIdx.x;
+    const unsigned id1 = a.div_heads.div(id0);
+    const int head = (int)(id0 - id1 * (unsigned)a.heads);
+    const unsigned id2 = a.div_nqb.div(id1);
+    const int qblk = (int)(id1 - id2 * (unsigned)a.nqb);
     const int nwin = a.nwy * a.nwx;
-    const int win = (int)(id % nwin);
-    const int b = (int)(id / nwin);
+    const unsigned id3 = a.div_nwin.div(id2);
+    const int win = (int)(id2 - id3 * (unsigned)nwin);
+    const int b = (int)id3;
 
     const WindowRect wr = window_rect(a, win);
     const int n = wr.rows * wr.cols;
@@ -231,24 +213,19 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const int li = lane & 31;
     const int h = lane >> 5;
 
-    const int wq0 = q_begin + wave * 64;
-    const int nq = min(64, n - wq0);   // queries of this wave (<= 0: the wave only loads)
+    const int wq0 = q_begin + wave * QW;
+    const int nq = min(QW, n - wq0);   // queries of this wave (<= 0: the wave only loads)
 
-    // ---- Q in registers, B-operand layout: lane holds q[query 32*qb + li][16*st + 8*h .. +8]
-    bf16x8 qop[2][4];
+    // ---- Q in registers, B-operand layout: lane holds q[query li][16*st + 8*h .. +8]
+    bf16x8 qop[4];
     if (nq > 0) {
-        for (int qb = 0; qb < 2; ++qb) {
-            const unsigned row = addr(min(wq0 + 32 * qb + li, n - 1));
-            for (int st = 0; st < 4; ++st)
-                qop[qb][st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
-        }
+        const unsigned row = addr(min(wq0 + li, n - 1));
+        for (int st = 0; st < 4; ++st)
+            qop[st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
     }
 
-    float m_run[2] = {-INFINITY, -INFINITY};
-    float l_run[2] = {0.f, 0.f};
-    floatx16 o[2][2];   // O^T: [channel block][query block]
-    for (int db = 0; db < 2; ++db)
-        for (int qb = 0; qb < 2; ++qb) o[db][qb] = floatx16{};
+    float m_run = -INFINITY, l_run = 0.f;
+    floatx16 o[2] = {floatx16{}, floatx16{}};   // O^T: [channel block]
 
     for (int kc0 = 0; kc0 < nk; kc0 += KC) {
         const int ck = min(KC, nk - kc0);
@@ -256,46 +233,36 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
         // ---- issue every global load of the chunk before the first LDS write, so a
         //      workgroup waits for one round trip to HBM, not one per load.
-        //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 32*it.
-        //      V: a thread takes 4 keys x 8 channels (job i = tid + 256*it).
-        uint4 kreg[KC / 32];
-        uint4 vreg[2][4];
+        //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 64*it.
+        //      V: a thread takes 4 consecutive keys (quad) x 8 channels (vpart) and writes
+        //      them transposed: 4 keys of one channel are one 8-byte LDS store.
+        uint4 kreg[KC / 64];
+        uint4 vreg[4];
         const int part = tid & 7;
 #pragma unroll
-        for (int it = 0; it < KC / 32; ++it) {
-            const int key = (tid >> 3) + 32 * it;
-            const int t = kc0 + key;   // keys past the window (and the pad slot) read 0
+        for (int it = 0; it < KC / 64; ++it) {
+            const int key = (tid >> 3) + 64 * it;
+            const int t = kc0 + key;
             kreg[it] = bload16(kr, (t < n ? addr(t) : kOutside) + part * 16);
         }
         const int vpart = (tid >> 3) & 7;
+        const int quad = (tid & 7) + ((tid >> 6) << 3);
 #pragma unroll
-        for (int it = 0; it < 2; ++it) {
-            const int quad = (tid & 7) + (((tid >> 6) + 4 * it) << 3);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int key = quad * 4 + u;
-                const int t = kc0 + key;
-                vreg[it][u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
-            }
+        for (int u = 0; u < 4; ++u) {
+            const int t = kc0 + quad * 4 + u;
+            vreg[u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
         }
-        // ---- K -> LDS row-major
 #pragma unroll
-        for (int it = 0; it < KC / 32; ++it) {
-            const int key = (tid >> 3) + 32 * it;
-            *reinterpret_cast<uint4*>(&Ks[key * KS + part * 8]) = kreg[it];
-        }
-        // ---- V -> LDS transposed: swap 16-bit halves of 4 keys in registers and write 8
-        //      rows of V^T (channels vpart*8 .. +7), 4 keys each
-#pragma unroll
-        for (int it = 0; it < 2; ++it) {
-            const int quad = (tid & 7) + (((tid >> 6) + 4 * it) << 3);
-            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[it][0]);
-            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[it][1]);
-            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[it][2]);
-            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[it][3]);
+        for (int it = 0; it < KC / 64; ++it)
+            *reinterpret_cast<uint4*>(&Ks[((tid >> 3) + 64 * it) * KS + part * 8]) = kreg[it];
+        {
+            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
+            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
+            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
+            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-                uint2 lo, hi;   // channel 2m and 2m+1 of keys quad*4 .. +3
+                uint2 lo, hi;
                 lo.x = (w0[m] & 0xffffu) | (w1[m] << 16);
                 lo.y = (w2[m] & 0xffffu) | (w3[m] << 16);
                 hi.x = (w0[m] >> 16) | (w1[m] & 0xffff0000u);
@@ -331,18 +298,15 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     // ---- epilogue: normalise, round to bf16 (RNE), store at the query's own token.
     //      Lane holds channels 32*db + 8*(r/4) + 4*h + r%4 of query 32*qb + li.
     if (nq > 0) {
-        for (int qb = 0; qb < 2; ++qb) {
-            const float inv = 1.f / xhalf_sum(l_run[qb]);
-            const int qi = 32 * qb + li;
-            const unsigned row = qi < nq ? addr(wq0 + qi) : kOutside;   // tail rows: dropped
-            for (int db = 0; db < 2; ++db)
-                for (int rg = 0; rg < 4; ++rg) {
-                    bf16x4 r4;
-                    for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][qb][4 * rg + u] * inv);
-                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, r4), orr,
-                                                          row + 2 * (32 * db + 8 * rg + 4 * h), 0, 0);
-                }
-        }
+        const float inv = 1.f / xhalf_sum(l_run);
+        const unsigned row = li < nq ? addr(wq0 + li) : kOutside;   // tail rows: dropped
+        for (int db = 0; db < 2; ++db)
+            for (int rg = 0; rg < 4; ++rg) {
+                bf16x4 r4;
+                for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][4 * rg + u] * inv);
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, r4), orr,
+                                                      row + 2 * (32 * db + 8 * rg + 4 * h), 0, 0);
+            }
     }
 }
 

@@ -6,6 +6,27 @@
 
 namespace fla {
 
+__host__ __device__ inline unsigned mulhi_u32(unsigned a, unsigned b) {
+    return (unsigned)(((unsigned long long)a * b) >> 32);
+}
+
+// Unsigned division by a divisor fixed at launch, exact for every n < 2^31.  Powers of two
+// shift; otherwise q = mulhi(n, m) >> s with s = floor(log2 d) and m = ceil(2^(32+s) / d)
+// (Granlund & Montgomery, 1994): m = 2^(32+s)/d + e with 0 <= e < 1, and the error term
+// n*e / 2^(32+s) stays below 1/d while n < 2^(32+s)/d, which exceeds 2^31.
+struct FastDiv {
+    unsigned m, s;
+    __host__ __device__ unsigned div(unsigned n) const { return (m ? mulhi_u32(n, m) : n) >> s; }
+    static __host__ FastDiv make(unsigned d) {
+        FastDiv f;
+        unsigned s = 0;
+        while ((2ull << s) <= d) ++s;   // s = floor(log2 d)
+        f.s = s;
+        f.m = (d & (d - 1)) == 0 ? 0u : (unsigned)((((unsigned long long)1 << (32 + s)) + d - 1) / d);
+        return f;
+    }
+};
+
 constexpr int kHeadDim = 64;    // head_dim supported by the kernels
 constexpr int kQueryBlock = 256; // queries of one window handled by one workgroup
 
@@ -27,6 +48,7 @@ struct SwinArgs {
     float scale_log2;           // log2(e) / sqrt(head_dim): logits go straight to exp2
     int64_t n_groups;           // workgroups: B * heads * windows * query blocks
     int n_cus;                  // compute units of the device
+    FastDiv div_heads, div_nqb, div_nwin, div_nwx;   // workgroup index decode
 };
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
@@ -38,7 +60,7 @@ struct WindowRect {
 };
 
 __device__ __forceinline__ WindowRect window_rect(const SwinArgs& a, int win) {
-    const int wy = win / a.nwx;
+    const int wy = (int)a.div_nwx.div((unsigned)win);
     const int wx = win - wy * a.nwx;
     const long long ys = (long long)wy * a.window - a.origin;
     const long long xs = (long long)wx * a.window - a.origin;
