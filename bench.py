@@ -14,6 +14,7 @@ on this host as a baseline.
 from __future__ import annotations
 
 import argparse
+import collections
 import hashlib
 import json
 import os
@@ -77,9 +78,12 @@ def summarize(prof_dir: str, workload: str, command: str):
                 out.extend(csv.DictReader(f))
         return out
 
-    trace = rows("trace/**/*kernel_trace.csv")
-    durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace
-            if "swin_fwd_bf16" in r["Kernel_Name"]]
+    trace = [r for r in rows("trace/**/*kernel_trace.csv") if "swin_fwd_bf16" in r["Kernel_Name"]]
+    # the workload's own launches: the most common grid (the bench also times a one-token
+    # launch of the same kernel, for the launch overhead)
+    grids = collections.Counter(r["Grid_Size_X"] for r in trace)
+    main_grid = grids.most_common(1)[0][0] if grids else None
+    durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace if r["Grid_Size_X"] == main_grid]
     stats = rows("trace/**/*kernel_stats.csv")
     counters = {}
     copies = {}
@@ -160,6 +164,48 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
             "sample": "fp64 textbook oracle on %d of %d heads of the %s layer, median of 3, "
                       "scaled to the whole layer; host %s with %d usable cores"
                       % (use_heads, heads, wl.name, os.uname().machine, len(os.sched_getaffinity(0)))}
+
+
+def device_info(torch) -> dict:
+    """Name, architecture and compute units as the runtime reports them, and the engine
+    clock range from sysfs when it is readable."""
+    p = torch.cuda.get_device_properties(0)
+    info = {"name": p.name, "arch": getattr(p, "gcnArchName", ""), "cus": p.multi_processor_count}
+    try:
+        import glob
+        for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+            with open(path) as f:
+                mhz = [int(t.split(":")[1].strip().lower().split("mhz")[0]) for t in f.read().splitlines() if ":" in t]
+            if mhz:
+                info["sclk_mhz_max"] = max(mhz)
+                break
+    except (OSError, ValueError, IndexError):
+        pass
+    return info
+
+
+def percentiles(xs):
+    xs = sorted(xs)
+    pick = lambda f: xs[min(len(xs) - 1, int(f * len(xs)))]
+    return round(pick(0.10), 3), round(pick(0.50), 3), round(pick(0.90), 3)
+
+
+def per_call_us(step, stream, calls: int, before=None):
+    """Duration of single calls, each bracketed by its own pair of events on the stream;
+    `before` (e.g. a cache flush) runs ahead of each call, outside its events."""
+    import torch
+    out = []
+    for _ in range(calls):
+        if before is not None:
+            before()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        e1.synchronize()
+        out.append(e0.elapsed_time(e1) * 1e3)
+    return out
 
 
 def main() -> int:
@@ -259,6 +305,22 @@ def main() -> int:
         "alg_flops": flops,
         "alg_bytes": nbytes,
     }
+    # distribution of single warm calls, cold calls (L2 and the 256 MB MALL flushed by a
+    # 1 GiB write before each), and the cost of a launch on a one-token problem
+    p10, p50, p90 = percentiles(per_call_us(step, stream, 200))
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    c10, c50, c90 = percentiles(per_call_us(step, stream, 50, before=lambda: flush.random_(0, 255)))
+    del flush
+    tq = torch.zeros(1, 1, 1, wl.head_dim, dtype=torch.bfloat16, device=dev)
+    tout = torch.empty_like(tq)
+    tiny = lambda: binding.fla_swin_attn_fwd(tq, tq, tq, tout, 1, 1, 1, 1, wl.head_dim, wl.window, 0,
+                                             0, stream)
+    l10, l50, l90 = percentiles(per_call_us(tiny, stream, 200))
+    torch.cuda.synchronize()
+    rec["timing"] = {"warm_mean_us": round(us, 3), "warm_p10_us": p10, "warm_p50_us": p50, "warm_p90_us": p90,
+                     "cold_p10_us": c10, "cold_p50_us": c50, "cold_p90_us": c90,
+                     "launch_one_token_p50_us": l50}
+    rec["device"] = device_info(torch)
     if args.copy_calibration:
         copy_calibration()
     if not args.no_cpu_baseline:

@@ -22,7 +22,10 @@
 //      The kernel is held to 128 VGPRs so that 4 waves share each SIMD (2 workgroups per
 //      CU): while one wave waits on the matrix core, another runs its softmax on the
 //      vector ALU, which is the busier of the two units.
-//   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.
+//   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.  The
+//      result goes through LDS first so that every store writes whole 128-byte rows (8 lanes
+//      x 16 B): stored straight from the MFMA layout, each instruction would write 8-byte
+//      pieces of 32 rows, and those partial-line writes cost about a tenth of the layer.
 //
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
 // the window and its logit is raised by log2(n_pad)/scale, so in the softmax it carries
@@ -37,6 +40,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef int v2i __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int D = kHeadDim;     // 64 channels per head
 constexpr int THREADS = 512;    // 8 waves of 64
@@ -295,18 +299,27 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         }
     }
 
-    // ---- epilogue: normalise, round to bf16 (RNE), store at the query's own token.
-    //      Lane holds channels 32*db + 8*(r/4) + 4*h + r%4 of query 32*qb + li.
+    // ---- epilogue: normalise, round to bf16 (RNE), and store each query row at its own
+    //      token.  The wave's 32 x 64 result is staged in LDS (in the K tile, free once every
+    //      wave is past its last tile) so that the stores are whole 128-byte rows: 8 lanes
+    //      per row, 16 bytes per lane.
+    __syncthreads();
     if (nq > 0) {
         const float inv = 1.f / xhalf_sum(l_run);
-        const unsigned row = li < nq ? addr(wq0 + li) : kOutside;   // tail rows: dropped
+        uint16_t* orow = Ks + (wave * QW + li) * KS;
         for (int db = 0; db < 2; ++db)
             for (int rg = 0; rg < 4; ++rg) {
                 bf16x4 r4;
                 for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][4 * rg + u] * inv);
-                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2i, r4), orr,
-                                                      row + 2 * (32 * db + 8 * rg + 4 * h), 0, 0);
+                *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * rg + 4 * h) = r4;
             }
+        const int part = lane & 7;
+        for (int i = 0; i < QW / 8; ++i) {
+            const int r = 8 * i + (lane >> 3);
+            const uint4 v = *reinterpret_cast<const uint4*>(Ks + (wave * QW + r) * KS + 8 * part);
+            const unsigned off = r < nq ? addr(wq0 + r) + 16 * part : kOutside;   // tail rows: dropped
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orr, off, 0, 0);
+        }
     }
 }
 

@@ -65,6 +65,10 @@ WORKLOADS = {
     "img4096": Workload("img4096", 1, 12, 256, 256, 64, 16, 8, "bf16", seed=3, stress_keys=0.01,
                         note="4096^2 image: 256x256 tokens, 12 heads x 64, window 16, shift 8, "
                              "1% of key rows x8"),
+    "img4096_kv": Workload("img4096_kv", 1, 12, 256, 256, 64, 16, 8, "bf16", seed=3, stress_keys=0.01,
+                           pad_mode=PAD_KVTOKEN,
+                           note="img4096 with KV-only padding: border windows attend the pad token "
+                                "(row L of k and v) with multiplicity window^2 - n"),
     "ragged150x203": Workload("ragged150x203", 4, 12, 150, 203, 64, 16, 8, "bf16", seed=4,
                               note="non-divisible 150x203 grid, B=4, 12 heads x 64, window 16, "
                                    "shift 8, padded keys masked"),

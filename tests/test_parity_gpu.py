@@ -116,8 +116,10 @@ def test_workload_full_size(name):
     print("[result] %s max %.3e mean %.3e" % (name, mx, mean), flush=True)
 
 
-@pytest.mark.parametrize("name", ["img1024", "ragged150x203"])
+@pytest.mark.parametrize("name", ["img1024", "ragged150x203", "img4096_kv"])
 def test_workload_kvtoken(name):
+    """KV-only padding at full size, in the launch configuration the bench times; sampled
+    queries (the oracle computes them one by one) include every border window kind."""
     wl = synth.WORKLOADS[name].with_(pad_mode=1)
     _say(name + " kvtoken")
     q, k, v = synth.make_inputs(wl)
