@@ -5,7 +5,8 @@ TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check in
 The GPU library never imports it and shares no code, table or helper with it.
 
 Every function here is a slow, obviously-correct restatement of the paper's
-definitions in float64 NumPy; see ``swin_oracle`` for the four forms.
+definitions in float64 NumPy; see ``swin_oracle`` for the four single-grid forms and
+``multiscale`` for the multi-scale (several grids in one sequence) forms of App. C.
 """
 from .swin_oracle import (  # noqa: F401
     PAD_MASK,
@@ -19,4 +20,13 @@ from .swin_oracle import (  # noqa: F401
     fla_kv_padding_indices,
     window_sizes,
     work_counts,
+)
+from .multiscale import (  # noqa: F401
+    grid_offsets,
+    ms_kv_padding_indices,
+    ms_shift_window_indices,
+    ms_work_counts,
+    swin_attention_ms,
+    swin_attention_ms_at,
+    swin_attention_ms_fla,
 )
