@@ -147,17 +147,23 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
     # subset of heads (every head is the same amount of work), scaled to a layer
     heads = wl.heads
     q64, k64, v64 = (synth.to_f64_numpy(t) for t in (q, k, v))
+
+    def layer(nh):
+        if wl.grids:
+            oracle.swin_attention_ms(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], list(wl.grid_list),
+                                     wl.window, wl.shift, wl.pad_mode)
+        else:
+            oracle.swin_attention_textbook(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh],
+                                           wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
+
     t0 = time.perf_counter()
-    oracle.swin_attention_textbook(q64[:, :, :1], k64[:, :, :1], v64[:, :, :1],
-                                   wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
+    layer(1)
     per_head = time.perf_counter() - t0
     use_heads = int(max(1, min(heads, budget_s / 3.0 / max(per_head, 1e-6))))
     times = []
     while len(times) < 3:
         t0 = time.perf_counter()
-        oracle.swin_attention_textbook(q64[:, :, :use_heads], k64[:, :, :use_heads],
-                                       v64[:, :, :use_heads], wl.H, wl.W, wl.window, wl.shift,
-                                       wl.pad_mode)
+        layer(use_heads)
         times.append((time.perf_counter() - t0) * heads / use_heads)
     return {"value": statistics.median(times) * 1e6, "unit": "us/layer", "cores": int(threads),
             "kind": "oracle",
@@ -215,7 +221,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5000,
                     help="untimed steps first; about half a second of them lets the clocks settle")
     ap.add_argument("--workload", default="img4096",
-                    help="img1024 | img2048 | img4096 | ragged150x203 (default: img4096)")
+                    help="img1024 | img2048 | img4096 | img4096_kv | ragged150x203 | ms_img2048 "
+                         "(default: img4096)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -251,13 +258,22 @@ def main() -> int:
     dev = torch.device("cuda:0")
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
     out = torch.empty_like(qd)
-    flops, nbytes = binding.fla_swin_attn_work(wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
-                                               wl.window, wl.shift, wl.pad_mode, wl.elem_bytes)
     stream = torch.cuda.current_stream()
+    if wl.grids:   # multi-scale: the grids' tokens one after the other, one launch
+        grids = list(wl.grid_list)
+        flops, nbytes = binding.fla_swin_attn_ms_work(wl.B, wl.heads, grids, wl.head_dim, wl.window,
+                                                      wl.shift, wl.pad_mode, wl.elem_bytes)
 
-    def step():
-        binding.fla_swin_attn_fwd(qd, kd, vd, out, wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
-                                  wl.window, wl.shift, wl.pad_mode, stream)
+        def step():
+            binding.fla_swin_attn_ms_fwd(qd, kd, vd, out, wl.B, wl.heads, grids, wl.head_dim,
+                                         wl.window, wl.shift, wl.pad_mode, stream)
+    else:
+        flops, nbytes = binding.fla_swin_attn_work(wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                                   wl.window, wl.shift, wl.pad_mode, wl.elem_bytes)
+
+        def step():
+            binding.fla_swin_attn_fwd(qd, kd, vd, out, wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                      wl.window, wl.shift, wl.pad_mode, stream)
 
     print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -294,7 +310,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": wl.name, "B": wl.B, "heads": wl.heads, "grid": [wl.H, wl.W],
+        "config": {"workload": wl.name, "B": wl.B, "heads": wl.heads,
+                   "grid": [list(g) for g in wl.grid_list] if wl.grids else [wl.H, wl.W],
                    "head_dim": wl.head_dim, "window": wl.window, "shift": wl.shift,
                    "pad_mode": wl.pad_mode, "parallelism": "none (1 GPU)"},
         "tflops": round(tflops, 2),

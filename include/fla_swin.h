@@ -51,7 +51,7 @@ typedef enum {
 
 typedef enum {
     FLA_OK = 0,
-    FLA_ERR_SHAPE = 1,     /* B, heads, Hgrid or Wgrid negative                            */
+    FLA_ERR_SHAPE = 1,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8       */
     FLA_ERR_NULL = 2,      /* a pointer is NULL on a non-empty problem                     */
     FLA_ERR_ALIGN = 3,     /* a pointer is not 16-byte aligned                             */
     FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (supported: 64)                      */
@@ -93,6 +93,36 @@ const char* fla_status_string(int status);
 int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim,
                        int window, int shift, int pad_mode, int elem_bytes,
                        double* flops, double* bytes);
+
+/* Multi-scale forward (HRSAM++, Sec. 3.6 "Multi-scale attention" and App. C): one launch over
+ * a sequence that holds the tokens of n_grids grids one after the other -- in the paper the
+ * image grid followed by the anchor-map grid.  grid_hw is a host array of 2 * n_grids ints,
+ * (H_0, W_0, H_1, W_1, ...); grid g's tokens are rows [off_g, off_g + H_g*W_g) of each batch
+ * entry, off_g = sum of the earlier grids' H*W, each grid in raster order.
+ *
+ * Every grid gets the shifted-window attention defined above on its own tokens (windows never
+ * span two grids; window, shift and pad_mode are shared).  In FLA_PAD_KVTOKEN mode all grids
+ * share one pad token, the row L = sum of H_g*W_g of k and v (App. C's KV-only padding with a
+ * shared learnable token).  With n_grids = 1 this is exactly fla_swin_attn_fwd.
+ *
+ * Layout: q and out [B, L, heads, head_dim]; k and v [B, L (+1), heads, head_dim].  Errors
+ * as above: n_grids outside 1..8 is FLA_ERR_SHAPE, grid_hw NULL is FLA_ERR_NULL (both checked
+ * before anything else), a negative H_g or W_g is FLA_ERR_SHAPE, a problem whose grids all
+ * have no tokens is empty, and the size limits of FLA_ERR_TOO_LARGE apply to every grid. */
+int fla_swin_attn_ms_fwd(const void* q, const void* k, const void* v, void* out,
+                         int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                         int window, int shift, int pad_mode, void* stream);
+
+/* fp32 multi-scale forward: the same with float tensors, computed entirely in fp32. */
+int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, float* out,
+                             int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                             int window, int shift, int pad_mode, void* stream);
+
+/* Algorithmic work of one multi-scale call: fla_swin_attn_work summed over the grids, with
+ * one shared pad row instead of one per grid. */
+int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                          int window, int shift, int pad_mode, int elem_bytes,
+                          double* flops, double* bytes);
 
 #ifdef __cplusplus
 }

@@ -12,7 +12,11 @@ from .binding import (  # noqa: F401
     fla_swin_attn_fwd_f32,
     fla_status_string,
     fla_swin_attn_work,
+    fla_swin_attn_ms_fwd,
+    fla_swin_attn_ms_fwd_f32,
+    fla_swin_attn_ms_work,
     swin_attn,
+    swin_attn_ms,
     library_path,
     load_library,
 )

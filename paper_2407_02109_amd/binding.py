@@ -40,6 +40,14 @@ def _declare(lib):
     lib.fla_status_string.restype = ctypes.c_char_p
     lib.fla_swin_attn_work.argtypes = [I, I, I, I, I, I, I, I, I, D, D]
     lib.fla_swin_attn_work.restype = I
+    IP = ctypes.POINTER(ctypes.c_int)
+    ms_args = [P, P, P, P, I, I, I, IP, I, I, I, I, P]
+    lib.fla_swin_attn_ms_fwd.argtypes = ms_args
+    lib.fla_swin_attn_ms_fwd.restype = I
+    lib.fla_swin_attn_ms_fwd_f32.argtypes = ms_args
+    lib.fla_swin_attn_ms_fwd_f32.restype = I
+    lib.fla_swin_attn_ms_work.argtypes = [I, I, I, IP, I, I, I, I, I, D, D]
+    lib.fla_swin_attn_ms_work.restype = I
 
 
 def load_library():
@@ -113,6 +121,66 @@ def fla_swin_attn_work(B, heads, Hgrid, Wgrid, head_dim, window, shift, pad_mode
                                            pad_mode, elem_bytes, ctypes.byref(f), ctypes.byref(b))
     _check(rc)
     return f.value, b.value
+
+
+def _grid_array(grids):
+    """(H, W) pairs -> (n, c_int array of 2n), or (0, None) for None."""
+    if grids is None:
+        return 0, None
+    flat = [int(t) for hw in grids for t in hw]
+    return len(flat) // 2, (ctypes.c_int * max(len(flat), 1))(*flat)
+
+
+def fla_swin_attn_ms_fwd(q, k, v, out, B, heads, grids, head_dim, window, shift,
+                         pad_mode=FLA_PAD_MASK, stream=None, check=True) -> int:
+    """Multi-scale bf16 forward; grids: sequence of (H, W), tokens of each grid one after
+    the other in q, k, v and out."""
+    n, arr = _grid_array(grids)
+    rc = load_library().fla_swin_attn_ms_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, heads, n, arr, head_dim, window, shift,
+        pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_ms_fwd_f32(q, k, v, out, B, heads, grids, head_dim, window, shift,
+                             pad_mode=FLA_PAD_MASK, stream=None, check=True) -> int:
+    """Multi-scale fp32 forward."""
+    n, arr = _grid_array(grids)
+    rc = load_library().fla_swin_attn_ms_fwd_f32(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, heads, n, arr, head_dim, window, shift,
+        pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_ms_work(B, heads, grids, head_dim, window, shift, pad_mode, elem_bytes):
+    """(flops, bytes) of one multi-scale call."""
+    n, arr = _grid_array(grids)
+    f, b = ctypes.c_double(), ctypes.c_double()
+    rc = load_library().fla_swin_attn_ms_work(B, heads, n, arr, head_dim, window, shift, pad_mode,
+                                              elem_bytes, ctypes.byref(f), ctypes.byref(b))
+    _check(rc)
+    return f.value, b.value
+
+
+def swin_attn_ms(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, out=None, stream=None):
+    """Tensor-level multi-scale wrapper: q [B, sum(H*W), heads, d]; k/v with one more row
+    (the shared pad token) in KV-token mode.  Allocates ``out`` when not given."""
+    import torch
+    if q.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError("q must be bfloat16 or float32")
+    for t in (q, k, v):
+        if t.dtype != q.dtype or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("q, k, v must share dtype and be contiguous device tensors")
+    B, L, heads, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    fn = fla_swin_attn_ms_fwd if q.dtype == torch.bfloat16 else fla_swin_attn_ms_fwd_f32
+    fn(q, k, v, out, B, heads, grids, d, window, shift, pad_mode, stream)
+    return out
 
 
 def swin_attn(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, out=None, stream=None):

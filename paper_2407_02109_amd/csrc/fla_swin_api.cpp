@@ -15,26 +15,45 @@ namespace {
 constexpr int64_t kMaxElems = int64_t(1) << 40;
 constexpr int64_t kMaxGroups = (int64_t(1) << 24) - 1;   // grid.x * 256 threads < 2^32
 
+// Windows of a grid list: the canvas has `origin` virtual tokens in front of each axis;
+// window i of an axis covers canvas [i*window, (i+1)*window) = grid [i*window - origin, ...).
 struct Geometry {
-    int origin, nwy, nwx, nqb;
+    int origin, nqb, n_windows;
+    int64_t L;                   // tokens per batch entry
     int64_t n_groups;
+    fla::GridDesc grid[fla::kMaxGrids];
 };
 
-// Windows per axis and the largest window: the canvas has `origin` virtual tokens in
-// front; window i covers canvas [i*window, (i+1)*window) = grid [i*window - origin, ...).
-Geometry geometry(int B, int heads, int H, int W, int window, int shift) {
-    Geometry g;
-    g.origin = (window - shift) % window;
-    const int64_t nwy = (int64_t(H) + g.origin + window - 1) / window;
-    const int64_t nwx = (int64_t(W) + g.origin + window - 1) / window;
-    g.nwy = (int)nwy;
-    g.nwx = (int)nwx;
-    const int64_t max_rows = window < H ? window : H;
-    const int64_t max_cols = window < W ? window : W;
-    const int64_t nmax = max_rows * max_cols;
-    g.nqb = (int)((nmax + fla::kQueryBlock - 1) / fla::kQueryBlock);
-    g.n_groups = int64_t(B) * heads * nwy * nwx * g.nqb;
-    return g;
+int64_t windows_along(int64_t len, int window, int origin) {
+    return len > 0 ? (len + origin + window - 1) / window : 0;
+}
+
+// Fills `g` for n grids of (hw[2i], hw[2i+1]) tokens; false if a count overflows int.
+bool geometry(int B, int heads, int n, const int* hw, int window, int shift, Geometry* g) {
+    g->origin = (window - shift) % window;
+    int64_t nmax = 0, wins = 0, L = 0;
+    for (int i = 0; i < n; ++i) {
+        const int H = hw[2 * i], W = hw[2 * i + 1];
+        const int64_t nwy = windows_along(H, window, g->origin);
+        const int64_t nwx = windows_along(W, window, g->origin);
+        fla::GridDesc& d = g->grid[i];
+        d.H = H;
+        d.W = W;
+        d.nwx = (int)nwx;
+        d.win_begin = (int)wins;
+        d.tok_off = L;
+        d.div_nwx = fla::FastDiv::make((unsigned)(nwx > 0 ? nwx : 1));
+        const int64_t rows = window < H ? window : H, cols = window < W ? window : W;
+        if (rows * cols > nmax) nmax = rows * cols;
+        wins += nwy * nwx;
+        L += int64_t(H) * W;
+        if (wins > (int64_t(1) << 30)) return false;
+    }
+    g->n_windows = (int)wins;
+    g->L = L;
+    g->nqb = (int)((nmax + fla::kQueryBlock - 1) / fla::kQueryBlock);
+    g->n_groups = int64_t(B) * heads * wins * g->nqb;
+    return true;
 }
 
 bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
@@ -44,10 +63,15 @@ bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
 
 // Size checks shared by every entry point.  Returns FLA_OK and sets *empty when there is
 // nothing to compute.
-int check_sizes(int B, int heads, int H, int W, bool* empty) {
+int check_sizes(int B, int heads, int n, const int* hw, bool* empty) {
     *empty = false;
-    if (B < 0 || heads < 0 || H < 0 || W < 0) return FLA_ERR_SHAPE;
-    *empty = B == 0 || heads == 0 || H == 0 || W == 0;
+    if (B < 0 || heads < 0) return FLA_ERR_SHAPE;
+    bool any = false;
+    for (int i = 0; i < n; ++i) {
+        if (hw[2 * i] < 0 || hw[2 * i + 1] < 0) return FLA_ERR_SHAPE;
+        any = any || (hw[2 * i] > 0 && hw[2 * i + 1] > 0);
+    }
+    *empty = B == 0 || heads == 0 || !any;
     return FLA_OK;
 }
 
@@ -88,11 +112,13 @@ int check_arch(int* cus) {
     return ok ? FLA_OK : FLA_ERR_ARCH;
 }
 
-int forward(const void* q, const void* k, const void* v, void* out, int B, int heads, int H,
-            int W, int head_dim, int window, int shift, int pad_mode, void* stream,
+int forward(const void* q, const void* k, const void* v, void* out, int B, int heads, int n_grids,
+            const int* hw, int head_dim, int window, int shift, int pad_mode, void* stream,
             int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t)) {
+    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
+    if (!hw) return FLA_ERR_NULL;
     bool empty = false;
-    int st = check_sizes(B, heads, H, W, &empty);
+    int st = check_sizes(B, heads, n_grids, hw, &empty);
     if (st != FLA_OK || empty) return st;
     if (!q || !k || !v || !out) return FLA_ERR_NULL;
     const uintptr_t mis = (reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) |
@@ -102,19 +128,27 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     if (st != FLA_OK) return st;
 
     // sizes, in an order that cannot overflow int64 before the bound check
-    const int64_t L = int64_t(H) * W;
+    int64_t L = 0;
+    for (int i = 0; i < n_grids; ++i) {
+        if (int64_t(hw[2 * i]) * hw[2 * i + 1] >= kMaxElems) return FLA_ERR_TOO_LARGE;
+        L += int64_t(hw[2 * i]) * hw[2 * i + 1];
+    }
     const int64_t tok = int64_t(heads) * head_dim;
     const int64_t kv_rows = L + (pad_mode == FLA_PAD_KVTOKEN ? 1 : 0);
     if (kv_rows >= kMaxElems || tok >= kMaxElems || kv_rows > kMaxElems / tok) return FLA_ERR_TOO_LARGE;
     if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
-    const Geometry geo = geometry(B, heads, H, W, window, shift);
+    Geometry geo;
+    if (!geometry(B, heads, n_grids, hw, window, shift, &geo)) return FLA_ERR_TOO_LARGE;
     if (geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
     // the kernels address a window with 32-bit byte offsets from its first token, and
     // split a window-local index into (row, col) with a 32-bit multiply-high
-    const int64_t win_rows = window < H ? window : H;
-    const int64_t win_cols = window < W ? window : W;
-    if (win_rows * W * tok * elem_bytes >= (int64_t(1) << 31)) return FLA_ERR_TOO_LARGE;
-    if (win_rows * win_cols * win_cols > (int64_t(1) << 32)) return FLA_ERR_TOO_LARGE;
+    for (int i = 0; i < n_grids; ++i) {
+        const int H = hw[2 * i], W = hw[2 * i + 1];
+        const int64_t win_rows = window < H ? window : H;
+        const int64_t win_cols = window < W ? window : W;
+        if (win_rows * W * tok * elem_bytes >= (int64_t(1) << 31)) return FLA_ERR_TOO_LARGE;
+        if (win_rows * win_cols * win_cols > (int64_t(1) << 32)) return FLA_ERR_TOO_LARGE;
+    }
 
     const int64_t q_bytes = int64_t(B) * L * tok * elem_bytes;
     const int64_t kv_bytes = int64_t(B) * kv_rows * tok * elem_bytes;
@@ -133,29 +167,76 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     a.out = out;
     a.B = B;
     a.heads = heads;
-    a.H = H;
-    a.W = W;
     a.window = window;
     a.shift = shift;
     a.origin = geo.origin;
-    a.nwy = geo.nwy;
-    a.nwx = geo.nwx;
     a.nqb = geo.nqb;
     a.pad_mode = pad_mode;
+    a.L = L;
     a.tok_stride = tok;
     a.q_batch_stride = L * tok;
     a.kv_batch_stride = kv_rows * tok;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
     a.n_groups = geo.n_groups;
     a.n_cus = cus;
+    a.n_grids = n_grids;
+    a.n_windows = geo.n_windows;
+    for (int i = 0; i < fla::kMaxGrids; ++i) a.grid[i] = geo.grid[i < n_grids ? i : 0];
     a.div_heads = fla::FastDiv::make((unsigned)heads);
     a.div_nqb = fla::FastDiv::make((unsigned)geo.nqb);
-    a.div_nwin = fla::FastDiv::make((unsigned)(geo.nwy * geo.nwx));
-    a.div_nwx = fla::FastDiv::make((unsigned)geo.nwx);
+    a.div_nwin = fla::FastDiv::make((unsigned)geo.n_windows);
     if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;
     }
+    return FLA_OK;
+}
+
+// Algorithmic work of the windows of one grid: sum of n^2 (and n for windows with virtual
+// slots in KV-token mode) over its windows.
+double grid_pairs(int H, int W, int window, int shift, int pad_mode) {
+    if (H <= 0 || W <= 0) return 0.0;
+    const int origin = (window - shift) % window;
+    const int64_t nwy = windows_along(H, window, origin), nwx = windows_along(W, window, origin);
+    auto extent = [&](int64_t i, int64_t len) -> double {
+        int64_t s0 = i * window - origin, s1 = s0 + window;
+        if (s0 < 0) s0 = 0;
+        if (s1 > len) s1 = len;
+        return double(s1 - s0);
+    };
+    const double full = double(window) * double(window);
+    double pairs = 0.0;
+    for (int64_t i = 0; i < nwy; ++i) {
+        const double a = extent(i, H);
+        for (int64_t j = 0; j < nwx; ++j) {
+            const double n = a * extent(j, W);
+            pairs += n * n;
+            if (pad_mode == FLA_PAD_KVTOKEN && n < full) pairs += n;
+        }
+    }
+    return pairs;
+}
+
+int work(int B, int heads, int n_grids, const int* hw, int head_dim, int window, int shift,
+         int pad_mode, int elem_bytes, double* flops, double* bytes) {
+    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
+    if (!hw) return FLA_ERR_NULL;
+    bool empty = false;
+    int st = check_sizes(B, heads, n_grids, hw, &empty);
+    if (st != FLA_OK) return st;
+    if (window < 1) return FLA_ERR_WINDOW;
+    if (shift < 0 || shift >= window) return FLA_ERR_SHIFT;
+    if (pad_mode != FLA_PAD_MASK && pad_mode != FLA_PAD_KVTOKEN) return FLA_ERR_PAD_MODE;
+    if (head_dim < 1 || elem_bytes < 1) return FLA_ERR_HEAD_DIM;
+    double pairs = 0.0, tokens = 0.0;
+    if (!empty)
+        for (int i = 0; i < n_grids; ++i) {
+            pairs += grid_pairs(hw[2 * i], hw[2 * i + 1], window, shift, pad_mode);
+            tokens += double(hw[2 * i]) * hw[2 * i + 1];
+        }
+    const double rows = empty ? 0.0 : 4.0 * tokens + (pad_mode == FLA_PAD_KVTOKEN ? 2.0 : 0.0);
+    if (flops) *flops = 4.0 * head_dim * double(heads) * B * pairs;
+    if (bytes) *bytes = rows * B * double(heads) * head_dim * elem_bytes;
     return FLA_OK;
 }
 
@@ -166,21 +247,37 @@ extern "C" {
 int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
                       int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
                       void* stream) {
-    return forward(q, k, v, out, B, heads, Hgrid, Wgrid, head_dim, window, shift, pad_mode,
-                   stream, 2, fla::launch_swin_fwd_bf16);
+    const int hw[2] = {Hgrid, Wgrid};
+    return forward(q, k, v, out, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
+                   fla::launch_swin_fwd_bf16);
 }
 
 int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                           int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
                           int pad_mode, void* stream) {
-    return forward(q, k, v, out, B, heads, Hgrid, Wgrid, head_dim, window, shift, pad_mode,
+    const int hw[2] = {Hgrid, Wgrid};
+    return forward(q, k, v, out, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 4,
+                   fla::launch_swin_fwd_f32);
+}
+
+int fla_swin_attn_ms_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
+                         int n_grids, const int* grid_hw, int head_dim, int window, int shift,
+                         int pad_mode, void* stream) {
+    return forward(q, k, v, out, B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode,
+                   stream, 2, fla::launch_swin_fwd_bf16);
+}
+
+int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
+                             int heads, int n_grids, const int* grid_hw, int head_dim, int window,
+                             int shift, int pad_mode, void* stream) {
+    return forward(q, k, v, out, B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode,
                    stream, 4, fla::launch_swin_fwd_f32);
 }
 
 const char* fla_status_string(int status) {
     switch (status) {
         case FLA_OK: return "ok";
-        case FLA_ERR_SHAPE: return "B, heads, Hgrid and Wgrid must be >= 0";
+        case FLA_ERR_SHAPE: return "B, heads and grid sizes must be >= 0 (1 to 8 grids)";
         case FLA_ERR_NULL: return "q, k, v and out must be non-NULL";
         case FLA_ERR_ALIGN: return "q, k, v and out must be 16-byte aligned";
         case FLA_ERR_HEAD_DIM: return "head_dim must be 64";
@@ -197,39 +294,15 @@ const char* fla_status_string(int status) {
 
 int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
                        int shift, int pad_mode, int elem_bytes, double* flops, double* bytes) {
-    bool empty = false;
-    int st = check_sizes(B, heads, Hgrid, Wgrid, &empty);
-    if (st != FLA_OK) return st;
-    if (window < 1) return FLA_ERR_WINDOW;
-    if (shift < 0 || shift >= window) return FLA_ERR_SHIFT;
-    if (pad_mode != FLA_PAD_MASK && pad_mode != FLA_PAD_KVTOKEN) return FLA_ERR_PAD_MODE;
-    if (head_dim < 1 || elem_bytes < 1) return FLA_ERR_HEAD_DIM;
-    double pairs = 0.0;
-    if (!empty) {
-        // window (i, j) holds rows_i * cols_j tokens; rows_i from the canvas geometry
-        const int origin = (window - shift) % window;
-        const int64_t nwy = (int64_t(Hgrid) + origin + window - 1) / window;
-        const int64_t nwx = (int64_t(Wgrid) + origin + window - 1) / window;
-        auto extent = [&](int64_t i, int64_t len) -> double {
-            int64_t s0 = i * window - origin, s1 = s0 + window;
-            if (s0 < 0) s0 = 0;
-            if (s1 > len) s1 = len;
-            return double(s1 - s0);
-        };
-        const double full = double(window) * double(window);
-        for (int64_t i = 0; i < nwy; ++i) {
-            const double a = extent(i, Hgrid);
-            for (int64_t j = 0; j < nwx; ++j) {
-                const double n = a * extent(j, Wgrid);
-                pairs += n * n;
-                if (pad_mode == FLA_PAD_KVTOKEN && n < full) pairs += n;
-            }
-        }
-    }
-    const double rows = empty ? 0.0 : 4.0 * double(Hgrid) * Wgrid + (pad_mode == FLA_PAD_KVTOKEN ? 2.0 : 0.0);
-    if (flops) *flops = 4.0 * head_dim * double(heads) * B * pairs;
-    if (bytes) *bytes = rows * B * double(heads) * head_dim * elem_bytes;
-    return FLA_OK;
+    const int hw[2] = {Hgrid, Wgrid};
+    return work(B, heads, 1, hw, head_dim, window, shift, pad_mode, elem_bytes, flops, bytes);
+}
+
+int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                          int window, int shift, int pad_mode, int elem_bytes, double* flops,
+                          double* bytes) {
+    return work(B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode, elem_bytes, flops,
+                bytes);
 }
 
 }  // extern "C"

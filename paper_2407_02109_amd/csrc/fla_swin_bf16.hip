@@ -173,7 +173,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const int head = (int)(id0 - id1 * (unsigned)a.heads);
     const unsigned id2 = a.div_nqb.div(id1);
     const int qblk = (int)(id1 - id2 * (unsigned)a.nqb);
-    const int nwin = a.nwy * a.nwx;
+    const int nwin = a.n_windows;
     const unsigned id3 = a.div_nwin.div(id2);
     const int win = (int)(id2 - id3 * (unsigned)nwin);
     const int b = (int)id3;
@@ -189,8 +189,8 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const float pad_bias_raw = has_pad ? log2f((float)n_pad) / a.scale_log2 : 0.f;
 
     // ---- buffer resources based at the window's first token (y0, x0) of head `head`
-    const long long L = (long long)a.H * a.W;
-    const long long win_elems = ((long long)wr.y0 * a.W + wr.x0) * a.tok_stride + head * D;
+    const long long L = a.L;
+    const long long win_elems = wr.tok0 * a.tok_stride + head * D;
     const long long q_base = (long long)b * a.q_batch_stride + win_elems;
     const long long kv_base = (long long)b * a.kv_batch_stride + win_elems;
     const long long q_total = (long long)a.B * a.q_batch_stride;
@@ -209,7 +209,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, has_pad ? D * 2 : 0);
 
     WindowAddr addr;
-    addr.init(wr.cols, (unsigned)((long long)a.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
+    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;

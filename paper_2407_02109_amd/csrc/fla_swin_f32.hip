@@ -25,7 +25,7 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     id /= a.heads;
     const int qblk = (int)(id % a.nqb);
     id /= a.nqb;
-    const int nwin = a.nwy * a.nwx;
+    const int nwin = a.n_windows;
     const int win = (int)(id % nwin);
     const int b = (int)(id / nwin);
 
@@ -43,12 +43,12 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     const float* kg = static_cast<const float*>(a.k) + (long long)b * a.kv_batch_stride + head * D;
     const float* vg = static_cast<const float*>(a.v) + (long long)b * a.kv_batch_stride + head * D;
     float* og = static_cast<float*>(a.out) + (long long)b * a.q_batch_stride + head * D;
-    const long long L = (long long)a.H * a.W;
+    const long long L = a.L;
     auto token_off = [&](int t) -> long long {
         if (t >= n) return L * a.tok_stride;
         const int r = t / wr.cols;
         const int c = t - r * wr.cols;
-        return ((long long)(wr.y0 + r) * a.W + (wr.x0 + c)) * a.tok_stride;
+        return (wr.tok0 + (long long)r * wr.W + c) * a.tok_stride;
     };
 
     const int tid = threadIdx.x;

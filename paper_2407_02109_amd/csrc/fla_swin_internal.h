@@ -30,47 +30,70 @@ struct FastDiv {
 constexpr int kHeadDim = 64;    // head_dim supported by the kernels
 constexpr int kQueryBlock = 256; // queries of one window handled by one workgroup
 
+constexpr int kMaxGrids = 8;    // token grids of one multi-scale sequence
+
+// One token grid of the sequence (a single grid, or the image grid and the anchor-map grid
+// of multi-scale attention).  Its windows are numbered after those of the grids before it.
+struct GridDesc {
+    int H, W;                   // rows and columns of tokens
+    int nwx;                    // windows per row: ceil((W + origin) / window)
+    int win_begin;              // index of its first window among all windows
+    int64_t tok_off;            // index of its first token within a batch entry
+    FastDiv div_nwx;
+};
+
 // Everything a kernel needs, computed once on the host per call.
 struct SwinArgs {
     const void* q;
     const void* k;
     const void* v;
     void* out;
-    int B, heads, H, W;
+    int B, heads;
     int window, shift;
     int origin;                 // (window - shift) % window: virtual tokens in front of each axis
-    int nwy, nwx;               // windows per axis: ceil((H + origin) / window), same for W
     int nqb;                    // query blocks per window: ceil(max window size / kQueryBlock)
     int pad_mode;               // 0 = mask virtual keys, 1 = pad token at row L
+    int64_t L;                  // tokens per batch entry, all grids (the pad token's row)
     int64_t tok_stride;         // elements between consecutive tokens: heads * head_dim
     int64_t q_batch_stride;     // elements between batch entries of q / out: L * tok_stride
     int64_t kv_batch_stride;    // same for k / v (L or L + 1 rows)
     float scale_log2;           // log2(e) / sqrt(head_dim): logits go straight to exp2
     int64_t n_groups;           // workgroups: B * heads * windows * query blocks
     int n_cus;                  // compute units of the device
-    FastDiv div_heads, div_nqb, div_nwin, div_nwx;   // workgroup index decode
+    int n_grids, n_windows;     // grids, and windows over all grids
+    GridDesc grid[kMaxGrids];
+    FastDiv div_heads, div_nqb, div_nwin;   // workgroup index decode
 };
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
-// Window of workgroup `win` (raster order over nwy x nwx), clipped to the grid.
+// Window `win` (numbered over all grids, raster order within a grid), clipped to its grid.
 struct WindowRect {
     int y0, x0, rows, cols;
+    int W;                      // tokens per row of its grid
+    int64_t tok0;               // index of its first token (y0, x0) within a batch entry
 };
 
 __device__ __forceinline__ WindowRect window_rect(const SwinArgs& a, int win) {
-    const int wy = (int)a.div_nwx.div((unsigned)win);
-    const int wx = win - wy * a.nwx;
+    int g = 0;
+    for (int i = 1; i < kMaxGrids; ++i)
+        if (i < a.n_grids && win >= a.grid[i].win_begin) g = i;
+    const GridDesc& G = a.grid[g];
+    const int lw = win - G.win_begin;
+    const int wy = (int)G.div_nwx.div((unsigned)lw);
+    const int wx = lw - wy * G.nwx;
     const long long ys = (long long)wy * a.window - a.origin;
     const long long xs = (long long)wx * a.window - a.origin;
-    const long long ye = ys + a.window < a.H ? ys + a.window : a.H;
-    const long long xe = xs + a.window < a.W ? xs + a.window : a.W;
+    const long long ye = ys + a.window < G.H ? ys + a.window : G.H;
+    const long long xe = xs + a.window < G.W ? xs + a.window : G.W;
     WindowRect r;
     r.y0 = ys > 0 ? (int)ys : 0;
     r.x0 = xs > 0 ? (int)xs : 0;
     r.rows = (int)(ye - r.y0);
     r.cols = (int)(xe - r.x0);
+    r.W = G.W;
+    r.tok0 = G.tok_off + (int64_t)r.y0 * G.W + r.x0;
     return r;
 }
 

@@ -35,11 +35,16 @@ class Workload:
     pad_mode: int = PAD_MASK
     scale: float = 1.0         # exact power of two applied to q, k and v before rounding
     stress_keys: float = 0.0   # fraction of (token, head) key rows multiplied by 8
+    grids: tuple = ()          # multi-scale: ((H, W), ...) one after the other; () = (H, W) alone
     note: str = field(default="", compare=False)
 
     @property
+    def grid_list(self) -> tuple:
+        return self.grids if self.grids else ((self.H, self.W),)
+
+    @property
     def L(self) -> int:
-        return self.H * self.W
+        return sum(h * w for h, w in self.grid_list)
 
     @property
     def elem_bytes(self) -> int:
@@ -69,6 +74,10 @@ WORKLOADS = {
                            pad_mode=PAD_KVTOKEN,
                            note="img4096 with KV-only padding: border windows attend the pad token "
                                 "(row L of k and v) with multiplicity window^2 - n"),
+    "ms_img2048": Workload("ms_img2048", 1, 12, 128, 128, 64, 16, 8, "bf16", seed=7,
+                           pad_mode=PAD_KVTOKEN, grids=((128, 128), (32, 32)),
+                           note="multi-scale (HRSAM++): the 2048^2 image's 128x128 tokens followed by "
+                                "the 512^2 anchor map's 32x32, one shared pad token"),
     "ragged150x203": Workload("ragged150x203", 4, 12, 150, 203, 64, 16, 8, "bf16", seed=4,
                               note="non-divisible 150x203 grid, B=4, 12 heads x 64, window 16, "
                                    "shift 8, padded keys masked"),
@@ -108,6 +117,26 @@ def make_inputs(wl: Workload, device: str | torch.device = "cpu"):
 def to_f64_numpy(t):
     """Exact float64 copy of a CPU/GPU tensor (bf16 and fp32 embed exactly in fp64)."""
     return t.detach().to("cpu", torch.float64).numpy()
+
+
+def random_ms_queries(wl: Workload, n: int, seed: int):
+    """n random (b, grid, y, x) query positions over the grids of a multi-scale workload, in
+    proportion to their token counts, plus the four corners of every grid; int64 [S, 4]."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    grids = wl.grid_list
+    sizes = torch.tensor([h * w for h, w in grids], dtype=torch.float64)
+    gi = torch.multinomial(sizes / sizes.sum(), n, replacement=True, generator=g)
+    b = torch.randint(0, wl.B, (n,), generator=g)
+    u = torch.rand(n, 2, generator=g, dtype=torch.float64)
+    hs = torch.tensor([h for h, _ in grids])[gi]
+    ws = torch.tensor([w for _, w in grids])[gi]
+    y = (u[:, 0] * hs).long().clamp(max=hs - 1)
+    x = (u[:, 1] * ws).long().clamp(max=ws - 1)
+    pts = [torch.stack([b, gi, y, x], dim=1)]
+    corners = [(0, i, yy, xx) for i, (h, w) in enumerate(grids) for yy in {0, h - 1} for xx in {0, w - 1}]
+    pts.append(torch.tensor(corners, dtype=torch.int64))
+    return torch.cat(pts, dim=0)
 
 
 def random_queries(wl: Workload, n: int, seed: int):

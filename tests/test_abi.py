@@ -36,7 +36,9 @@ def lib():
 
 def test_header_declares_the_entry_points():
     assert _header_functions() == ["fla_status_string", "fla_swin_attn_fwd",
-                                   "fla_swin_attn_fwd_f32", "fla_swin_attn_work"]
+                                   "fla_swin_attn_fwd_f32", "fla_swin_attn_ms_fwd",
+                                   "fla_swin_attn_ms_fwd_f32", "fla_swin_attn_ms_work",
+                                   "fla_swin_attn_work"]
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -173,6 +175,68 @@ def test_work_counts_errors(lib):
     f = ctypes.c_double(-1)
     assert lib.fla_swin_attn_work(0, 1, 8, 8, 64, 4, 0, 0, 2, ctypes.byref(f), None) == 0
     assert f.value == 0.0
+
+
+# ---- multi-scale entry points --------------------------------------------------------
+MS_GOOD = dict(B=1, heads=12, grids=[(64, 64), (32, 32)], head_dim=64, window=16, shift=8, pad_mode=0)
+
+
+def _call_ms(fn, q=Q, k=K, v=V, out=OUT, **kw):
+    a = dict(MS_GOOD)
+    a.update(kw)
+    return fn(q, k, v, out, a["B"], a["heads"], a["grids"], a["head_dim"], a["window"], a["shift"],
+              a["pad_mode"], 0, check=False)
+
+
+MS_CASES = [
+    ("FLA_ERR_SHAPE", dict(grids=[])), ("FLA_ERR_SHAPE", dict(grids=[(4, 4)] * 9)),
+    ("FLA_ERR_SHAPE", dict(grids=[(64, 64), (-1, 32)])), ("FLA_ERR_SHAPE", dict(B=-1)),
+    ("FLA_ERR_NULL", dict(q=0)), ("FLA_ERR_ALIGN", dict(out=OUT + 4)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=128)), ("FLA_ERR_SHIFT", dict(shift=16)),
+    ("FLA_ERR_PAD_MODE", dict(pad_mode=3)),
+    ("FLA_ERR_TOO_LARGE", dict(grids=[(64, 64), (4, 1 << 21)], window=8, shift=0)),
+    ("FLA_ERR_ALIAS", dict(out=Q + (64 * 64 + 32 * 32 - 1) * 12 * 64 * 2)),   # last row of q
+]
+
+
+@pytest.mark.parametrize("fn", [fb.fla_swin_attn_ms_fwd, fb.fla_swin_attn_ms_fwd_f32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("status,kw", MS_CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(MS_CASES)])
+def test_ms_argument_checks(lib, fn, status, kw):
+    kw = dict(kw)
+    if fn is fb.fla_swin_attn_ms_fwd_f32 and status == "FLA_ERR_ALIAS":
+        kw["out"] = Q + (64 * 64 + 32 * 32 - 1) * 12 * 64 * 4
+    assert _call_ms(fn, **kw) == _header_enum("FLA")[status]
+
+
+def test_ms_null_grid_list_and_empty_grids(lib):
+    codes = _header_enum("FLA")
+    assert lib.fla_swin_attn_ms_fwd(Q, K, V, OUT, 1, 12, 2, None, 64, 16, 8, 0, None) == codes["FLA_ERR_NULL"]
+    # a grid count outside 1..8 is reported before the NULL list
+    assert lib.fla_swin_attn_ms_fwd(Q, K, V, OUT, 1, 12, 0, None, 64, 16, 8, 0, None) == codes["FLA_ERR_SHAPE"]
+    # every grid empty: nothing to do, pointers ignored
+    assert _call_ms(fb.fla_swin_attn_ms_fwd, q=0, grids=[(0, 5), (7, 0)]) == 0
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_ms_no_device_reports_arch(lib):
+    assert _call_ms(fb.fla_swin_attn_ms_fwd) == _header_enum("FLA")["FLA_ERR_ARCH"]
+    assert _call_ms(fb.fla_swin_attn_ms_fwd, grids=[(64, 64)]) == _header_enum("FLA")["FLA_ERR_ARCH"]
+
+
+@pytest.mark.parametrize("grids,k,s,pm", [
+    ([(128, 128), (32, 32)], 16, 8, 1), ([(64, 64), (32, 32)], 16, 8, 0), ([(20, 13), (7, 9), (1, 1)], 8, 3, 1),
+    ([(150, 203)], 16, 8, 0), ([(5, 0), (9, 9)], 4, 1, 1)])
+def test_ms_work_counts_match_oracle(lib, grids, k, s, pm):
+    for eb in (2, 4):
+        f, b = fb.fla_swin_attn_ms_work(2, 3, grids, 64, k, s, pm, eb)
+        f0, b0 = O.ms_work_counts(2, 3, [g for g in grids if g[0] * g[1] > 0], 64, k, s, pm, eb)
+        assert f == f0 and b == b0
+
+
+def test_single_grid_work_equals_ms_work(lib):
+    for args in [(1, 12, 256, 256, 64, 16, 8, 0, 2), (4, 12, 150, 203, 64, 16, 8, 1, 2)]:
+        B, heads, H, W, d, k, s, pm, eb = args
+        assert fb.fla_swin_attn_work(*args) == fb.fla_swin_attn_ms_work(B, heads, [(H, W)], d, k, s, pm, eb)
 
 
 def test_product_code_never_touches_the_oracle():
