@@ -5,8 +5,9 @@ TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check in
 The GPU library never imports it and shares no code, table or helper with it.
 
 Every function here is a slow, obviously-correct restatement of the paper's
-definitions in float64 NumPy; see ``swin_oracle`` for the four single-grid forms and
-``multiscale`` for the multi-scale (several grids in one sequence) forms of App. C.
+definitions in float64 NumPy; see ``swin_oracle`` for the four single-grid forms,
+``multiscale`` for the multi-scale (several grids in one sequence) forms of App. C and
+``backward`` for the gradients (dq, dk, dv) and the log-sum-exp a training forward keeps.
 """
 from .swin_oracle import (  # noqa: F401
     PAD_MASK,
@@ -20,6 +21,12 @@ from .swin_oracle import (  # noqa: F401
     fla_kv_padding_indices,
     window_sizes,
     work_counts,
+)
+from .backward import (  # noqa: F401
+    swin_attention_bwd,
+    swin_attention_lse,
+    swin_attention_ms_bwd,
+    swin_attention_ms_lse,
 )
 from .multiscale import (  # noqa: F401
     grid_offsets,
