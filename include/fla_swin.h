@@ -1,4 +1,4 @@
-/* Flash Swin attention forward for AMD MI355X (gfx950) -- C ABI.
+/* Flash Swin attention (forward and backward) for AMD MI355X (gfx950) -- C ABI.
  *
  * Operation (HRSAM, arXiv 2407.02109):
  *   Eq. 1 (Sec. 3.2) scaled dot-product attention, evaluated independently inside each
@@ -40,6 +40,8 @@
 #ifndef FLA_SWIN_H
 #define FLA_SWIN_H
 
+#include <stddef.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -62,9 +64,14 @@ typedef enum {
                               2^24 workgroups or more, the rows of one window span 2 GiB or
                               more (min(window, Hgrid) * Wgrid * heads * head_dim * element
                               bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
-    FLA_ERR_ALIAS = 9,     /* out overlaps q, k or v                                       */
+    FLA_ERR_ALIAS = 9,     /* an output (out, lse, dq, dk, dv, workspace) overlaps an input
+                              or another output                                          */
     FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
-    FLA_ERR_LAUNCH = 11    /* the HIP runtime refused the kernel launch                    */
+    FLA_ERR_LAUNCH = 11,   /* the HIP runtime refused the kernel launch                    */
+    FLA_ERR_UNSUPPORTED = 12, /* bf16 backward with a window of more than 256 tokens
+                                 (min(window, H) * min(window, W) > 256 for some grid)    */
+    FLA_ERR_WORKSPACE = 13 /* backward: workspace NULL or smaller than
+                              fla_swin_attn_bwd_workspace() reports                       */
 } fla_status;
 
 /* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
@@ -123,6 +130,95 @@ int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, flo
 int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
                           int window, int shift, int pad_mode, int elem_bytes,
                           double* flops, double* bytes);
+
+/* ---------------------------------------------------------------------------------------
+ * Training: the forward that keeps the log-sum-exp, and the backward pass.
+ *
+ * The paper trains HRSAM through Flash Swin attention (App. D); the gradients are those of
+ * the operation above.  With c = 1/sqrt(head_dim), for a query i with key set R_i (plus, in
+ * FLA_PAD_KVTOKEN mode, the pad token p with weight w_p = n_pad; w_j = 1 otherwise):
+ *
+ *   LSE_i = log sum_j w_j exp(c <q_i, k_j>)            P_ij = w_j exp(c <q_i, k_j> - LSE_i)
+ *   D_i   = <dout_i, out_i>                            dS_ij = P_ij (<dout_i, v_j> - D_i)
+ *   dq_i  = c sum_j dS_ij k_j     dk_j = c sum_i dS_ij q_i     dv_j = sum_i P_ij dout_i
+ *
+ * dk and dv of the pad token (row L) sum over every query of every window that has virtual
+ * slots.  P is recomputed from q, k and LSE; nothing of size n^2 is stored.
+ * --------------------------------------------------------------------------------------- */
+
+/* Training forward: fla_swin_attn_fwd, and also lse [B, heads, L] (fp32, contiguous):
+ * LSE_i above, the natural log of each query's softmax denominator.  lse is a device
+ * pointer, non-NULL, 16-byte aligned, and must not overlap q, k, v or out.  In bf16 the
+ * denominator is the sum of the bf16-rounded probabilities the output uses. */
+int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
+                          int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                          int window, int shift, int pad_mode, void* stream);
+int fla_swin_attn_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
+                              float* lse, int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                              int window, int shift, int pad_mode, void* stream);
+int fla_swin_attn_ms_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
+                             int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                             int window, int shift, int pad_mode, void* stream);
+int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
+                                 float* lse, int B, int heads, int n_grids, const int* grid_hw,
+                                 int head_dim, int window, int shift, int pad_mode, void* stream);
+
+/* Workspace the backward needs, in bytes (host arithmetic only): in FLA_PAD_KVTOKEN mode
+ * 512 bytes per (batch entry, head, window, block of 256 window tokens), holding each
+ * block's share of the pad token's gradient; 0 in FLA_PAD_MASK mode.  Single-grid callers
+ * pass n_grids = 1 and grid_hw = {Hgrid, Wgrid}.  Argument errors as for the forward;
+ * bytes must be non-NULL (FLA_ERR_NULL). */
+int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,
+                                int shift, int pad_mode, size_t* bytes);
+
+/* bf16 backward.  Inputs: q, k, v and dout as for the forward, out and lse as the training
+ * forward wrote them.  Outputs: dq (layout of q), dk and dv (layout of k and v; in
+ * FLA_PAD_KVTOKEN mode row L holds the pad token's gradient).  Every output element is
+ * written; nothing is accumulated into what the buffers held.  workspace: device memory
+ * of at least fla_swin_attn_bwd_workspace() bytes (may be NULL when that is 0), contents
+ * ignored on entry.  All pointers are device pointers, 16-byte aligned.  Inputs may alias
+ * each other; dq, dk, dv and the workspace must not overlap any input or each other.
+ * S = Q.K^T, dP = dO.V^T, dV = P^T.dO, dK = dS^T.Q and dQ = dS.K run on bf16 matrix cores
+ * with fp32 accumulation (P and dS rounded to bf16 before their products); outputs are
+ * rounded to bf16 (RNE).  The result does not depend on scheduling (fixed summation
+ * order).  Windows are limited to 256 tokens (FLA_ERR_UNSUPPORTED), i.e. window <= 16
+ * covers every grid.  Errors: checked in the order of the status codes (after the size
+ * checks), then FLA_ERR_UNSUPPORTED, FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS,
+ * FLA_ERR_ARCH; nothing is launched and no output is touched on error.  Asynchronous on
+ * `stream`: one kernel (two in FLA_PAD_KVTOKEN mode). */
+int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                      const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                      void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
+                      int Wgrid, int head_dim, int window, int shift, int pad_mode, void* stream);
+
+/* fp32 backward: the same with float tensors, computed entirely in fp32, any window size. */
+int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,
+                          const float* dout, const float* lse, float* dq, float* dk, float* dv,
+                          void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
+                          int Wgrid, int head_dim, int window, int shift, int pad_mode,
+                          void* stream);
+
+/* Multi-scale backward (App. C): the backward of fla_swin_attn_ms_fwd; the shared pad
+ * token's gradient sums over all grids. */
+int fla_swin_attn_ms_bwd(const void* q, const void* k, const void* v, const void* out,
+                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                         void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
+                         const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
+                         void* stream);
+int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, const float* out,
+                             const float* dout, const float* lse, float* dq, float* dk, float* dv,
+                             void* workspace, size_t workspace_bytes, int B, int heads,
+                             int n_grids, const int* grid_hw, int head_dim, int window, int shift,
+                             int pad_mode, void* stream);
+
+/* Algorithmic work of one backward call:
+ *   *flops = 10 * head_dim * heads * B * pairs (pairs as in fla_swin_attn_work: the five
+ *            products S, dP, dV, dK, dQ over the unmasked pairs and pad keys);
+ *   *bytes = elem_bytes * heads * head_dim * B * (8 * L (+4 pad rows)) + 4 * B * heads * L:
+ *            q, k, v, out, dout read once, dq, dk, dv written once, lse read once. */
+int fla_swin_attn_bwd_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                           int window, int shift, int pad_mode, int elem_bytes,
+                           double* flops, double* bytes);
 
 #ifdef __cplusplus
 }

@@ -15,8 +15,16 @@ from .binding import (  # noqa: F401
     fla_swin_attn_ms_fwd,
     fla_swin_attn_ms_fwd_f32,
     fla_swin_attn_ms_work,
+    fla_swin_attn_fwd_lse,
+    fla_swin_attn_ms_fwd_lse,
+    fla_swin_attn_bwd_workspace,
+    fla_swin_attn_bwd,
+    fla_swin_attn_ms_bwd,
+    fla_swin_attn_bwd_work,
     swin_attn,
     swin_attn_ms,
+    swin_attn_fwd_train,
+    swin_attn_bwd,
     library_path,
     load_library,
 )

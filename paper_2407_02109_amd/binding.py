@@ -48,6 +48,24 @@ def _declare(lib):
     lib.fla_swin_attn_ms_fwd_f32.restype = I
     lib.fla_swin_attn_ms_work.argtypes = [I, I, I, IP, I, I, I, I, I, D, D]
     lib.fla_swin_attn_ms_work.restype = I
+    lse_args = [P, P, P, P, P, I, I, I, I, I, I, I, I, P]
+    ms_lse_args = [P, P, P, P, P, I, I, I, IP, I, I, I, I, P]
+    for name, args in (("fla_swin_attn_fwd_lse", lse_args), ("fla_swin_attn_fwd_lse_f32", lse_args),
+                       ("fla_swin_attn_ms_fwd_lse", ms_lse_args),
+                       ("fla_swin_attn_ms_fwd_lse_f32", ms_lse_args)):
+        getattr(lib, name).argtypes = args
+        getattr(lib, name).restype = I
+    Z = ctypes.c_size_t
+    bwd_args = [P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, I, I, I, I, P]
+    ms_bwd_args = [P, P, P, P, P, P, P, P, P, P, Z, I, I, I, IP, I, I, I, I, P]
+    for name, args in (("fla_swin_attn_bwd", bwd_args), ("fla_swin_attn_bwd_f32", bwd_args),
+                       ("fla_swin_attn_ms_bwd", ms_bwd_args), ("fla_swin_attn_ms_bwd_f32", ms_bwd_args)):
+        getattr(lib, name).argtypes = args
+        getattr(lib, name).restype = I
+    lib.fla_swin_attn_bwd_workspace.argtypes = [I, I, I, IP, I, I, I, ctypes.POINTER(Z)]
+    lib.fla_swin_attn_bwd_workspace.restype = I
+    lib.fla_swin_attn_bwd_work.argtypes = [I, I, I, IP, I, I, I, I, I, D, D]
+    lib.fla_swin_attn_bwd_work.restype = I
 
 
 def load_library():
@@ -198,3 +216,114 @@ def swin_attn(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, out=N
     fn = fla_swin_attn_fwd if q.dtype == torch.bfloat16 else fla_swin_attn_fwd_f32
     fn(q, k, v, out, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, stream)
     return out
+
+
+# ---- training: forward with log-sum-exp, backward ------------------------------------------
+
+def fla_swin_attn_fwd_lse(q, k, v, out, lse, B, heads, Hgrid, Wgrid, head_dim, window, shift,
+                          pad_mode=FLA_PAD_MASK, stream=None, check=True, f32=False) -> int:
+    """Training forward (bf16, or fp32 with f32=True): out and lse [B, heads, L] fp32."""
+    fn = load_library().fla_swin_attn_fwd_lse_f32 if f32 else load_library().fla_swin_attn_fwd_lse
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, heads, Hgrid, Wgrid, head_dim,
+            window, shift, pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_ms_fwd_lse(q, k, v, out, lse, B, heads, grids, head_dim, window, shift,
+                             pad_mode=FLA_PAD_MASK, stream=None, check=True, f32=False) -> int:
+    """Multi-scale training forward."""
+    n, arr = _grid_array(grids)
+    lib = load_library()
+    fn = lib.fla_swin_attn_ms_fwd_lse_f32 if f32 else lib.fla_swin_attn_ms_fwd_lse
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, heads, n, arr, head_dim, window,
+            shift, pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_bwd_workspace(B, heads, grids, window, shift, pad_mode=FLA_PAD_MASK) -> int:
+    """Workspace bytes the backward needs (0 in mask mode)."""
+    n, arr = _grid_array(grids)
+    out = ctypes.c_size_t()
+    _check(load_library().fla_swin_attn_bwd_workspace(B, heads, n, arr, window, shift, pad_mode,
+                                                      ctypes.byref(out)))
+    return out.value
+
+
+def fla_swin_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads,
+                      Hgrid, Wgrid, head_dim, window, shift, pad_mode=FLA_PAD_MASK, stream=None,
+                      check=True, f32=False) -> int:
+    """Backward (bf16, or fp32 with f32=True); all tensors as raw addresses or tensors."""
+    lib = load_library()
+    fn = lib.fla_swin_attn_bwd_f32 if f32 else lib.fla_swin_attn_bwd
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+            _ptr(workspace), int(workspace_bytes), B, heads, Hgrid, Wgrid, head_dim, window, shift,
+            pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_ms_bwd(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads,
+                         grids, head_dim, window, shift, pad_mode=FLA_PAD_MASK, stream=None,
+                         check=True, f32=False) -> int:
+    """Multi-scale backward."""
+    n, arr = _grid_array(grids)
+    lib = load_library()
+    fn = lib.fla_swin_attn_ms_bwd_f32 if f32 else lib.fla_swin_attn_ms_bwd
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+            _ptr(workspace), int(workspace_bytes), B, heads, n, arr, head_dim, window, shift,
+            pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_bwd_work(B, heads, grids, head_dim, window, shift, pad_mode, elem_bytes):
+    """(flops, bytes) of one backward call."""
+    n, arr = _grid_array(grids)
+    f, b = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().fla_swin_attn_bwd_work(B, heads, n, arr, head_dim, window, shift, pad_mode,
+                                                 elem_bytes, ctypes.byref(f), ctypes.byref(b)))
+    return f.value, b.value
+
+
+def _check_tensors(*ts):
+    import torch
+    t0 = ts[0]
+    if t0.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError("tensors must be bfloat16 or float32")
+    for t in ts:
+        if t.dtype != t0.dtype or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must share dtype and be contiguous device tensors")
+    return t0.dtype == torch.float32
+
+
+def swin_attn_fwd_train(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, stream=None):
+    """Training forward over a grid list ((H, W), ...): returns (out, lse)."""
+    import torch
+    f32 = _check_tensors(q, k, v)
+    B, L, heads, d = q.shape
+    out = torch.empty_like(q)
+    lse = torch.empty((B, heads, L), dtype=torch.float32, device=q.device)
+    fla_swin_attn_ms_fwd_lse(q, k, v, out, lse, B, heads, grids, d, window, shift, pad_mode, stream,
+                             f32=f32)
+    return out, lse
+
+
+def swin_attn_bwd(q, k, v, out, dout, lse, grids, window, shift, pad_mode=FLA_PAD_MASK, stream=None):
+    """Backward over a grid list: returns (dq, dk, dv); allocates the workspace it needs."""
+    import torch
+    f32 = _check_tensors(q, k, v, out, dout)
+    if lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 tensor")
+    B, L, heads, d = q.shape
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    nbytes = fla_swin_attn_bwd_workspace(B, heads, grids, window, shift, pad_mode)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+    fla_swin_attn_ms_bwd(q, k, v, out, dout, lse, dq, dk, dv, ws, nbytes, B, heads, grids, d, window,
+                         shift, pad_mode, stream, f32=f32)
+    return dq, dk, dv

@@ -112,21 +112,15 @@ int check_arch(int* cus) {
     return ok ? FLA_OK : FLA_ERR_ARCH;
 }
 
-int forward(const void* q, const void* k, const void* v, void* out, int B, int heads, int n_grids,
-            const int* hw, int head_dim, int window, int shift, int pad_mode, void* stream,
-            int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t)) {
-    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
-    if (!hw) return FLA_ERR_NULL;
-    bool empty = false;
-    int st = check_sizes(B, heads, n_grids, hw, &empty);
-    if (st != FLA_OK || empty) return st;
-    if (!q || !k || !v || !out) return FLA_ERR_NULL;
-    const uintptr_t mis = (reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) |
-                           reinterpret_cast<uintptr_t>(v) | reinterpret_cast<uintptr_t>(out)) & 15u;
-    if (mis) return FLA_ERR_ALIGN;
-    st = check_scalars(head_dim, window, shift, pad_mode);
-    if (st != FLA_OK) return st;
+// Shape and size limits shared by the forward and backward entry points.  Assumes sizes
+// and scalars were checked; fills the launch geometry.
+struct Problem {
+    int64_t L, tok, kv_rows;
+    Geometry geo;
+};
 
+int check_limits(int B, int heads, int n_grids, const int* hw, int head_dim, int window, int shift,
+                 int pad_mode, int elem_bytes, Problem* pr) {
     // sizes, in an order that cannot overflow int64 before the bound check
     int64_t L = 0;
     for (int i = 0; i < n_grids; ++i) {
@@ -137,9 +131,8 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     const int64_t kv_rows = L + (pad_mode == FLA_PAD_KVTOKEN ? 1 : 0);
     if (kv_rows >= kMaxElems || tok >= kMaxElems || kv_rows > kMaxElems / tok) return FLA_ERR_TOO_LARGE;
     if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
-    Geometry geo;
-    if (!geometry(B, heads, n_grids, hw, window, shift, &geo)) return FLA_ERR_TOO_LARGE;
-    if (geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    if (!geometry(B, heads, n_grids, hw, window, shift, &pr->geo)) return FLA_ERR_TOO_LARGE;
+    if (pr->geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
     // the kernels address a window with 32-bit byte offsets from its first token, and
     // split a window-local index into (row, col) with a 32-bit multiply-high
     for (int i = 0; i < n_grids; ++i) {
@@ -149,22 +142,24 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
         if (win_rows * W * tok * elem_bytes >= (int64_t(1) << 31)) return FLA_ERR_TOO_LARGE;
         if (win_rows * win_cols * win_cols > (int64_t(1) << 32)) return FLA_ERR_TOO_LARGE;
     }
+    pr->L = L;
+    pr->tok = tok;
+    pr->kv_rows = kv_rows;
+    return FLA_OK;
+}
 
-    const int64_t q_bytes = int64_t(B) * L * tok * elem_bytes;
-    const int64_t kv_bytes = int64_t(B) * kv_rows * tok * elem_bytes;
-    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, k, kv_bytes) ||
-        overlaps(out, q_bytes, v, kv_bytes))
-        return FLA_ERR_ALIAS;
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-    int cus = 0;
-    st = check_arch(&cus);
-    if (st != FLA_OK) return st;
-
+fla::SwinArgs make_args(const Problem& pr, const void* q, const void* k, const void* v, void* out,
+                        float* lse, int B, int heads, int n_grids, int head_dim, int window, int shift,
+                        int pad_mode, int cus) {
+    const Geometry& geo = pr.geo;
     fla::SwinArgs a;
     a.q = q;
     a.k = k;
     a.v = v;
     a.out = out;
+    a.lse = lse;
     a.B = B;
     a.heads = heads;
     a.window = window;
@@ -172,10 +167,10 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     a.origin = geo.origin;
     a.nqb = geo.nqb;
     a.pad_mode = pad_mode;
-    a.L = L;
-    a.tok_stride = tok;
-    a.q_batch_stride = L * tok;
-    a.kv_batch_stride = kv_rows * tok;
+    a.L = pr.L;
+    a.tok_stride = pr.tok;
+    a.q_batch_stride = pr.L * pr.tok;
+    a.kv_batch_stride = pr.kv_rows * pr.tok;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
     a.n_groups = geo.n_groups;
     a.n_cus = cus;
@@ -185,7 +180,120 @@ int forward(const void* q, const void* k, const void* v, void* out, int B, int h
     a.div_heads = fla::FastDiv::make((unsigned)heads);
     a.div_nqb = fla::FastDiv::make((unsigned)geo.nqb);
     a.div_nwin = fla::FastDiv::make((unsigned)geo.n_windows);
+    return a;
+}
+
+// lse: NULL for the plain forward; the training forward passes want_lse and its buffer.
+int forward(const void* q, const void* k, const void* v, void* out, float* lse, bool want_lse, int B,
+            int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
+            void* stream, int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t)) {
+    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
+    if (!hw) return FLA_ERR_NULL;
+    bool empty = false;
+    int st = check_sizes(B, heads, n_grids, hw, &empty);
+    if (st != FLA_OK || empty) return st;
+    if (!q || !k || !v || !out || (want_lse && !lse)) return FLA_ERR_NULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || (want_lse && !aligned16(lse)))
+        return FLA_ERR_ALIGN;
+    st = check_scalars(head_dim, window, shift, pad_mode);
+    if (st != FLA_OK) return st;
+    Problem pr;
+    st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
+    if (st != FLA_OK) return st;
+
+    const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
+    const int64_t kv_bytes = int64_t(B) * pr.kv_rows * pr.tok * elem_bytes;
+    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, k, kv_bytes) ||
+        overlaps(out, q_bytes, v, kv_bytes))
+        return FLA_ERR_ALIAS;
+    if (want_lse) {
+        const int64_t lse_bytes = int64_t(B) * heads * pr.L * 4;
+        if (overlaps(lse, lse_bytes, q, q_bytes) || overlaps(lse, lse_bytes, k, kv_bytes) ||
+            overlaps(lse, lse_bytes, v, kv_bytes) || overlaps(lse, lse_bytes, out, q_bytes))
+            return FLA_ERR_ALIAS;
+    }
+
+    int cus = 0;
+    st = check_arch(&cus);
+    if (st != FLA_OK) return st;
+
+    const fla::SwinArgs a = make_args(pr, q, k, v, out, want_lse ? lse : nullptr, B, heads, n_grids,
+                                      head_dim, window, shift, pad_mode, cus);
     if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
+        (void)hipGetLastError();
+        return FLA_ERR_LAUNCH;
+    }
+    return FLA_OK;
+}
+
+// Workspace bytes of a backward call: one pad-gradient partial per (b, head, window, query
+// block) in KV-token mode, none otherwise.  Assumes the geometry is valid.
+int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
+    if (pad_mode != FLA_PAD_KVTOKEN) return 0;
+    return int64_t(B) * heads * geo.n_windows * geo.nqb * fla::kPadPartial * 4;
+}
+
+int backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
+             const float* lse, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes, int B,
+             int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
+             void* stream, int elem_bytes) {
+    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
+    if (!hw) return FLA_ERR_NULL;
+    bool empty = false;
+    int st = check_sizes(B, heads, n_grids, hw, &empty);
+    if (st != FLA_OK || empty) return st;
+    if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return FLA_ERR_NULL;
+    for (const void* p : {q, k, v, out, dout, static_cast<const void*>(lse), static_cast<const void*>(dq),
+                          static_cast<const void*>(dk), static_cast<const void*>(dv)})
+        if (!aligned16(p)) return FLA_ERR_ALIGN;
+    if (ws && !aligned16(ws)) return FLA_ERR_ALIGN;
+    st = check_scalars(head_dim, window, shift, pad_mode);
+    if (st != FLA_OK) return st;
+    Problem pr;
+    st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
+    if (st != FLA_OK) return st;
+    // the bf16 kernel holds a whole window (at most kBwdMaxTokens = kQueryBlock tokens)
+    if (elem_bytes == 2 && pr.geo.nqb > 1) return FLA_ERR_UNSUPPORTED;
+    const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
+    if (need > 0 && (!ws || ws_bytes < uint64_t(need))) return FLA_ERR_WORKSPACE;
+
+    const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
+    const int64_t kv_bytes = int64_t(B) * pr.kv_rows * pr.tok * elem_bytes;
+    const int64_t lse_bytes = int64_t(B) * heads * pr.L * 4;
+    struct Range {
+        const void* p;
+        int64_t n;
+    };
+    const Range inputs[] = {{q, q_bytes}, {k, kv_bytes}, {v, kv_bytes}, {out, q_bytes}, {dout, q_bytes},
+                            {lse, lse_bytes}};
+    const Range outputs[] = {{dq, q_bytes}, {dk, kv_bytes}, {dv, kv_bytes}, {ws, need}};
+    for (int i = 0; i < 4; ++i) {
+        if (outputs[i].n == 0) continue;
+        for (const Range& r : inputs)
+            if (overlaps(outputs[i].p, outputs[i].n, r.p, r.n)) return FLA_ERR_ALIAS;
+        for (int j = 0; j < i; ++j)
+            if (outputs[j].n > 0 && overlaps(outputs[i].p, outputs[i].n, outputs[j].p, outputs[j].n))
+                return FLA_ERR_ALIAS;
+    }
+
+    int cus = 0;
+    st = check_arch(&cus);
+    if (st != FLA_OK) return st;
+
+    fla::SwinBwdArgs a;
+    a.f = make_args(pr, q, k, v, nullptr, nullptr, B, heads, n_grids, head_dim, window, shift, pad_mode, cus);
+    a.out = out;
+    a.dout = dout;
+    a.lse = lse;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.ws = static_cast<float*>(ws);
+    a.scale = (float)(1.0 / std::sqrt((double)head_dim));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = elem_bytes == 2 ? fla::launch_swin_bwd_bf16(a, s) : fla::launch_swin_bwd_f32(a, s);
+    if (e == hipSuccess && pad_mode == FLA_PAD_KVTOKEN) e = fla::launch_swin_bwd_pad_reduce(a, elem_bytes, s);
+    if (e != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;
     }
@@ -217,8 +325,10 @@ double grid_pairs(int H, int W, int window, int shift, int pad_mode) {
     return pairs;
 }
 
+// backward: five products instead of two (S, dP, dV, dK, dQ), and q, k, v, out, dout read
+// with dq, dk, dv written (8 tensors instead of 4) plus the fp32 log-sum-exp per query.
 int work(int B, int heads, int n_grids, const int* hw, int head_dim, int window, int shift,
-         int pad_mode, int elem_bytes, double* flops, double* bytes) {
+         int pad_mode, int elem_bytes, bool bwd, double* flops, double* bytes) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
     bool empty = false;
@@ -234,9 +344,11 @@ int work(int B, int heads, int n_grids, const int* hw, int head_dim, int window,
             pairs += grid_pairs(hw[2 * i], hw[2 * i + 1], window, shift, pad_mode);
             tokens += double(hw[2 * i]) * hw[2 * i + 1];
         }
-    const double rows = empty ? 0.0 : 4.0 * tokens + (pad_mode == FLA_PAD_KVTOKEN ? 2.0 : 0.0);
-    if (flops) *flops = 4.0 * head_dim * double(heads) * B * pairs;
-    if (bytes) *bytes = rows * B * double(heads) * head_dim * elem_bytes;
+    const double pad_rows = pad_mode == FLA_PAD_KVTOKEN ? (bwd ? 4.0 : 2.0) : 0.0;
+    const double rows = empty ? 0.0 : (bwd ? 8.0 : 4.0) * tokens + pad_rows;
+    if (flops) *flops = (bwd ? 10.0 : 4.0) * head_dim * double(heads) * B * pairs;
+    if (bytes)
+        *bytes = rows * B * double(heads) * head_dim * elem_bytes + (bwd ? 4.0 * tokens * B * heads : 0.0);
     return FLA_OK;
 }
 
@@ -248,46 +360,134 @@ int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out, in
                       int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
                       void* stream) {
     const int hw[2] = {Hgrid, Wgrid};
-    return forward(q, k, v, out, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
-                   fla::launch_swin_fwd_bf16);
+    return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
+                   stream, 2, fla::launch_swin_fwd_bf16);
 }
 
 int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                           int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
                           int pad_mode, void* stream) {
     const int hw[2] = {Hgrid, Wgrid};
-    return forward(q, k, v, out, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 4,
-                   fla::launch_swin_fwd_f32);
+    return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
+                   stream, 4, fla::launch_swin_fwd_f32);
 }
 
 int fla_swin_attn_ms_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
                          int n_grids, const int* grid_hw, int head_dim, int window, int shift,
                          int pad_mode, void* stream) {
-    return forward(q, k, v, out, B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode,
-                   stream, 2, fla::launch_swin_fwd_bf16);
+    return forward(q, k, v, out, nullptr, false, B, heads, n_grids, grid_hw, head_dim, window, shift,
+                   pad_mode, stream, 2, fla::launch_swin_fwd_bf16);
 }
 
 int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                              int heads, int n_grids, const int* grid_hw, int head_dim, int window,
                              int shift, int pad_mode, void* stream) {
-    return forward(q, k, v, out, B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode,
-                   stream, 4, fla::launch_swin_fwd_f32);
+    return forward(q, k, v, out, nullptr, false, B, heads, n_grids, grid_hw, head_dim, window, shift,
+                   pad_mode, stream, 4, fla::launch_swin_fwd_f32);
+}
+
+int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse, int B,
+                          int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                          int pad_mode, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
+                   fla::launch_swin_fwd_bf16);
+}
+
+int fla_swin_attn_fwd_lse_f32(const float* q, const float* k, const float* v, float* out, float* lse,
+                              int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
+                              int shift, int pad_mode, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 4,
+                   fla::launch_swin_fwd_f32);
+}
+
+int fla_swin_attn_ms_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
+                             int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                             int window, int shift, int pad_mode, void* stream) {
+    return forward(q, k, v, out, lse, true, B, heads, n_grids, grid_hw, head_dim, window, shift,
+                   pad_mode, stream, 2, fla::launch_swin_fwd_bf16);
+}
+
+int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
+                                 float* lse, int B, int heads, int n_grids, const int* grid_hw,
+                                 int head_dim, int window, int shift, int pad_mode, void* stream) {
+    return forward(q, k, v, out, lse, true, B, heads, n_grids, grid_hw, head_dim, window, shift,
+                   pad_mode, stream, 4, fla::launch_swin_fwd_f32);
+}
+
+int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,
+                                int shift, int pad_mode, size_t* bytes) {
+    if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
+    if (!grid_hw || !bytes) return FLA_ERR_NULL;
+    bool empty = false;
+    int st = check_sizes(B, heads, n_grids, grid_hw, &empty);
+    if (st != FLA_OK) return st;
+    st = check_scalars(fla::kHeadDim, window, shift, pad_mode);
+    if (st != FLA_OK) return st;
+    if (empty) {
+        *bytes = 0;
+        return FLA_OK;
+    }
+    Problem pr;
+    st = check_limits(B, heads, n_grids, grid_hw, fla::kHeadDim, window, shift, pad_mode, 2, &pr);
+    if (st != FLA_OK) return st;
+    *bytes = (size_t)workspace_bytes(B, heads, pr.geo, pad_mode);
+    return FLA_OK;
+}
+
+int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                      const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                      size_t workspace_bytes, int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                      int window, int shift, int pad_mode, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
+                    head_dim, window, shift, pad_mode, stream, 2);
+}
+
+int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,
+                          const float* dout, const float* lse, float* dq, float* dk, float* dv,
+                          void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
+                          int Wgrid, int head_dim, int window, int shift, int pad_mode, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
+                    head_dim, window, shift, pad_mode, stream, 4);
+}
+
+int fla_swin_attn_ms_bwd(const void* q, const void* k, const void* v, const void* out,
+                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                         void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
+                         const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
+                         void* stream) {
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, n_grids,
+                    grid_hw, head_dim, window, shift, pad_mode, stream, 2);
+}
+
+int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, const float* out,
+                             const float* dout, const float* lse, float* dq, float* dk, float* dv,
+                             void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
+                             const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
+                             void* stream) {
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, n_grids,
+                    grid_hw, head_dim, window, shift, pad_mode, stream, 4);
 }
 
 const char* fla_status_string(int status) {
     switch (status) {
         case FLA_OK: return "ok";
         case FLA_ERR_SHAPE: return "B, heads and grid sizes must be >= 0 (1 to 8 grids)";
-        case FLA_ERR_NULL: return "q, k, v and out must be non-NULL";
-        case FLA_ERR_ALIGN: return "q, k, v and out must be 16-byte aligned";
+        case FLA_ERR_NULL: return "a tensor pointer (or the grid list) is NULL";
+        case FLA_ERR_ALIGN: return "tensor pointers must be 16-byte aligned";
         case FLA_ERR_HEAD_DIM: return "head_dim must be 64";
         case FLA_ERR_WINDOW: return "window must be >= 1";
         case FLA_ERR_SHIFT: return "shift must satisfy 0 <= shift < window";
         case FLA_ERR_PAD_MODE: return "pad_mode must be FLA_PAD_MASK (0) or FLA_PAD_KVTOKEN (1)";
         case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements, 2^24 workgroups or a 2 GiB window span)";
-        case FLA_ERR_ALIAS: return "out overlaps q, k or v";
+        case FLA_ERR_ALIAS: return "an output overlaps an input or another output";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";
+        case FLA_ERR_UNSUPPORTED: return "the bf16 backward takes windows of at most 256 tokens (window <= 16)";
+        case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
         default: return "unknown status";
     }
 }
@@ -295,13 +495,20 @@ const char* fla_status_string(int status) {
 int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
                        int shift, int pad_mode, int elem_bytes, double* flops, double* bytes) {
     const int hw[2] = {Hgrid, Wgrid};
-    return work(B, heads, 1, hw, head_dim, window, shift, pad_mode, elem_bytes, flops, bytes);
+    return work(B, heads, 1, hw, head_dim, window, shift, pad_mode, elem_bytes, false, flops, bytes);
 }
 
 int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
                           int window, int shift, int pad_mode, int elem_bytes, double* flops,
                           double* bytes) {
-    return work(B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode, elem_bytes, flops,
+    return work(B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode, elem_bytes, false, flops,
+                bytes);
+}
+
+int fla_swin_attn_bwd_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
+                           int window, int shift, int pad_mode, int elem_bytes, double* flops,
+                           double* bytes) {
+    return work(B, heads, n_grids, grid_hw, head_dim, window, shift, pad_mode, elem_bytes, true, flops,
                 bytes);
 }
 

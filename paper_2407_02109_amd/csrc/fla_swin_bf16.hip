@@ -22,7 +22,8 @@
 //      The kernel is held to 128 VGPRs so that 4 waves share each SIMD (2 workgroups per
 //      CU): while one wave waits on the matrix core, another runs its softmax on the
 //      vector ALU, which is the busier of the two units.
-//   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token.  The
+//   3. Epilogue: O^T / l, round to bf16 (RNE), store each query row at its own token; if
+//      asked, also the log-sum-exp m + log(l) of every query (the training forward).  The
 //      result goes through LDS first so that every store writes whole 128-byte rows (8 lanes
 //      x 16 B): stored straight from the MFMA layout, each instruction would write 8-byte
 //      pieces of 32 rows, and those partial-line writes cost about a tenth of the layer.
@@ -30,17 +31,10 @@
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
 // the window and its logit is raised by log2(n_pad)/scale, so in the softmax it carries
 // the weight of the n_pad = window^2 - n virtual slots it stands for.
-#include "fla_swin_internal.h"
+#include "fla_swin_device.h"
 
 namespace fla {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef int v2i __attribute__((ext_vector_type(2)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int D = kHeadDim;     // 64 channels per head
 constexpr int THREADS = 512;    // 8 waves of 64
@@ -50,53 +44,7 @@ constexpr int KT = 32;          // keys per inner tile
 constexpr int KS = D + 8;       // K row stride in LDS, bf16 elements (144 B)
 constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
 constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
-
-// max / sum over lanes l and l ^ 32 (the two halves holding the same query column)
-__device__ __forceinline__ float xhalf_max(float x) {
-    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xhalf_sum(float x) {
-    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// ---- global memory through buffer resources: 32-bit byte offsets from the window's first
-//      token, and hardware range checks (a load outside the resource returns 0, a store
-//      outside it is dropped), so no access can leave the tensor it belongs to.
-constexpr unsigned kOutside = 0x80000000u;   // offset that is always out of range
-constexpr int kMaxRecords = 0x7fffffff;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long long bytes) {
-    const int n = bytes < kMaxRecords ? (int)bytes : kMaxRecords;
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
-}
-__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, unsigned off) {
-    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
-
-// Byte offset of window-local index t (t = row * cols + col, row-major in the window's
-// rectangle) from the window's first token.  row = t / cols is a multiply-high by
-// ceil(2^32 / cols), exact for t * cols < 2^32 (the host guarantees n * cols <= 2^32);
-// cols == 1 uses magic 0 and adds t through one_mask.
-struct WindowAddr {
-    unsigned row_bytes;   // bytes between grid rows: W * heads * head_dim * 2
-    unsigned tok_bytes;   // bytes between adjacent tokens of a row: heads * head_dim * 2
-    unsigned magic, one_mask, cols;
-
-    __device__ __forceinline__ void init(int c, unsigned rowb, unsigned tokb) {
-        cols = (unsigned)c;
-        magic = c > 1 ? (unsigned)(((1ull << 32) + c - 1) / c) : 0u;
-        one_mask = c > 1 ? 0u : 0xffffffffu;
-        row_bytes = rowb;
-        tok_bytes = tokb;
-    }
-    __device__ __forceinline__ unsigned operator()(int t) const {
-        const unsigned r = __umulhi((unsigned)t, magic) + ((unsigned)t & one_mask);
-        const unsigned c = (unsigned)t - r * cols;
-        return r * row_bytes + c * tok_bytes;
-    }
-};
+constexpr float kLn2 = 0.693147180559945309f;
 
 __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, const uint16_t* __restrict__ Vt,
                                             bool masked, int t0, int kc0, int nk, int n, float pad_bias_raw,
@@ -160,6 +108,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
 
 // 4 waves per SIMD: at most 128 VGPRs, and the LDS footprint (2 x 69 KB) admits the two
 // workgroups per CU that this takes.
+template <bool MULTI>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void swin_fwd_bf16_kernel(SwinArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * KS];
@@ -178,7 +127,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const int win = (int)(id2 - id3 * (unsigned)nwin);
     const int b = (int)id3;
 
-    const WindowRect wr = window_rect(a, win);
+    const WindowRect wr = window_rect<MULTI>(a, win);
     const int n = wr.rows * wr.cols;
     const int q_begin = qblk * kQueryBlock;
     if (q_begin >= n) return;   // whole workgroup: this window has fewer query blocks
@@ -305,7 +254,14 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     //      per row, 16 bytes per lane.
     __syncthreads();
     if (nq > 0) {
-        const float inv = 1.f / xhalf_sum(l_run);
+        const float lsum = xhalf_sum(l_run);
+        const float inv = 1.f / lsum;
+        if (a.lse != nullptr && h == 0 && li < nq) {
+            // log of the softmax denominator over the logits q.k / sqrt(d), natural units
+            const long long row = ((long long)b * a.heads + head) * L + wr.tok0 +
+                                  addr.token(wq0 + li, (unsigned)wr.W);
+            a.lse[row] = (m_run * a.scale_log2 + log2f(lsum)) * kLn2;
+        }
         uint16_t* orow = Ks + (wave * QW + li) * KS;
         for (int db = 0; db < 2; ++db)
             for (int rg = 0; rg < 4; ++rg) {
@@ -328,7 +284,9 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream) {
     SwinArgs args = a;
     void* params[] = {&args};
-    return hipLaunchKernel(reinterpret_cast<const void*>(&swin_fwd_bf16_kernel),
+    const void* fn = a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true>)
+                                   : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false>);
+    return hipLaunchKernel(fn,
                            dim3((unsigned)a.n_groups), dim3(THREADS), params, 0, stream);
 }
 

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     const int win = (int)(id % nwin);
     const int b = (int)(id / nwin);
 
-    const WindowRect wr = window_rect(a, win);
+    const WindowRect wr = window_rect<true>(a, win);
     const int n = wr.rows * wr.cols;
     const int q_begin = qblk * kQueryBlock;
     if (q_begin >= n) return;
@@ -113,6 +113,11 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     }
 
     if (active) {
+        if (a.lse != nullptr) {
+            const int r = t / wr.cols;
+            const long long tok = wr.tok0 + (long long)r * wr.W + (t - r * wr.cols);
+            a.lse[((long long)b * a.heads + head) * L + tok] = (m_run + log2f(l_run)) * 0.693147180559945309f;
+        }
         const float inv = 1.f / l_run;
         float4* row = reinterpret_cast<float4*>(og + token_off(t));
         for (int i = 0; i < D / 4; ++i)

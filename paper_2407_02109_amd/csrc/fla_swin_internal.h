@@ -48,6 +48,7 @@ struct SwinArgs {
     const void* k;
     const void* v;
     void* out;
+    float* lse;                 // optional [B, heads, L] log-sum-exp output (NULL: not kept)
     int B, heads;
     int window, shift;
     int origin;                 // (window - shift) % window: virtual tokens in front of each axis
@@ -68,6 +69,31 @@ struct SwinArgs {
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
+constexpr int kBwdMaxTokens = 256;   // window tokens the bf16 backward kernel holds (window <= 16)
+constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: dk then dv
+
+// Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
+// out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,
+// window, query block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * nqb
+// + qblk][0:64] = dk part, [64:128] = dv part (written only by blocks whose window has
+// virtual slots, and summed by the pad reduce kernel).
+struct SwinBwdArgs {
+    SwinArgs f;
+    const void* out;
+    const void* dout;
+    const float* lse;
+    void* dq;
+    void* dk;
+    void* dv;
+    float* ws;
+    float scale;                // 1 / sqrt(head_dim)
+};
+
+hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
+hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
+// sums the partials of ws into row L of dk and dv (elem_bytes 2: bf16, 4: fp32)
+hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
+
 // Window `win` (numbered over all grids, raster order within a grid), clipped to its grid.
 struct WindowRect {
     int y0, x0, rows, cols;
@@ -75,10 +101,14 @@ struct WindowRect {
     int64_t tok0;               // index of its first token (y0, x0) within a batch entry
 };
 
+// MULTI = false: the launch has one grid, and the scan over the grid list (dependent
+// kernel-argument loads) is skipped.
+template <bool MULTI>
 __device__ __forceinline__ WindowRect window_rect(const SwinArgs& a, int win) {
     int g = 0;
-    for (int i = 1; i < kMaxGrids; ++i)
-        if (i < a.n_grids && win >= a.grid[i].win_begin) g = i;
+    if constexpr (MULTI)
+        for (int i = 1; i < kMaxGrids; ++i)
+            if (i < a.n_grids && win >= a.grid[i].win_begin) g = i;
     const GridDesc& G = a.grid[g];
     const int lw = win - G.win_begin;
     const int wy = (int)G.div_nwx.div((unsigned)lw);

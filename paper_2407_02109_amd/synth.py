@@ -114,6 +114,17 @@ def make_inputs(wl: Workload, device: str | torch.device = "cpu"):
     return tuple(out)
 
 
+def make_grad(wl: Workload, device: str | torch.device = "cpu"):
+    """Upstream gradient dOut for a backward pass: N(0, 1) of q's shape, drawn from its own
+    generator seeded with wl.seed + 1000 (so q, k, v stay those of make_inputs), rounded to
+    wl's dtype."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(wl.seed + 1000)
+    t = torch.randn(wl.B, wl.L, wl.heads, wl.head_dim, generator=g, dtype=torch.float32)
+    t = t.to(wl.torch_dtype).contiguous()
+    return t.to(device) if str(device) != "cpu" else t
+
+
 def to_f64_numpy(t):
     """Exact float64 copy of a CPU/GPU tensor (bf16 and fp32 embed exactly in fp64)."""
     return t.detach().to("cpu", torch.float64).numpy()

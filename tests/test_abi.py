@@ -35,10 +35,13 @@ def lib():
 
 
 def test_header_declares_the_entry_points():
-    assert _header_functions() == ["fla_status_string", "fla_swin_attn_fwd",
-                                   "fla_swin_attn_fwd_f32", "fla_swin_attn_ms_fwd",
-                                   "fla_swin_attn_ms_fwd_f32", "fla_swin_attn_ms_work",
-                                   "fla_swin_attn_work"]
+    assert _header_functions() == sorted([
+        "fla_status_string", "fla_swin_attn_fwd", "fla_swin_attn_fwd_f32", "fla_swin_attn_ms_fwd",
+        "fla_swin_attn_ms_fwd_f32", "fla_swin_attn_ms_work", "fla_swin_attn_work",
+        "fla_swin_attn_fwd_lse", "fla_swin_attn_fwd_lse_f32", "fla_swin_attn_ms_fwd_lse",
+        "fla_swin_attn_ms_fwd_lse_f32", "fla_swin_attn_bwd_workspace", "fla_swin_attn_bwd",
+        "fla_swin_attn_bwd_f32", "fla_swin_attn_ms_bwd", "fla_swin_attn_ms_bwd_f32",
+        "fla_swin_attn_bwd_work"])
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -254,3 +257,132 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(fb, "library_path", lambda: str(tmp_path / "libfla_swin.so"))
     with pytest.raises(fb.FlaError):
         fb.load_library()
+
+
+# ---- training forward and backward entry points -------------------------------------
+LSE, DOUT, DQ, DK, DV, WS = 0x50000000, 0x60000000, 0x70000000, 0x80000000, 0x90000000, 0xA0000000
+
+
+def _call_lse(f32=False, lse=LSE, **kw):
+    a = dict(GOOD)
+    a.update({k: v for k, v in kw.items() if k in GOOD})
+    ptrs = dict(q=Q, k=K, v=V, out=OUT)
+    ptrs.update({k: v for k, v in kw.items() if k in ptrs})
+    return fb.fla_swin_attn_fwd_lse(ptrs["q"], ptrs["k"], ptrs["v"], ptrs["out"], lse, a["B"], a["heads"],
+                                    a["Hgrid"], a["Wgrid"], a["head_dim"], a["window"], a["shift"],
+                                    a["pad_mode"], 0, check=False, f32=f32)
+
+
+def _call_bwd(f32=False, ws_bytes=1 << 24, **kw):
+    a = dict(GOOD)
+    a.update({k: v for k, v in kw.items() if k in GOOD})
+    p = dict(q=Q, k=K, v=V, out=OUT, dout=DOUT, lse=LSE, dq=DQ, dk=DK, dv=DV, ws=WS)
+    p.update({k: v for k, v in kw.items() if k in p})
+    return fb.fla_swin_attn_bwd(p["q"], p["k"], p["v"], p["out"], p["dout"], p["lse"], p["dq"], p["dk"],
+                                p["dv"], p["ws"], ws_bytes, a["B"], a["heads"], a["Hgrid"], a["Wgrid"],
+                                a["head_dim"], a["window"], a["shift"], a["pad_mode"], 0, check=False,
+                                f32=f32)
+
+
+LSE_CASES = [
+    ("FLA_ERR_NULL", dict(lse=0)), ("FLA_ERR_NULL", dict(q=0)), ("FLA_ERR_ALIGN", dict(lse=LSE + 4)),
+    ("FLA_ERR_SHIFT", dict(shift=20)),
+    ("FLA_ERR_ALIAS", dict(lse=OUT + 64)), ("FLA_ERR_ALIAS", dict(lse=Q)),
+    ("FLA_ERR_ALIAS", dict(lse=K - 64 * 64 * 12 * 4 + 16)),   # lse's last bytes run into k
+]
+
+
+@pytest.mark.parametrize("f32", [False, True], ids=["bf16", "f32"])
+@pytest.mark.parametrize("status,kw", LSE_CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(LSE_CASES)])
+def test_lse_argument_checks(lib, f32, status, kw):
+    assert _call_lse(f32=f32, **kw) == _header_enum("FLA")[status]
+
+
+TOK_B = 64 * 64 * 12 * 64 * 2      # bytes of one bf16 tensor of GOOD
+BWD_CASES = [
+    ("FLA_ERR_SHAPE", dict(B=-1)),
+    ("FLA_ERR_NULL", dict(out=0)), ("FLA_ERR_NULL", dict(dout=0)), ("FLA_ERR_NULL", dict(lse=0)),
+    ("FLA_ERR_NULL", dict(dq=0)), ("FLA_ERR_NULL", dict(dk=0)), ("FLA_ERR_NULL", dict(dv=0)),
+    ("FLA_ERR_ALIGN", dict(dout=DOUT + 2)), ("FLA_ERR_ALIGN", dict(dv=DV + 8)),
+    ("FLA_ERR_ALIGN", dict(ws=WS + 4)), ("FLA_ERR_ALIGN", dict(lse=LSE + 4)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=128)), ("FLA_ERR_WINDOW", dict(window=0)),
+    ("FLA_ERR_SHIFT", dict(shift=16)), ("FLA_ERR_PAD_MODE", dict(pad_mode=5)),
+    ("FLA_ERR_TOO_LARGE", dict(Hgrid=1 << 20, Wgrid=1 << 20)),
+    ("FLA_ERR_WORKSPACE", dict(pad_mode=1, ws=0)), ("FLA_ERR_WORKSPACE", dict(pad_mode=1, ws_bytes=16)),
+    ("FLA_ERR_ALIAS", dict(dq=Q)), ("FLA_ERR_ALIAS", dict(dk=DOUT + 128)), ("FLA_ERR_ALIAS", dict(dv=LSE)),
+    ("FLA_ERR_ALIAS", dict(dv=DK + 64)), ("FLA_ERR_ALIAS", dict(pad_mode=1, ws=DQ + TOK_B - 16)),
+    ("FLA_ERR_ALIAS", dict(dq=OUT + TOK_B - 16)),
+]
+
+
+@pytest.mark.parametrize("f32", [False, True], ids=["bf16", "f32"])
+@pytest.mark.parametrize("status,kw", BWD_CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(BWD_CASES)])
+def test_bwd_argument_checks(lib, f32, status, kw):
+    kw = dict(kw)
+    if f32 and status == "FLA_ERR_ALIAS" and kw.get("ws") == DQ + TOK_B - 16:
+        kw["ws"] = DQ + 2 * TOK_B - 16
+    if f32 and status == "FLA_ERR_ALIAS" and kw.get("dq") == OUT + TOK_B - 16:
+        kw["dq"] = OUT + 2 * TOK_B - 16
+    assert _call_bwd(f32=f32, **kw) == _header_enum("FLA")[status]
+
+
+def test_bwd_unsupported_window_only_for_bf16(lib):
+    codes = _header_enum("FLA")
+    # 17 x 17 = 289 tokens per window: over the bf16 kernel's 256
+    assert _call_bwd(window=17, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_bwd(f32=True, window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    # a 32-wide window on a 4-row grid holds 128 tokens: fine
+    assert _call_bwd(Hgrid=4, window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+
+
+def test_bwd_mask_mode_needs_no_workspace(lib):
+    codes = _header_enum("FLA")
+    st = _call_bwd(ws=0, ws_bytes=0)
+    assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"])
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_training_entry_points_without_device_report_arch(lib):
+    codes = _header_enum("FLA")
+    assert _call_lse() == codes["FLA_ERR_ARCH"] and _call_lse(f32=True) == codes["FLA_ERR_ARCH"]
+    assert _call_bwd() == codes["FLA_ERR_ARCH"] and _call_bwd(f32=True) == codes["FLA_ERR_ARCH"]
+    assert _call_bwd(pad_mode=1) == codes["FLA_ERR_ARCH"]
+
+
+def test_empty_training_calls_are_ok(lib):
+    assert _call_lse(B=0, lse=0, q=0) == 0
+    assert _call_bwd(heads=0, dq=0, ws=0, ws_bytes=0) == 0
+
+
+@pytest.mark.parametrize("grids,k,s,pm", [
+    ([(256, 256)], 16, 8, 1), ([(64, 64)], 16, 8, 0), ([(150, 203)], 16, 8, 1),
+    ([(128, 128), (32, 32)], 16, 8, 1), ([(40, 24)], 20, 10, 1), ([(3, 3)], 1, 0, 1)])
+def test_bwd_workspace_size(lib, grids, k, s, pm):
+    B, heads = 2, 3
+    n_win = sum(len(O.window_sizes(h, w, k, s)) for h, w in grids)
+    nqb = max(-(-max(sz for h, w in grids for sz in O.window_sizes(h, w, k, s)) // 256), 1)
+    want = B * heads * n_win * nqb * 128 * 4 if pm == 1 else 0
+    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, pm) == want
+    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, 0) == 0
+
+
+def test_bwd_workspace_errors(lib):
+    codes = _header_enum("FLA")
+    n = ctypes.c_size_t()
+    arr = (ctypes.c_int * 2)(8, 8)
+    assert lib.fla_swin_attn_bwd_workspace(1, 1, 1, arr, 4, 4, 1, ctypes.byref(n)) == codes["FLA_ERR_SHIFT"]
+    assert lib.fla_swin_attn_bwd_workspace(1, 1, 1, arr, 4, 0, 1, None) == codes["FLA_ERR_NULL"]
+    assert lib.fla_swin_attn_bwd_workspace(1, 1, 0, arr, 4, 0, 1, ctypes.byref(n)) == codes["FLA_ERR_SHAPE"]
+
+
+@pytest.mark.parametrize("grids,k,s,pm", [
+    ([(256, 256)], 16, 8, 0), ([(256, 256)], 16, 8, 1), ([(150, 203)], 16, 8, 0),
+    ([(128, 128), (32, 32)], 16, 8, 1), ([(20, 13)], 8, 3, 1)])
+def test_bwd_work_counts(lib, grids, k, s, pm):
+    B, heads = 2, 12
+    for eb in (2, 4):
+        f, b = fb.fla_swin_attn_bwd_work(B, heads, grids, 64, k, s, pm, eb)
+        f0, b0 = O.ms_work_counts(B, heads, grids, 64, k, s, pm, eb)
+        L = sum(h * w for h, w in grids)
+        assert f == 2.5 * f0                           # five products instead of two
+        assert b == 2 * b0 + 4 * B * heads * L         # eight tensors instead of four, plus lse

@@ -1,0 +1,247 @@
+"""GPU parity of the training forward (log-sum-exp) and the backward pass against the fp64
+oracle, through the C ABI.
+
+Tolerances.  A gradient tensor has no fixed scale (dq and dk carry the factor 1/sqrt(d)),
+so errors are measured against M = max |reference| of that tensor:
+  * bf16: max |err| <= 2e-2 M and mean |err| <= 2e-3 M -- the forward's bf16 bounds for
+    outputs of unit scale.  The kernel rounds P and dS to bf16 (relative 2^-9) before their
+    products and the outputs once more; a CPU emulation of exactly these roundings on full
+    16x16 windows stays below 1e-2 M (max) and 5e-4 M (mean), also with 1% of keys x8.
+  * fp32: max |err| <= 1e-5 M.
+  * log-sum-exp, natural log: bf16 4e-3 absolute -- the bf16 forward sums probabilities
+    rounded to bf16 (relative 2^-9 each, so the sum is off by at most 2^-9 relative and its
+    log by at most 2^-9 ~ 1.95e-3), twice that for margin; fp32 1e-5.
+A reference that is exactly zero (one-token windows) instead needs |got| <= 1e-5.
+Outputs start as NaN so that an unwritten element fails."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from oracle import swin_oracle as SO
+from paper_2407_02109_amd import binding as fb
+from paper_2407_02109_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+BF16_MAX, BF16_MEAN, F32_MAX = 2e-2, 2e-3, 1e-5
+LSE_BF16, LSE_F32 = 4e-3, 1e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fb.load_library()
+
+
+def _say(msg):
+    print("[case] %s" % msg, flush=True)
+
+
+def _wl(B, heads, H, W, k, s, dtype, pm, seed, grids=()):
+    return synth.Workload("case", B, heads, H, W, 64, k, s, dtype, seed=seed, pad_mode=pm, grids=grids)
+
+
+def _train(wl, q, k, v, dout):
+    """GPU training forward + backward; returns out, lse, dq, dk, dv (device tensors)."""
+    B, L, heads, d = q.shape
+    f32 = q.dtype == torch.float32
+    out = torch.full_like(q, float("nan"))
+    lse = torch.full((B, heads, L), float("nan"), dtype=torch.float32, device=q.device)
+    grids = wl.grid_list
+    fb.fla_swin_attn_ms_fwd_lse(q, k, v, out, lse, B, heads, grids, d, wl.window, wl.shift, wl.pad_mode,
+                                f32=f32)
+    dq, dk, dv = (torch.full_like(t, float("nan")) for t in (q, k, v))
+    nbytes = fb.fla_swin_attn_bwd_workspace(B, heads, grids, wl.window, wl.shift, wl.pad_mode)
+    ws = torch.full((max(nbytes // 4, 4),), float("nan"), dtype=torch.float32, device=q.device)
+    fb.fla_swin_attn_ms_bwd(q, k, v, out, dout, lse, dq, dk, dv, ws, nbytes, B, heads, grids, d,
+                            wl.window, wl.shift, wl.pad_mode, f32=f32)
+    torch.cuda.synchronize()
+    return out, lse, dq, dk, dv
+
+
+def _check_grad(name, got, ref, f32):
+    got = synth.to_f64_numpy(got)
+    assert np.isfinite(got).all(), "%s: non-finite element (unwritten?)" % name
+    M = np.abs(ref).max()
+    if M < 1e-12:
+        # an exactly zero gradient (a one-token window: P = 1 and dS = <dO, v> - <dO, o> = 0);
+        # only fp32 rounding of the two dot products remains
+        assert np.abs(got).max() <= 1e-5, (name, np.abs(got).max())
+        return 0.0
+    err = np.abs(got - ref)
+    if f32:
+        assert err.max() <= F32_MAX * M, (name, err.max() / M)
+    else:
+        assert err.max() <= BF16_MAX * M and err.mean() <= BF16_MEAN * M, (name, err.max() / M, err.mean() / M)
+    return err.max() / M
+
+
+SHAPES = [  # B, heads, H, W, window, shift
+    (2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 2, 23, 41, 12, 5),
+    (1, 1, 9, 7, 16, 0), (1, 2, 5, 6, 1, 0), (1, 2, 16, 16, 16, 0), (1, 2, 33, 17, 5, 2),
+]
+F32_WIDE = [(1, 2, 40, 24, 20, 10), (1, 1, 40, 40, 32, 16)]   # windows of more than 256 tokens
+
+
+def _case(B, heads, H, W, k, s, dtype, pm, seed):
+    wl = _wl(B, heads, H, W, k, s, dtype, pm, seed)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    out, lse, dq, dk, dv = _train(wl, q, kk, v, dout)
+    return wl, (q, kk, v, dout), (out, lse, dq, dk, dv)
+
+
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_lse_and_backward(shape, dtype, pm):
+    B, heads, H, W, k, s = shape
+    _say("bwd %s %s pad_mode=%d" % (shape, dtype, pm))
+    wl, ins, outs = _case(B, heads, H, W, k, s, dtype, pm, seed=100 + sum(shape) + pm)
+    q, kk, v, dout = (synth.to_f64_numpy(t) for t in ins)
+    out, lse, dq, dk, dv = outs
+    f32 = dtype == "f32"
+    # the training forward's output is the plain forward's, bit for bit, and the single-grid
+    # entry point gives what the grid-list one gave
+    ref_out = torch.empty_like(ins[0])
+    fn = fb.fla_swin_attn_fwd_f32 if f32 else fb.fla_swin_attn_fwd
+    fn(ins[0], ins[1], ins[2], ref_out, B, heads, H, W, 64, k, s, pm)
+    out1 = torch.empty_like(ins[0])
+    lse1 = torch.empty_like(lse)
+    fb.fla_swin_attn_fwd_lse(ins[0], ins[1], ins[2], out1, lse1, B, heads, H, W, 64, k, s, pm, f32=f32)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref_out) and torch.equal(out1, out) and torch.equal(lse1, lse)
+    lse_ref = O.swin_attention_lse(q, kk, v, H, W, k, s, pm)
+    lerr = np.abs(synth.to_f64_numpy(lse) - lse_ref).max()
+    assert lerr <= (LSE_F32 if f32 else LSE_BF16), lerr
+    gq, gk, gv = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
+    for name, got, ref in (("dq", dq, gq), ("dk", dk, gk), ("dv", dv, gv)):
+        _check_grad(name, got, ref, f32)
+    if pm == 1:   # the pad row on its own scale
+        _check_grad("dk_pad", dk[:, -1], gk[:, -1], f32)
+        _check_grad("dv_pad", dv[:, -1], gv[:, -1], f32)
+
+
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+@pytest.mark.parametrize("shape", F32_WIDE, ids=lambda s: "x".join(map(str, s)))
+def test_f32_backward_wide_windows(shape, pm):
+    B, heads, H, W, k, s = shape
+    _say("bwd f32 wide %s pad_mode=%d" % (shape, pm))
+    wl, ins, outs = _case(B, heads, H, W, k, s, "f32", pm, seed=7 + pm)
+    q, kk, v, dout = (synth.to_f64_numpy(t) for t in ins)
+    _, lse, dq, dk, dv = outs
+    assert np.abs(synth.to_f64_numpy(lse) - O.swin_attention_lse(q, kk, v, H, W, k, s, pm)).max() <= LSE_F32
+    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)):
+        _check_grad(name, got, ref, True)
+
+
+def test_bf16_backward_rejects_windows_over_256_tokens():
+    B, heads, H, W = 1, 1, 40, 24
+    wl = _wl(B, heads, H, W, 20, 10, "bf16", 0, 1)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    z = torch.zeros_like(q)
+    lse = torch.zeros((B, heads, H * W), dtype=torch.float32, device="cuda")
+    rc = fb.fla_swin_attn_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
+                              torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, check=False)
+    assert rc == 12   # FLA_ERR_UNSUPPORTED
+    # a 16-wide window on a grid only 16 tokens tall but wide is fine
+    rc = fb.fla_swin_attn_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
+                              torch.empty_like(v), None, 0, B, heads, H, W, 64, 16, 0, 0, check=False)
+    torch.cuda.synchronize()
+    assert rc == 0
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+def test_multiscale_backward(dtype, pm):
+    grids = ((40, 36), (9, 9), (3, 20))
+    _say("bwd ms %s %s pad_mode=%d" % (grids, dtype, pm))
+    wl = _wl(2, 2, 40, 36, 16, 8, dtype, pm, 21 + pm, grids=grids)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    _, lse, dq, dk, dv = _train(wl, q, kk, v, dout)
+    qn, kn, vn, dn = (synth.to_f64_numpy(t) for t in (q, kk, v, dout))
+    lerr = np.abs(synth.to_f64_numpy(lse) - O.swin_attention_ms_lse(qn, kn, vn, grids, 16, 8, pm)).max()
+    assert lerr <= (LSE_F32 if dtype == "f32" else LSE_BF16)
+    ref = O.swin_attention_ms_bwd(qn, kn, vn, dn, grids, 16, 8, pm)
+    for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+        _check_grad(name, got, r, dtype == "f32")
+
+
+def test_workspace_contents_are_ignored():
+    wl = _wl(1, 2, 37, 29, 16, 8, "bf16", 1, 5)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    first = _train(wl, q, kk, v, dout)   # workspace starts as NaN inside _train
+    B, L, heads, d = q.shape
+    nbytes = fb.fla_swin_attn_bwd_workspace(B, heads, wl.grid_list, 16, 8, 1)
+    ws = torch.full((nbytes // 4,), 1e30, dtype=torch.float32, device="cuda")
+    dq, dk, dv = (torch.empty_like(t) for t in (q, kk, v))
+    fb.fla_swin_attn_bwd(q, kk, v, first[0], dout, first[1], dq, dk, dv, ws, nbytes, B, heads, wl.H, wl.W,
+                         d, 16, 8, 1)
+    torch.cuda.synchronize()
+    for a, b in zip((dq, dk, dv), first[2:]):
+        assert torch.equal(a, b)
+
+
+# ---- full size: sampled windows against the oracle, computed window by window ---------
+def _window_rects(H, W, k, s):
+    ry = SO._region(np.arange(H), k, s)
+    rx = SO._region(np.arange(W), k, s)
+    ys = [np.flatnonzero(ry == r) for r in np.unique(ry)]
+    xs = [np.flatnonzero(rx == r) for r in np.unique(rx)]
+    return [(y[0], y[-1] + 1, x[0], x[-1] + 1) for y in ys for x in xs]
+
+
+def _window_grads(q, kk, v, dout, H, W, rect, k, pm, L):
+    """Oracle gradients of one window's tokens: the window alone is a grid of one region
+    (window k, no shift), and in KV-token mode keeps its pad multiplicity k^2 - n."""
+    y0, y1, x0, x1 = rect
+    idx = (np.arange(y0, y1)[:, None] * W + np.arange(x0, x1)[None, :]).ravel()
+    rows = np.concatenate([idx, [L]]) if pm else idx
+    g = O.swin_attention_bwd(q[:, idx], kk[:, rows], v[:, rows], dout[:, idx], y1 - y0, x1 - x0, k, 0, pm)
+    return idx, g
+
+
+@pytest.mark.parametrize("name", ["img4096", "img4096_kv"])
+def test_full_size_sampled_windows(name):
+    wl = synth.WORKLOADS[name]
+    _say("bwd full size %s" % name)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    out1 = _train(wl, q, kk, v, dout)
+    out2 = _train(wl, q, kk, v, dout)
+    for a, b in zip(out1, out2):
+        assert torch.equal(a, b), "backward is not deterministic"
+    _, lse, dq, dk, dv = (synth.to_f64_numpy(t) for t in out1)
+    for t in (lse, dq, dk, dv):
+        assert np.isfinite(t).all()
+    qn, kn, vn, dn = (synth.to_f64_numpy(t) for t in (q, kk, v, dout))
+    H, W, k, s, pm, L = wl.H, wl.W, wl.window, wl.shift, wl.pad_mode, wl.L
+    rects = _window_rects(H, W, k, s)
+    nwx = len(np.unique(SO._region(np.arange(W), k, s)))
+    pick = sorted({0, nwx - 1, len(rects) - nwx, len(rects) - 1, 1, nwx, len(rects) // 2, 5 * nwx + 7})
+    ref = {"dq": [], "dk": [], "dv": []}
+    got = {"dq": [], "dk": [], "dv": []}
+    for i in pick:
+        idx, (gq, gk, gv) = _window_grads(qn, kn, vn, dn, H, W, rects[i], k, pm, L)
+        n = len(idx)
+        for key, gt, rf in (("dq", dq[:, idx], gq), ("dk", dk[:, idx], gk[:, :n]), ("dv", dv[:, idx], gv[:, :n])):
+            got[key].append(gt)
+            ref[key].append(rf)
+    for key in ref:
+        _check_grad(key, torch.from_numpy(np.concatenate(got[key], axis=1)), np.concatenate(ref[key], axis=1),
+                    False)
+    if pm == 1:
+        # the pad row: the sum over every window with virtual slots
+        pk = np.zeros_like(dk[:, L])
+        pv = np.zeros_like(dv[:, L])
+        for rect in rects:
+            if (rect[1] - rect[0]) * (rect[3] - rect[2]) < k * k:
+                idx, (_, gk, gv) = _window_grads(qn, kn, vn, dn, H, W, rect, k, pm, L)
+                pk += gk[:, len(idx)]
+                pv += gv[:, len(idx)]
+        _check_grad("dk_pad", torch.from_numpy(dk[:, L]), pk, False)
+        _check_grad("dv_pad", torch.from_numpy(dv[:, L]), pv, False)
