@@ -8,8 +8,9 @@ kernel).  Inputs are synthetic (seeded N(0,1), see paper_2407_02109_amd/synth.py
 resident in HBM before timing starts.
 
 Prints one JSON line: microseconds per layer (the headline), TFLOP/s and the fraction of
-the bf16 matrix-core peak, the HBM roofline of the kernel, and the fp64 CPU oracle timed
-on this host as a baseline.
+the bf16 matrix-core peak, the HBM roofline of the kernel, the fp64 CPU oracle timed on
+this host as a baseline, and a "backward" object: the same layer's training forward and
+backward pass (dq, dk, dv) with their own roofline.
 """
 from __future__ import annotations
 
@@ -28,27 +29,38 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
-KERNEL_SOURCES = ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
-                  "paper_2407_02109_amd/csrc/fla_swin_internal.h"]
+# the kernel each leg's roofline is about, and the sources its hash covers
+KERNELS = {
+    "fwd": ("swin_fwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
+                              "paper_2407_02109_amd/csrc/fla_swin_internal.h",
+                              "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
+    "bwd": ("swin_bwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bwd_bf16.hip",
+                              "paper_2407_02109_amd/csrc/fla_swin_internal.h",
+                              "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
+}
 
 
-def kernel_hash() -> str:
+def kernel_hash(leg: str = "fwd") -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNELS[leg][1]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def traffic_path(leg: str, workload: str) -> str:
+    return os.path.join(ROOT, "profiles", "traffic_%s%s.json" % ("" if leg == "fwd" else "bwd_", workload))
+
+
+def measured_traffic(workload: str, leg: str = "fwd"):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
     or None when it is missing or was taken on another version of the kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    path = traffic_path(leg, workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_hash") != kernel_hash():
+    if rec.get("kernel_hash") != kernel_hash(leg):
         return None
     return rec.get("bytes_per_launch")
 
@@ -64,9 +76,11 @@ def copy_calibration(nbytes: int = 512 << 20, reps: int = 3):
     torch.cuda.synchronize()
 
 
-def summarize(prof_dir: str, workload: str, command: str):
+def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd"):
     """Turn rocprofv3 CSV output (kernel trace + FETCH_SIZE + WRITE_SIZE passes) into the
-    committed summaries under profiles/: a markdown table and traffic_<workload>.json."""
+    committed summaries under profiles/: a markdown table and the traffic JSON of the leg's
+    kernel (swin_fwd_bf16 or swin_bwd_bf16)."""
+    kname = KERNELS[leg][0]
     import csv
     import glob
     import statistics as st
@@ -78,7 +92,7 @@ def summarize(prof_dir: str, workload: str, command: str):
                 out.extend(csv.DictReader(f))
         return out
 
-    trace = [r for r in rows("trace/**/*kernel_trace.csv") if "swin_fwd_bf16" in r["Kernel_Name"]]
+    trace = [r for r in rows("trace/**/*kernel_trace.csv") if kname in r["Kernel_Name"]]
     # the workload's own launches: the most common grid (the bench also times a one-token
     # launch of the same kernel, for the launch overhead)
     grids = collections.Counter(r["Grid_Size_X"] for r in trace)
@@ -93,7 +107,7 @@ def summarize(prof_dir: str, workload: str, command: str):
             if r["Counter_Name"] != name:
                 continue
             key = r["Dispatch_Id"]
-            if "swin_fwd_bf16" in r["Kernel_Name"]:
+            if kname in r["Kernel_Name"]:
                 per_dispatch[key] = per_dispatch.get(key, 0.0) + float(r["Counter_Value"])
             elif "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= 65536:
                 # the 512 MiB calibration copies (small copies elsewhere have tiny grids)
@@ -106,7 +120,7 @@ def summarize(prof_dir: str, workload: str, command: str):
     traffic = None
     if counters["FETCH_SIZE"] and counters["WRITE_SIZE"] and fetch_scale and write_scale:
         traffic = (counters["FETCH_SIZE"] * 1024 * fetch_scale + counters["WRITE_SIZE"] * 1024 * write_scale)
-    lines = ["# rocprofv3 summary: swin_fwd_bf16_kernel, workload %s" % workload, "",
+    lines = ["# rocprofv3 summary: %s_kernel, workload %s" % (kname, workload), "",
              "Command (run from the repository root on the GPU host):", "", "```", command, "```", ""]
     if durs:
         lines += ["Kernel trace: %d dispatches, duration avg %.2f us, median %.2f us, min %.2f us, max %.2f us"
@@ -121,13 +135,14 @@ def summarize(prof_dir: str, workload: str, command: str):
               "Copy calibration (512 MiB device copy, KiB per dispatch): FETCH_SIZE %s, WRITE_SIZE %s" % (copies["FETCH_SIZE"], copies["WRITE_SIZE"]),
               "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (fetch_scale, write_scale),
               "Traffic per launch (scaled): %s bytes" % (None if traffic is None else int(traffic)),
-              "Kernel source hash: %s" % kernel_hash(), ""]
+              "Kernel source hash: %s" % kernel_hash(leg), ""]
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", "swin_fwd_bf16_%s.md" % workload), "w") as f:
+    with open(os.path.join(ROOT, "profiles", "%s_%s.md" % (kname, workload)), "w") as f:
         f.write("\n".join(lines))
     if traffic is not None:
-        with open(os.path.join(ROOT, "profiles", "traffic_%s.json" % workload), "w") as f:
-            json.dump({"workload": workload, "kernel_hash": kernel_hash(), "bytes_per_launch": int(traffic),
+        with open(traffic_path(leg, workload), "w") as f:
+            json.dump({"workload": workload, "kernel": kname, "kernel_hash": kernel_hash(leg),
+                       "bytes_per_launch": int(traffic),
                        "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],
                        "fetch_scale": fetch_scale, "write_scale": write_scale,
                        "avg_duration_us": st.mean(durs) / 1e3 if durs else None}, f, indent=1)
@@ -214,6 +229,56 @@ def per_call_us(step, stream, calls: int, before=None):
     return out
 
 
+def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
+    """Training on the same layer: the forward that keeps the log-sum-exp, then the backward
+    (dq, dk, dv for a seeded upstream gradient), each timed with events on the stream.  The
+    roofline is that of swin_bwd_bf16_kernel, the backward's dominant kernel."""
+    import torch
+    grids = list(wl.grid_list)
+    B, L, heads, d = qd.shape
+    dout = synth.make_grad(wl).to(qd.device)
+    out = torch.empty_like(qd)
+    lse = torch.empty((B, heads, L), dtype=torch.float32, device=qd.device)
+    dq, dk, dv = torch.empty_like(qd), torch.empty_like(kd), torch.empty_like(vd)
+    nws = binding.fla_swin_attn_bwd_workspace(B, heads, grids, wl.window, wl.shift, wl.pad_mode)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=qd.device)
+
+    def fwd():
+        binding.fla_swin_attn_ms_fwd_lse(qd, kd, vd, out, lse, B, heads, grids, d, wl.window, wl.shift,
+                                         wl.pad_mode, stream)
+
+    def bwd():
+        binding.fla_swin_attn_ms_bwd(qd, kd, vd, out, dout, lse, dq, dk, dv, ws, nws, B, heads, grids, d,
+                                     wl.window, wl.shift, wl.pad_mode, stream)
+
+    def mean_us(fn, n):
+        for _ in range(max(n // 4, 10)):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    fwd_us = mean_us(fwd, steps)
+    fwd()
+    us = mean_us(bwd, steps)
+    p10, p50, p90 = percentiles(per_call_us(bwd, stream, 100))
+    assert torch.isfinite(dq[:, :64].float()).all() and torch.isfinite(dk[:, :64].float()).all()
+    flops, nbytes = binding.fla_swin_attn_bwd_work(B, heads, grids, d, wl.window, wl.shift, wl.pad_mode, 2)
+    tflops = flops / (us * 1e-6) / 1e12
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"us_per_layer": round(us, 3), "steps": steps, "fwd_lse_us": round(fwd_us, 3),
+            "tflops": round(tflops, 2), "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": measured_traffic(wl.name, "bwd")},
+            "alg_flops": flops, "alg_bytes": nbytes,
+            "timing": {"p10_us": p10, "p50_us": p50, "p90_us": p90}}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,10 +295,14 @@ def main() -> int:
     ap.add_argument("--summarize", metavar="PROF_DIR",
                     help="summarise rocprofv3 CSV output into profiles/ and exit (no GPU needed)")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize")
+    ap.add_argument("--leg", default="fwd", choices=["fwd", "bwd"],
+                    help="kernel --summarize is about: the forward or the backward")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward leg")
+    ap.add_argument("--bwd-steps", type=int, default=500, help="timed backward calls")
     args = ap.parse_args()
 
     if args.summarize:
-        summarize(args.summarize, args.workload, args.command)
+        summarize(args.summarize, args.workload, args.command, args.leg)
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -338,6 +407,9 @@ def main() -> int:
                      "cold_p10_us": c10, "cold_p50_us": c50, "cold_p90_us": c90,
                      "launch_one_token_p50_us": l50}
     rec["device"] = device_info(torch)
+    if not args.no_backward:
+        print("[bench] backward", file=sys.stderr, flush=True)
+        rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps)
     if args.copy_calibration:
         copy_calibration()
     if not args.no_cpu_baseline:

@@ -243,10 +243,14 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
     for (int dh = 0; dh < 2; ++dh)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) kt[dh][s2] = tr_operand(kstage, RS, 16 * s2, 32 * dh, lane);
-    if (has_pad && tid < kPadPartial) {
-        const float* wsum = reinterpret_cast<const float*>(DST);
+    if (KVPAD && tid < kPadPartial) {
+        // every workgroup writes its share (zero without virtual slots), so the reduction
+        // reads a dense array
         float acc = 0.f;
-        for (int w = 0; w < NW; ++w) acc += wsum[w * kPadPartial + tid];
+        if (has_pad) {
+            const float* wsum = reinterpret_cast<const float*>(DST);
+            for (int w = 0; w < NW; ++w) acc += wsum[w * kPadPartial + tid];
+        }
         const long long e = ((long long)b * a.heads + head) * a.n_windows + win;
         ba.ws[e * kPadPartial + tid] = tid < D ? acc * ba.scale : acc;
     }

@@ -62,11 +62,17 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
     const WindowRect wr = window_rect<true>(a, blk.win);
     const int n = wr.rows * wr.cols;
     const int q_begin = blk.blk * kQueryBlock;
-    if (q_begin >= n) return;
-    const int nq = min(kQueryBlock, n - q_begin);
-
     const long long n_pad = (long long)a.window * a.window - n;
     const bool has_pad = a.pad_mode == 1 && n_pad > 0;
+    // KV-token mode: every block writes its share of the pad token's gradient (zero when the
+    // window has no virtual slots or the block no queries), so the reduction reads a dense array
+    float* ws_entry = a.pad_mode == 1
+        ? ba.ws + (((long long)blk.b * a.heads + blk.head) * a.n_windows + blk.win) * a.nqb * kPadPartial +
+              (long long)blk.blk * kPadPartial
+        : nullptr;
+    if (ws_entry != nullptr && !(has_pad && q_begin < n) && threadIdx.x < kPadPartial) ws_entry[threadIdx.x] = 0.f;
+    if (q_begin >= n) return;
+    const int nq = min(kQueryBlock, n - q_begin);
 
     const long long qoff = (long long)blk.b * a.q_batch_stride + blk.head * D;
     const long long kvoff = (long long)blk.b * a.kv_batch_stride + blk.head * D;
@@ -161,8 +167,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
             const float* wgt = is_k ? Sp : Pp;
             float acc = 0.f;
             for (int i = 0; i < nq; ++i) acc = fmaf(wgt[i], src[token_elems(a, wr, q_begin + i) + ch], acc);
-            const long long e = ((long long)(blk.b * a.heads + blk.head) * a.n_windows + blk.win) * a.nqb + blk.blk;
-            ba.ws[e * kPadPartial + tid] = is_k ? acc * ba.scale : acc;
+            ws_entry[tid] = is_k ? acc * ba.scale : acc;
         }
     }
 }
@@ -263,8 +268,8 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
 }
 
 // One workgroup per (batch entry, head): row L of dk and dv = the sum of the partials of
-// every (window, query block) that has virtual slots.  512 threads = 4 slices x 128
-// columns; slice s adds entries s, s + 4, ... and the four slice sums are added in order.
+// every (window, query block).  512 threads = 4 slices x 128 columns; slice s adds entries
+// s, s + 4, ... and the four slice sums are added in order.
 template <typename T>
 __global__ __launch_bounds__(512) void swin_bwd_pad_reduce_kernel(SwinBwdArgs ba) {
     const SwinArgs& a = ba.f;
@@ -273,15 +278,10 @@ __global__ __launch_bounds__(512) void swin_bwd_pad_reduce_kernel(SwinBwdArgs ba
     const int col = threadIdx.x % kPadPartial;
     const int slice = threadIdx.x / kPadPartial;
     const long long nent = (long long)a.n_windows * a.nqb;
-    const float* src = ba.ws + (long long)bh * nent * kPadPartial;
+    const float* src = ba.ws + (long long)bh * nent * kPadPartial + col;
     float acc = 0.f;
-    for (long long e = slice; e < nent; e += 4) {
-        const int win = (int)(e / a.nqb);
-        const int qb = (int)(e - (long long)win * a.nqb);
-        const WindowRect wr = window_rect<true>(a, win);
-        const int n = wr.rows * wr.cols;
-        if (n < (long long)a.window * a.window && qb * kQueryBlock < n) acc += src[e * kPadPartial + col];
-    }
+#pragma unroll 8
+    for (long long e = slice; e < nent; e += 4) acc += src[e * kPadPartial];
     part[slice][col] = acc;
     __syncthreads();
     if (slice == 0) {

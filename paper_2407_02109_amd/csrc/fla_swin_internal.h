@@ -75,8 +75,8 @@ constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: 
 // Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
 // out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,
 // window, query block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * nqb
-// + qblk][0:64] = dk part, [64:128] = dv part (written only by blocks whose window has
-// virtual slots, and summed by the pad reduce kernel).
+// + qblk][0:64] = dk part, [64:128] = dv part.  Every block writes its entry (zero when its
+// window has no virtual slots), and the pad reduce kernel sums them.
 struct SwinBwdArgs {
     SwinArgs f;
     const void* out;
