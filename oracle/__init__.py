@@ -7,7 +7,8 @@ The GPU library never imports it and shares no code, table or helper with it.
 Every function here is a slow, obviously-correct restatement of the paper's
 definitions in float64 NumPy; see ``swin_oracle`` for the four single-grid forms,
 ``multiscale`` for the multi-scale (several grids in one sequence) forms of App. C and
-``backward`` for the gradients (dq, dk, dv) and the log-sum-exp a training forward keeps.
+``backward`` for the gradients (dq, dk, dv) and the log-sum-exp a training forward keeps,
+``rope`` for 2-D rotary position embedding of q and k ahead of the attention.
 """
 from .swin_oracle import (  # noqa: F401
     PAD_MASK,
@@ -28,6 +29,7 @@ from .backward import (  # noqa: F401
     swin_attention_ms_bwd,
     swin_attention_ms_lse,
 )
+from .rope import apply_rope, rope_angles, swin_attention_rope, swin_attention_rope_at  # noqa: F401
 from .multiscale import (  # noqa: F401
     grid_offsets,
     ms_kv_padding_indices,

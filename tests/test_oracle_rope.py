@@ -1,0 +1,166 @@
+"""Pins of the fp64 RoPE oracle (``oracle.rope``) and planted mistakes they must catch (CPU).
+
+Pins: hand-derived rotations (tests/golden/rope_small.txt); the same rotation written as a
+complex multiplication of channel pairs with positions and frequencies computed here; norm
+preservation per channel pair; scale 0 reduces to the plain textbook attention; and the
+property RoPE exists for -- attention logits depend only on relative positions, so shifting
+every coordinate by a constant leaves the MASK-mode output unchanged."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle.rope as R
+from oracle import swin_oracle as SO
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "rope_small.txt")
+
+
+def _golden_rows():
+    env = {"cos": math.cos, "sin": math.sin}
+    for line in open(GOLDEN):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        head, vin, vout = (p.split() for p in line.split("|"))
+        H, W = int(head[0]), int(head[1])
+        theta, scale = float(head[2]), float(head[3])
+        tok, y, x = int(head[4]), int(head[5]), int(head[6])
+        yield H, W, theta, scale, tok, y, x, [float(t) for t in vin], [eval(t, env) for t in vout]
+
+
+def pin_golden(M):
+    for H, W, theta, scale, tok, y, x, vin, vout in _golden_rows():
+        assert tok == y * W + x
+        xs = np.zeros((1, H * W, 1, 8))
+        xs[0, tok, 0] = vin
+        got = M.apply_rope(xs, H, W, theta, scale)[0, tok, 0]
+        np.testing.assert_allclose(got, vout, rtol=0, atol=1e-14)
+
+
+def pin_complex_form(M):
+    rng = np.random.default_rng(31)
+    for H, W, d, theta, scale in ((5, 7, 16, 10000.0, 1.0), (4, 3, 64, 500.0, 0.25), (2, 9, 8, 10.0, 3.0)):
+        x = rng.standard_normal((2, H * W, 3, d))
+        got = M.apply_rope(x, H, W, theta, scale)
+        half = d // 2
+        freqs = np.array([theta ** (-(2.0 * j) / half) for j in range(half // 2)])
+        for t in range(H * W):
+            y, xx = divmod(t, W)
+            ang = np.concatenate([scale * y * freqs, scale * xx * freqs])
+            z = x[:, t, :, 0::2] + 1j * x[:, t, :, 1::2]
+            zr = z * np.exp(1j * ang)
+            np.testing.assert_allclose(got[:, t, :, 0::2], zr.real, atol=1e-12)
+            np.testing.assert_allclose(got[:, t, :, 1::2], zr.imag, atol=1e-12)
+
+
+def pin_norms_and_pad_row(M):
+    rng = np.random.default_rng(32)
+    x = rng.standard_normal((1, 6 * 5 + 1, 2, 16))
+    got = M.apply_rope(x, 6, 5, 10000.0, 1.0)
+    n_in = x[:, :30, :, 0::2] ** 2 + x[:, :30, :, 1::2] ** 2
+    n_out = got[:, :30, :, 0::2] ** 2 + got[:, :30, :, 1::2] ** 2
+    np.testing.assert_allclose(n_out, n_in, rtol=1e-12)
+    np.testing.assert_array_equal(got[:, 30], x[:, 30])      # the pad token has no position
+
+
+def pin_scale_zero_is_plain(M):
+    rng = np.random.default_rng(33)
+    for pm in (0, 1):
+        q = rng.standard_normal((1, 42, 2, 16))
+        k = rng.standard_normal((1, 42 + pm, 2, 16))
+        v = rng.standard_normal((1, 42 + pm, 2, 16))
+        np.testing.assert_allclose(M.swin_attention_rope(q, k, v, 6, 7, 4, 2, pm, 10000.0, 0.0),
+                                   SO.swin_attention_textbook(q, k, v, 6, 7, 4, 2, pm), atol=1e-13)
+
+
+def pin_relative_positions(M):
+    rng = np.random.default_rng(34)
+    for H, W, k, s, d in ((9, 7, 4, 2, 16), (8, 8, 8, 4, 64)):
+        q = rng.standard_normal((1, H * W, 2, d))
+        kk = rng.standard_normal((1, H * W, 2, d))
+        v = rng.standard_normal((1, H * W, 2, d))
+        base = M.swin_attention_rope(q, kk, v, H, W, k, s, 0, 100.0, 1.0)
+        moved = M.swin_attention_rope(q, kk, v, H, W, k, s, 0, 100.0, 1.0, y0=5.0, x0=-3.0)
+        np.testing.assert_allclose(moved, base, atol=1e-12)
+        # and RoPE does change the result (the pin is not vacuous)
+        assert np.abs(base - SO.swin_attention_textbook(q, kk, v, H, W, k, s, 0)).max() > 1e-3
+
+
+PINS = [pin_golden, pin_complex_form, pin_norms_and_pad_row, pin_scale_zero_is_plain, pin_relative_positions]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
+def test_pin(pin):
+    pin(R)
+
+
+_orig_angles = R.rope_angles
+
+
+def _angles_axes_swapped(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    a = _orig_angles(H, W, d, theta, scale, y0, x0)
+    q = a.shape[1] // 2
+    return np.concatenate([a[:, q:], a[:, :q]], axis=1)
+
+
+def _angles_sign(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    return -_orig_angles(H, W, d, theta, scale, y0, x0)
+
+
+def _angles_freq_over_d(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    # frequency exponent 2j/d instead of 2j/(d/2)
+    freq = float(theta) ** (-2.0 * np.arange(d // 4) / d)
+    ys = (np.arange(H) + y0) * scale
+    xs = (np.arange(W) + x0) * scale
+    return np.concatenate([np.repeat(ys, W)[:, None] * freq, np.tile(xs, H)[:, None] * freq], axis=1)
+
+
+def _angles_no_scale(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    return _orig_angles(H, W, d, theta, 1.0, y0, x0)
+
+
+def _apply_half_split(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    # pairs (j, j + d/4) within each half instead of adjacent channels
+    x = np.asarray(x, dtype=np.float64)
+    B, rows, heads, d = x.shape
+    perm = np.concatenate([np.stack([np.arange(h0, h0 + d // 4), np.arange(h0 + d // 4, h0 + d // 2)], 1).ravel()
+                           for h0 in (0, d // 2)])
+    inv = np.argsort(perm)
+    return _orig_apply(x[..., perm], H, W, theta, scale, y0, x0)[..., inv]
+
+
+def _apply_rotates_pad(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+    x = np.asarray(x, dtype=np.float64)
+    out = _orig_apply(x, H, W, theta, scale, y0, x0)
+    if x.shape[1] > H * W:   # rotate the pad row as if it were the token after the grid
+        ext = np.zeros((x.shape[0], (H + 1) * W) + x.shape[2:])
+        ext[:, :H * W + 1] = x[:, :H * W + 1]
+        out[:, H * W] = _orig_apply(ext, H + 1, W, theta, scale, y0, x0)[:, H * W]
+    return out
+
+
+_orig_apply = R.apply_rope
+
+MUTANTS = {
+    "axes_swapped": {"rope_angles": _angles_axes_swapped},
+    "rotation_sign": {"rope_angles": _angles_sign},
+    "frequency_exponent_over_d": {"rope_angles": _angles_freq_over_d},
+    "scale_ignored": {"rope_angles": _angles_no_scale},
+    "pairs_half_split": {"apply_rope": _apply_half_split},
+    "pad_row_rotated": {"apply_rope": _apply_rotates_pad},
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    for attr, fn in MUTANTS[name].items():
+        monkeypatch.setattr(R, attr, fn)
+    failed = []
+    for pin in PINS:
+        try:
+            pin(R)
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, "mutant %s passed every pin" % name
