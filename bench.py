@@ -164,7 +164,10 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
     q64, k64, v64 = (synth.to_f64_numpy(t) for t in (q, k, v))
 
     def layer(nh):
-        if wl.grids:
+        if wl.rope:
+            oracle.swin_attention_rope(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], wl.H, wl.W, wl.window,
+                                       wl.shift, wl.pad_mode, wl.rope[0], wl.rope[1])
+        elif wl.grids:
             oracle.swin_attention_ms(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], list(wl.grid_list),
                                      wl.window, wl.shift, wl.pad_mode)
         else:
@@ -286,8 +289,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5000,
                     help="untimed steps first; about half a second of them lets the clocks settle")
     ap.add_argument("--workload", default="img4096",
-                    help="img1024 | img2048 | img4096 | img4096_kv | ragged150x203 | ms_img2048 "
-                         "(default: img4096)")
+                    help="img1024 | img2048 | img4096 | img4096_kv | img4096_rope | ragged150x203 | "
+                         "ms_img2048 (default: img4096)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -336,6 +339,14 @@ def main() -> int:
         def step():
             binding.fla_swin_attn_ms_fwd(qd, kd, vd, out, wl.B, wl.heads, grids, wl.head_dim,
                                          wl.window, wl.shift, wl.pad_mode, stream)
+    elif wl.rope:   # 2-D RoPE fused into the prologue: same bytes, same products
+        flops, nbytes = binding.fla_swin_attn_work(wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                                   wl.window, wl.shift, wl.pad_mode, wl.elem_bytes)
+        theta, scale = wl.rope
+
+        def step():
+            binding.fla_swin_attn_rope_fwd(qd, kd, vd, out, wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
+                                           wl.window, wl.shift, wl.pad_mode, theta, scale, stream)
     else:
         flops, nbytes = binding.fla_swin_attn_work(wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
                                                    wl.window, wl.shift, wl.pad_mode, wl.elem_bytes)
@@ -407,7 +418,7 @@ def main() -> int:
                      "cold_p10_us": c10, "cold_p50_us": c50, "cold_p90_us": c90,
                      "launch_one_token_p50_us": l50}
     rec["device"] = device_info(torch)
-    if not args.no_backward:
+    if not args.no_backward and not wl.rope:   # the backward has no RoPE form
         print("[bench] backward", file=sys.stderr, flush=True)
         rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps)
     if args.copy_calibration:

@@ -69,9 +69,13 @@ typedef enum {
     FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
     FLA_ERR_LAUNCH = 11,   /* the HIP runtime refused the kernel launch                    */
     FLA_ERR_UNSUPPORTED = 12, /* bf16 backward with a window of more than 256 tokens
-                                 (min(window, H) * min(window, W) > 256 for some grid)    */
-    FLA_ERR_WORKSPACE = 13 /* backward: workspace NULL or smaller than
-                              fla_swin_attn_bwd_workspace() reports                       */
+                                 (min(window, H) * min(window, W) > 256 for some grid), or
+                                 bf16 RoPE forward with min(window, H) or min(window, W)
+                                 above 32                                                 */
+    FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
+                               fla_swin_attn_bwd_workspace() reports                      */
+    FLA_ERR_ROPE = 14      /* RoPE entry points: rope_theta not finite and > 0, or
+                              rope_scale not finite (checked after FLA_ERR_PAD_MODE)      */
 } fla_status;
 
 /* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
@@ -101,7 +105,7 @@ int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim,
                        int window, int shift, int pad_mode, int elem_bytes,
                        double* flops, double* bytes);
 
-/* Multi-scale forward (HRSAM++, Sec. 3.6 "Multi-scale attention" and App. C): one launch over
+/* Multi-scale forward (HRSAM++, Sec. 3.6 "Multi-scale Fusion" and App. C): one launch over
  * a sequence that holds the tokens of n_grids grids one after the other -- in the paper the
  * image grid followed by the anchor-map grid.  grid_hw is a host array of 2 * n_grids ints,
  * (H_0, W_0, H_1, W_1, ...); grid g's tokens are rows [off_g, off_g + H_g*W_g) of each batch
@@ -130,6 +134,27 @@ int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, flo
 int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
                           int window, int shift, int pad_mode, int elem_bytes,
                           double* flops, double* bytes);
+
+/* Forward with 2-D rotary position embedding fused into its prologue (HRSAM uses RoPE in
+ * place of SAM's relative position bias, Sec. 3.1).  The attention above is applied to
+ * rotated q' and k' (v unchanged): for token (y, x) and channel pair (2j, 2j+1) of the
+ * first half of a head, (q[2j], q[2j+1]) is turned by the angle (y * rope_scale) * f_j,
+ * in the second half by (x * rope_scale) * f_j, f_j = rope_theta^(-2j / (head_dim / 2)),
+ * j = 0 .. head_dim/4 - 1; likewise k.  (y, x) are grid coordinates; the pad token of
+ * FLA_PAD_KVTOKEN mode has no position and is not rotated.  The rotation runs in fp32 on
+ * the loaded values (bf16: rounded back to bf16 before the products), so no rotated copy of
+ * q or k is written.  rope_theta = 10000, rope_scale = 1 is RoFormer's choice.  Errors as
+ * for fla_swin_attn_fwd, plus FLA_ERR_ROPE, and FLA_ERR_UNSUPPORTED (after FLA_ERR_TOO_LARGE)
+ * when the bf16 kernel gets a window of more than 32 rows or columns (its per-window
+ * cos/sin table covers 32 x 32; the fp32 entry point takes any window). */
+int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out,
+                           int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                           int window, int shift, int pad_mode, float rope_theta,
+                           float rope_scale, void* stream);
+int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, float* out,
+                               int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                               int window, int shift, int pad_mode, float rope_theta,
+                               float rope_scale, void* stream);
 
 /* ---------------------------------------------------------------------------------------
  * Training: the forward that keeps the log-sum-exp, and the backward pass.

@@ -24,6 +24,8 @@ from .binding import (  # noqa: F401
     swin_attn,
     swin_attn_ms,
     swin_attn_fwd_train,
+    fla_swin_attn_rope_fwd,
+    swin_attn_rope,
     swin_attn_bwd,
     library_path,
     load_library,

@@ -66,6 +66,11 @@ def _declare(lib):
     lib.fla_swin_attn_bwd_workspace.restype = I
     lib.fla_swin_attn_bwd_work.argtypes = [I, I, I, IP, I, I, I, I, I, D, D]
     lib.fla_swin_attn_bwd_work.restype = I
+    F = ctypes.c_float
+    rope_args = [P, P, P, P, I, I, I, I, I, I, I, I, F, F, P]
+    for name in ("fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32"):
+        getattr(lib, name).argtypes = rope_args
+        getattr(lib, name).restype = I
 
 
 def load_library():
@@ -327,3 +332,31 @@ def swin_attn_bwd(q, k, v, out, dout, lse, grids, window, shift, pad_mode=FLA_PA
     fla_swin_attn_ms_bwd(q, k, v, out, dout, lse, dq, dk, dv, ws, nbytes, B, heads, grids, d, window,
                          shift, pad_mode, stream, f32=f32)
     return dq, dk, dv
+
+
+# ---- forward with 2-D RoPE fused into its prologue ---------------------------------------
+
+def fla_swin_attn_rope_fwd(q, k, v, out, B, heads, Hgrid, Wgrid, head_dim, window, shift,
+                           pad_mode=FLA_PAD_MASK, rope_theta=10000.0, rope_scale=1.0, stream=None,
+                           check=True, f32=False) -> int:
+    """Forward of RoPE-rotated q and k (bf16, or fp32 with f32=True)."""
+    lib = load_library()
+    fn = lib.fla_swin_attn_rope_fwd_f32 if f32 else lib.fla_swin_attn_rope_fwd
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, heads, Hgrid, Wgrid, head_dim, window, shift,
+            pad_mode, float(rope_theta), float(rope_scale), _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def swin_attn_rope(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, rope_theta=10000.0,
+                   rope_scale=1.0, out=None, stream=None):
+    """Tensor-level RoPE forward; allocates ``out`` when not given."""
+    import torch
+    f32 = _check_tensors(q, k, v)
+    B, L, heads, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    fla_swin_attn_rope_fwd(q, k, v, out, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, rope_theta,
+                           rope_scale, stream, f32=f32)
+    return out

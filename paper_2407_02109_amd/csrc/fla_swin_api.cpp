@@ -180,13 +180,37 @@ fla::SwinArgs make_args(const Problem& pr, const void* q, const void* k, const v
     a.div_heads = fla::FastDiv::make((unsigned)heads);
     a.div_nqb = fla::FastDiv::make((unsigned)geo.nqb);
     a.div_nwin = fla::FastDiv::make((unsigned)geo.n_windows);
+    a.rope = 0;
+    a.rope_scale = 0.f;
+    for (float& f : a.rope_rev) f = 0.f;
+    for (double& f : a.rope_freq) f = 0.0;
     return a;
+}
+
+// 2-D RoPE parameters of the rope entry points (theta: frequency base, scale: position unit)
+struct Rope {
+    double theta, scale;
+};
+
+bool rope_ok(const Rope& r) {
+    return std::isfinite(r.theta) && r.theta > 0.0 && std::isfinite(r.scale);
+}
+
+void set_rope(fla::SwinArgs* a, const Rope& r) {
+    a->rope = 1;
+    a->rope_scale = (float)r.scale;
+    const int half = fla::kHeadDim / 2;
+    for (int j = 0; j < fla::kHeadDim / 4; ++j) {
+        a->rope_freq[j] = std::pow(r.theta, -2.0 * j / half);
+        a->rope_rev[j] = (float)(a->rope_freq[j] / (2.0 * 3.14159265358979323846));
+    }
 }
 
 // lse: NULL for the plain forward; the training forward passes want_lse and its buffer.
 int forward(const void* q, const void* k, const void* v, void* out, float* lse, bool want_lse, int B,
             int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
-            void* stream, int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t)) {
+            void* stream, int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t),
+            const Rope* rope = nullptr) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
     bool empty = false;
@@ -197,9 +221,15 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
         return FLA_ERR_ALIGN;
     st = check_scalars(head_dim, window, shift, pad_mode);
     if (st != FLA_OK) return st;
+    if (rope && !rope_ok(*rope)) return FLA_ERR_ROPE;
     Problem pr;
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
+    if (rope && elem_bytes == 2)   // the bf16 kernel's per-window RoPE table covers 32 x 32
+        for (int i = 0; i < n_grids; ++i)
+            if ((window < hw[2 * i] ? window : hw[2 * i]) > fla::kRopeMaxSide ||
+                (window < hw[2 * i + 1] ? window : hw[2 * i + 1]) > fla::kRopeMaxSide)
+                return FLA_ERR_UNSUPPORTED;
 
     const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
     const int64_t kv_bytes = int64_t(B) * pr.kv_rows * pr.tok * elem_bytes;
@@ -217,8 +247,9 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
     st = check_arch(&cus);
     if (st != FLA_OK) return st;
 
-    const fla::SwinArgs a = make_args(pr, q, k, v, out, want_lse ? lse : nullptr, B, heads, n_grids,
-                                      head_dim, window, shift, pad_mode, cus);
+    fla::SwinArgs a = make_args(pr, q, k, v, out, want_lse ? lse : nullptr, B, heads, n_grids, head_dim,
+                                window, shift, pad_mode, cus);
+    if (rope) set_rope(&a, *rope);
     if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;
@@ -416,6 +447,24 @@ int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v,
                    pad_mode, stream, 4, fla::launch_swin_fwd_f32);
 }
 
+int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
+                           int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
+                           float rope_theta, float rope_scale, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    const Rope r{rope_theta, rope_scale};
+    return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
+                   stream, 2, fla::launch_swin_fwd_bf16, &r);
+}
+
+int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
+                               int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                               int pad_mode, float rope_theta, float rope_scale, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    const Rope r{rope_theta, rope_scale};
+    return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
+                   stream, 4, fla::launch_swin_fwd_f32, &r);
+}
+
 int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,
                                 int shift, int pad_mode, size_t* bytes) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
@@ -486,8 +535,9 @@ const char* fla_status_string(int status) {
         case FLA_ERR_ALIAS: return "an output overlaps an input or another output";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";
-        case FLA_ERR_UNSUPPORTED: return "the bf16 backward takes windows of at most 256 tokens (window <= 16)";
+        case FLA_ERR_UNSUPPORTED: return "window too large for this bf16 entry point (backward: 256 tokens; RoPE forward: 32 x 32)";
         case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
+        case FLA_ERR_ROPE: return "rope_theta must be finite and > 0, rope_scale finite";
         default: return "unknown status";
     }
 }

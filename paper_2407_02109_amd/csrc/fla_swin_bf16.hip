@@ -31,6 +31,11 @@
 // KV-only padding (Sec. 3.4, App. B): the pad token (row L of k, v) is loaded as key n of
 // the window and its logit is raised by log2(n_pad)/scale, so in the softmax it carries
 // the weight of the n_pad = window^2 - n virtual slots it stands for.
+//
+// Optional prologue fusion of 2-D RoPE (Sec. 3.1): q in registers and each K row before its
+// LDS write are rotated by their token's grid coordinates, with the cos / sin of the
+// window's row and column positions in a per-workgroup LDS table, so a rotated copy
+// of q and k never goes through HBM.  The pad token has no position and is not rotated.
 #include "fla_swin_device.h"
 
 namespace fla {
@@ -108,11 +113,34 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
 
 // 4 waves per SIMD: at most 128 VGPRs, and the LDS footprint (2 x 69 KB) admits the two
 // workgroups per CU that this takes.
-template <bool MULTI>
+// (row, col) of window-local index t inside the window's rectangle
+__device__ __forceinline__ void window_rc(const WindowAddr& addr, int t, int& r, int& c) {
+    const unsigned ru = __umulhi((unsigned)t, addr.magic) + ((unsigned)t & addr.one_mask);
+    r = (int)ru;
+    c = (int)((unsigned)t - ru * addr.cols);
+}
+
+// RoPE of 8 consecutive channels (4 pairs) from a table of (cos, sin) per pair
+__device__ __forceinline__ void rope_rotate8_tab(uint16_t (&x)[8], const float2* cs) {
+    for (int i = 0; i < 4; ++i) {
+        const float2 t = cs[i];
+        const float a = __uint_as_float((unsigned)x[2 * i] << 16);
+        const float b = __uint_as_float((unsigned)x[2 * i + 1] << 16);
+        const __bf16 ra = (__bf16)(a * t.x - b * t.y), rb = (__bf16)(b * t.x + a * t.y);
+        x[2 * i] = __builtin_bit_cast(uint16_t, ra);
+        x[2 * i + 1] = __builtin_bit_cast(uint16_t, rb);
+    }
+}
+
+constexpr int kRopeTab = kRopeMaxSide;   // window rows / columns covered by the per-workgroup RoPE table
+
+template <bool MULTI, bool ROPE>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void swin_fwd_bf16_kernel(SwinArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * KS];
     __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
+    // RoPE: (cos, sin) of the window's row positions [0][r][j] and column positions [1][c][j]
+    __shared__ float2 Rtab[ROPE ? 2 * kRopeTab * (D / 4) : 1];
 
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
     //      workgroups of one window read adjacent 128-byte pieces of the same token rows.
@@ -170,13 +198,25 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const int nq = min(QW, n - wq0);   // queries of this wave (<= 0: the wave only loads)
 
     // ---- Q in registers, B-operand layout: lane holds q[query li][16*st + 8*h .. +8]
+    if constexpr (ROPE) {
+        // one (cos, sin) table per workgroup for the window's row and column positions (1024
+        // entries, two per thread; the host admits only windows whose rectangle fits
+        // kRopeTab x kRopeTab), filled before anything else is live in registers
+        for (int e = tid; e < 2 * kRopeTab * (D / 4); e += THREADS) {
+            const int axis = e / (kRopeTab * (D / 4)), p = (e / (D / 4)) % kRopeTab, j = e % (D / 4);
+            const float pos = (float)(axis ? wr.x0 + p : wr.y0 + p) * a.rope_scale;
+            float t = pos * a.rope_rev[j];
+            t -= __builtin_rintf(t);   // to [-1/2, 1/2] revolution for v_sin_f32 / v_cos_f32
+            Rtab[e] = make_float2(__builtin_amdgcn_cosf(t), __builtin_amdgcn_sinf(t));
+        }
+    }
+
     bf16x8 qop[4];
     if (nq > 0) {
         const unsigned row = addr(min(wq0 + li, n - 1));
         for (int st = 0; st < 4; ++st)
             qop[st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
     }
-
     float m_run = -INFINITY, l_run = 0.f;
     floatx16 o[2] = {floatx16{}, floatx16{}};   // O^T: [channel block]
 
@@ -225,6 +265,24 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + quad * 4]) = hi;
             }
         }
+        if constexpr (ROPE) {
+            // RoPE on this thread's pieces of the K rows it just wrote (8 channels per row: the
+            // row half for part < 4), in place in LDS now that the chunk's registers are free
+            if (kc0 == 0) __syncthreads();   // the cos / sin table is complete
+#pragma unroll
+            for (int it = 0; it < KC / 64; ++it) {
+                const int key = (tid >> 3) + 64 * it;
+                if (kc0 + key < n) {
+                    int kr_, kc_;
+                    window_rc(addr, kc0 + key, kr_, kc_);
+                    uint16_t e[8];
+                    __builtin_memcpy(e, &Ks[key * KS + part * 8], 16);
+                    rope_rotate8_tab(e, Rtab + ((part < 4 ? 0 : kRopeTab) + (part < 4 ? kr_ : kc_)) * (D / 4) +
+                                            4 * (part & 3));
+                    __builtin_memcpy(&Ks[key * KS + part * 8], e, 16);
+                }
+            }
+        }
         if (has_pad && n - kc0 < KC) {
             // the pad token is key n of the window: its slot was zero-filled above; after
             // the barrier, 8 threads put its K row and its V^T column in place
@@ -239,6 +297,21 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         }
         __syncthreads();
 
+        if constexpr (ROPE) {
+            if (kc0 == 0 && nq > 0) {
+                // q, once, now that the chunk's K and V registers are free: channels
+                // 16 st + 8 h .. + 7, the row half for st < 2, the column half after
+                int qr_, qc_;
+                window_rc(addr, min(wq0 + li, n - 1), qr_, qc_);
+                for (int st = 0; st < 4; ++st) {
+                    uint16_t e[8];
+                    __builtin_memcpy(e, &qop[st], 16);
+                    const int j0 = 8 * (st & 1) + 4 * h;
+                    rope_rotate8_tab(e, Rtab + ((st < 2 ? 0 : kRopeTab) + (st < 2 ? qr_ : qc_)) * (D / 4) + j0);
+                    __builtin_memcpy(&qop[st], e, 16);
+                }
+            }
+        }
         if (nq > 0) {
             for (int t0 = 0; t0 < ck; t0 += KT) {
                 // a tile needs masking only if it runs past the keys or holds the pad token
@@ -284,8 +357,10 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream) {
     SwinArgs args = a;
     void* params[] = {&args};
-    const void* fn = a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true>)
-                                   : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false>);
+    const void* fn = a.rope ? (a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, true>)
+                                             : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, true>))
+                            : (a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, false>)
+                                             : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, false>));
     return hipLaunchKernel(fn,
                            dim3((unsigned)a.n_groups), dim3(THREADS), params, 0, stream);
 }

@@ -55,11 +55,26 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     const int t = q_begin + tid;
     const bool active = t < n;
 
+    // 2-D RoPE (when asked): rotate the pairs of 4 channels starting at channel c0 of token t
+    // (angles in double: the fp32 path is the tight-tolerance reference)
+    auto rope4 = [&](float4& x, int tt, int c0) {
+        const int r = tt / wr.cols;
+        const double pos = (double)(c0 < D / 2 ? wr.y0 + r : wr.x0 + (tt - r * wr.cols)) * (double)a.rope_scale;
+        const int j = (c0 % (D / 2)) / 2;
+        double s0, c0s, s1, c1s;
+        sincos(pos * a.rope_freq[j], &s0, &c0s);
+        sincos(pos * a.rope_freq[j + 1], &s1, &c1s);
+        x = make_float4((float)(x.x * c0s - x.y * s0), (float)(x.y * c0s + x.x * s0),
+                        (float)(x.z * c1s - x.w * s1), (float)(x.w * c1s + x.z * s1));
+    };
+
     float qv[D], o[D];
     {
-        const float4* row = reinterpret_cast<const float4*>(qg + token_off(active ? t : n - 1));
+        const int tq = active ? t : n - 1;
+        const float4* row = reinterpret_cast<const float4*>(qg + token_off(tq));
         for (int i = 0; i < D / 4; ++i) {
-            const float4 x = row[i];
+            float4 x = row[i];
+            if (a.rope) rope4(x, tq, 4 * i);
             qv[4 * i] = x.x * a.scale_log2;
             qv[4 * i + 1] = x.y * a.scale_log2;
             qv[4 * i + 2] = x.z * a.scale_log2;
@@ -80,6 +95,7 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
                 const long long off = token_off(kc0 + key) + part * 4;
                 kx = *reinterpret_cast<const float4*>(kg + off);
                 vx = *reinterpret_cast<const float4*>(vg + off);
+                if (a.rope && kc0 + key < n) rope4(kx, kc0 + key, part * 4);   // not the pad token
             }
             *reinterpret_cast<float4*>(&Kf[key * D + part * 4]) = kx;
             *reinterpret_cast<float4*>(&Vf[key * D + part * 4]) = vx;

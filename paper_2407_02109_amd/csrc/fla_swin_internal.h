@@ -64,13 +64,24 @@ struct SwinArgs {
     int n_grids, n_windows;     // grids, and windows over all grids
     GridDesc grid[kMaxGrids];
     FastDiv div_heads, div_nqb, div_nwin;   // workgroup index decode
+    // 2-D rotary position embedding of q and k (0: none): channel pair (2j, 2j+1) of the
+    // first half of a head turns by (row * rope_scale) * f_j, of the second half by
+    // (column * rope_scale) * f_j, f_j = theta^(-2j / (head_dim / 2)).  rope_rev[j] is f_j in
+    // revolutions per position unit (f_j / 2 pi, for the hardware sine of the bf16 kernel);
+    // rope_freq[j] is f_j in double for the fp32 kernel.
+    int rope;
+    float rope_scale;
+    float rope_rev[kHeadDim / 4];
+    double rope_freq[kHeadDim / 4];
 };
+
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
 constexpr int kBwdMaxTokens = 256;   // window tokens the bf16 backward kernel holds (window <= 16)
 constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: dk then dv
+constexpr int kRopeMaxSide = 32;   // bf16 RoPE forward: window rows and columns it takes
 
 // Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
 // out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,

@@ -36,6 +36,7 @@ class Workload:
     scale: float = 1.0         # exact power of two applied to q, k and v before rounding
     stress_keys: float = 0.0   # fraction of (token, head) key rows multiplied by 8
     grids: tuple = ()          # multi-scale: ((H, W), ...) one after the other; () = (H, W) alone
+    rope: tuple = ()           # (theta, scale): 2-D RoPE on q and k inside the kernel; () = none
     note: str = field(default="", compare=False)
 
     @property
@@ -74,6 +75,10 @@ WORKLOADS = {
                            pad_mode=PAD_KVTOKEN,
                            note="img4096 with KV-only padding: border windows attend the pad token "
                                 "(row L of k and v) with multiplicity window^2 - n"),
+    "img4096_rope": Workload("img4096_rope", 1, 12, 256, 256, 64, 16, 8, "bf16", seed=5,
+                             rope=(10000.0, 1.0),
+                             note="256x256 tokens, 12 heads x 64, window 16, shift 8, N(0,1), with 2-D RoPE "
+                                  "(theta 10000, grid coordinates) applied to q and k in the kernel's prologue"),
     "ms_img2048": Workload("ms_img2048", 1, 12, 128, 128, 64, 16, 8, "bf16", seed=7,
                            pad_mode=PAD_KVTOKEN, grids=((128, 128), (32, 32)),
                            note="multi-scale (HRSAM++): the 2048^2 image's 128x128 tokens followed by "

@@ -41,7 +41,7 @@ def test_header_declares_the_entry_points():
         "fla_swin_attn_fwd_lse", "fla_swin_attn_fwd_lse_f32", "fla_swin_attn_ms_fwd_lse",
         "fla_swin_attn_ms_fwd_lse_f32", "fla_swin_attn_bwd_workspace", "fla_swin_attn_bwd",
         "fla_swin_attn_bwd_f32", "fla_swin_attn_ms_bwd", "fla_swin_attn_ms_bwd_f32",
-        "fla_swin_attn_bwd_work"])
+        "fla_swin_attn_bwd_work", "fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32"])
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -386,3 +386,37 @@ def test_bwd_work_counts(lib, grids, k, s, pm):
         L = sum(h * w for h, w in grids)
         assert f == 2.5 * f0                           # five products instead of two
         assert b == 2 * b0 + 4 * B * heads * L         # eight tensors instead of four, plus lse
+
+
+# ---- RoPE forward ---------------------------------------------------------------------
+def _call_rope(f32=False, theta=10000.0, scale=1.0, **kw):
+    a = dict(GOOD)
+    a.update({k: v for k, v in kw.items() if k in GOOD})
+    p = dict(q=Q, k=K, v=V, out=OUT)
+    p.update({k: v for k, v in kw.items() if k in p})
+    return fb.fla_swin_attn_rope_fwd(p["q"], p["k"], p["v"], p["out"], a["B"], a["heads"], a["Hgrid"],
+                                     a["Wgrid"], a["head_dim"], a["window"], a["shift"], a["pad_mode"],
+                                     theta, scale, 0, check=False, f32=f32)
+
+
+ROPE_CASES = [
+    ("FLA_ERR_ROPE", dict(theta=0.0)), ("FLA_ERR_ROPE", dict(theta=-10.0)),
+    ("FLA_ERR_ROPE", dict(theta=float("inf"))), ("FLA_ERR_ROPE", dict(theta=float("nan"))),
+    ("FLA_ERR_ROPE", dict(scale=float("inf"))), ("FLA_ERR_ROPE", dict(scale=float("nan"))),
+    ("FLA_ERR_PAD_MODE", dict(pad_mode=2, theta=0.0)),      # pad mode is checked first
+    ("FLA_ERR_NULL", dict(q=0, theta=0.0)), ("FLA_ERR_ALIAS", dict(out=Q)),
+]
+
+
+@pytest.mark.parametrize("f32", [False, True], ids=["bf16", "f32"])
+@pytest.mark.parametrize("status,kw", ROPE_CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(ROPE_CASES)])
+def test_rope_argument_checks(lib, f32, status, kw):
+    assert _call_rope(f32=f32, **kw) == _header_enum("FLA")[status]
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_rope_without_device_reports_arch(lib):
+    codes = _header_enum("FLA")
+    for kw in (dict(), dict(scale=0.0), dict(scale=-2.0, theta=1.0), dict(pad_mode=1)):
+        assert _call_rope(**kw) == codes["FLA_ERR_ARCH"]
+        assert _call_rope(f32=True, **kw) == codes["FLA_ERR_ARCH"]
