@@ -46,6 +46,7 @@ constexpr int THREADS = 512;    // 8 waves of 64
 constexpr int QW = 32;          // queries per wave
 constexpr int KC = 256;         // keys staged in LDS at a time
 constexpr int KT = 32;          // keys per inner tile
+constexpr int KH = KC / 2;      // keys per half chunk (staged and computed in turn)
 constexpr int KS = D + 8;       // K row stride in LDS, bf16 elements (144 B)
 constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
 constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
@@ -228,27 +229,32 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         //      workgroup waits for one round trip to HBM, not one per load.
         //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 64*it.
         //      V: a thread takes 4 consecutive keys (quad) x 8 channels (vpart) and writes
-        //      them transposed: 4 keys of one channel are one 8-byte LDS store.
+        //      them transposed: 4 keys of one channel are one 8-byte LDS store.  Waves 0-3
+        //      hold keys 0-127 of the chunk, waves 4-7 keys 128-255.
+        //      The chunk is consumed in two halves of 128 keys: the first half is written to
+        //      LDS and computed while the loads of the second half are still arriving.  Loads
+        //      are issued in the order they are consumed (K of the first half, V, then K of
+        //      the second half), since a wave waits for its loads in issue order.
         uint4 kreg[KC / 64];
         uint4 vreg[4];
         const int part = tid & 7;
-#pragma unroll
-        for (int it = 0; it < KC / 64; ++it) {
-            const int key = (tid >> 3) + 64 * it;
-            const int t = kc0 + key;
-            kreg[it] = bload16(kr, (t < n ? addr(t) : kOutside) + part * 16);
-        }
         const int vpart = (tid >> 3) & 7;
         const int quad = (tid & 7) + ((tid >> 6) << 3);
+        auto load_k = [&](int it) {
+            const int t = kc0 + (tid >> 3) + 64 * it;
+            kreg[it] = bload16(kr, (t < n ? addr(t) : kOutside) + part * 16);
+        };
+        load_k(0);
+        load_k(1);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int t = kc0 + quad * 4 + u;
             vreg[u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
         }
-#pragma unroll
-        for (int it = 0; it < KC / 64; ++it)
-            *reinterpret_cast<uint4*>(&Ks[((tid >> 3) + 64 * it) * KS + part * 8]) = kreg[it];
-        {
+        load_k(2);
+        load_k(3);
+
+        auto write_v = [&]() {
             const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
             const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
             const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
@@ -264,43 +270,50 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 *reinterpret_cast<uint2*>(&Vt[ch * VS + quad * 4]) = lo;
                 *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + quad * 4]) = hi;
             }
-        }
-        if constexpr (ROPE) {
-            // RoPE on this thread's pieces of the K rows it just wrote (8 channels per row: the
-            // row half for part < 4), in place in LDS now that the chunk's registers are free
-            if (kc0 == 0) __syncthreads();   // the cos / sin table is complete
-#pragma unroll
-            for (int it = 0; it < KC / 64; ++it) {
-                const int key = (tid >> 3) + 64 * it;
-                if (kc0 + key < n) {
-                    int kr_, kc_;
-                    window_rc(addr, kc0 + key, kr_, kc_);
-                    uint16_t e[8];
-                    __builtin_memcpy(e, &Ks[key * KS + part * 8], 16);
-                    rope_rotate8_tab(e, Rtab + ((part < 4 ? 0 : kRopeTab) + (part < 4 ? kr_ : kc_)) * (D / 4) +
-                                            4 * (part & 3));
-                    __builtin_memcpy(&Ks[key * KS + part * 8], e, 16);
+        };
+        // K rows (its it0, it0 + 1) and, for the waves that hold this half, V^T; RoPE on the
+        // K rows in place; the pad token if its slot falls in this half; then the barrier
+        auto stage_half = [&](int half) {
+            for (int it = 2 * half; it < 2 * half + 2; ++it)
+                *reinterpret_cast<uint4*>(&Ks[((tid >> 3) + 64 * it) * KS + part * 8]) = kreg[it];
+            if ((wave >> 2) == half) write_v();
+            if constexpr (ROPE) {
+                // RoPE on this thread's pieces of the K rows it just wrote (8 channels per row:
+                // the row half for part < 4), in place in LDS
+                if (kc0 == 0 && half == 0) __syncthreads();   // the cos / sin table is complete
+                for (int it = 2 * half; it < 2 * half + 2; ++it) {
+                    const int key = (tid >> 3) + 64 * it;
+                    if (kc0 + key < n) {
+                        int kr_, kc_;
+                        window_rc(addr, kc0 + key, kr_, kc_);
+                        uint16_t e[8];
+                        __builtin_memcpy(e, &Ks[key * KS + part * 8], 16);
+                        rope_rotate8_tab(e, Rtab + ((part < 4 ? 0 : kRopeTab) + (part < 4 ? kr_ : kc_)) * (D / 4) +
+                                                4 * (part & 3));
+                        __builtin_memcpy(&Ks[key * KS + part * 8], e, 16);
+                    }
                 }
             }
-        }
-        if (has_pad && n - kc0 < KC) {
-            // the pad token is key n of the window: its slot was zero-filled above; after
-            // the barrier, 8 threads put its K row and its V^T column in place
-            __syncthreads();
             const int slot = n - kc0;
-            if (tid < 8) {
-                *reinterpret_cast<uint4*>(&Ks[slot * KS + tid * 8]) = bload16(kpr, tid * 16);
-                const uint4 vv = bload16(vpr, tid * 16);
-                const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
-                for (int e = 0; e < 8; ++e) Vt[(tid * 8 + e) * VS + slot] = ve[e];
+            if (has_pad && slot >= KH * half && slot < KH * (half + 1)) {
+                // the pad token is key n of the window: its slot was zero-filled above; after
+                // the barrier, 8 threads put its K row and its V^T column in place
+                __syncthreads();
+                if (tid < 8) {
+                    *reinterpret_cast<uint4*>(&Ks[slot * KS + tid * 8]) = bload16(kpr, tid * 16);
+                    const uint4 vv = bload16(vpr, tid * 16);
+                    const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
+                    for (int e = 0; e < 8; ++e) Vt[(tid * 8 + e) * VS + slot] = ve[e];
+                }
             }
-        }
-        __syncthreads();
+            __syncthreads();
+        };
 
+        stage_half(0);
         if constexpr (ROPE) {
             if (kc0 == 0 && nq > 0) {
-                // q, once, now that the chunk's K and V registers are free: channels
-                // 16 st + 8 h .. + 7, the row half for st < 2, the column half after
+                // q, once: channels 16 st + 8 h .. + 7, the row half for st < 2, the column
+                // half after
                 int qr_, qc_;
                 window_rc(addr, min(wq0 + li, n - 1), qr_, qc_);
                 for (int st = 0; st < 4; ++st) {
@@ -312,12 +325,17 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 }
             }
         }
-        if (nq > 0) {
-            for (int t0 = 0; t0 < ck; t0 += KT) {
-                // a tile needs masking only if it runs past the keys or holds the pad token
-                attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run,
-                            l_run, a.scale_log2, lane);
-            }
+        // a tile needs masking only if it runs past the keys or holds the pad token
+        if (nq > 0)
+            for (int t0 = 0; t0 < min(ck, KH); t0 += KT)
+                attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
+                            a.scale_log2, lane);
+        if (ck > KH) {
+            stage_half(1);
+            if (nq > 0)
+                for (int t0 = KH; t0 < ck; t0 += KT)
+                    attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
+                                a.scale_log2, lane);
         }
     }
 
