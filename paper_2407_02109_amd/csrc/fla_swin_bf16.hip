@@ -229,12 +229,12 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         //      workgroup waits for one round trip to HBM, not one per load.
         //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 64*it.
         //      V: a thread takes 4 consecutive keys (quad) x 8 channels (vpart) and writes
-        //      them transposed: 4 keys of one channel are one 8-byte LDS store.  Waves 0-3
-        //      hold keys 0-127 of the chunk, waves 4-7 keys 128-255.
-        //      The chunk is consumed in two halves of 128 keys: the first half is written to
-        //      LDS and computed while the loads of the second half are still arriving.  Loads
-        //      are issued in the order they are consumed (K of the first half, V, then K of
-        //      the second half), since a wave waits for its loads in issue order.
+        //      them transposed: 4 keys of one channel are one 8-byte LDS store.
+        //      The chunk is consumed in two halves of 128 keys: V and the first half of K are
+        //      written to LDS and that half is computed while the K rows of the second half
+        //      are still arriving (deferring V as well would exceed 128 VGPRs).  Loads are
+        //      issued in the order they are consumed, since a wave waits for its loads in
+        //      issue order.
         uint4 kreg[KC / 64];
         uint4 vreg[4];
         const int part = tid & 7;
@@ -271,17 +271,21 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + quad * 4]) = hi;
             }
         };
-        // K rows (its it0, it0 + 1) and, for the waves that hold this half, V^T; RoPE on the
-        // K rows in place; the pad token if its slot falls in this half; then the barrier
+        // K rows of this half (and all of V^T with the first); RoPE on the K rows in place;
+        // the pad token if its slot falls in this half; then the barrier
+        // (with RoPE the whole chunk is one "half": deferring half of K would need more than
+        // the 128-VGPR budget next to the rotation)
+        constexpr int kh = ROPE ? KC : KH;
+        constexpr int its = kh / 64;   // K rows per thread in one half
         auto stage_half = [&](int half) {
-            for (int it = 2 * half; it < 2 * half + 2; ++it)
+            for (int it = its * half; it < its * (half + 1); ++it)
                 *reinterpret_cast<uint4*>(&Ks[((tid >> 3) + 64 * it) * KS + part * 8]) = kreg[it];
-            if ((wave >> 2) == half) write_v();
+            if (half == 0) write_v();
             if constexpr (ROPE) {
                 // RoPE on this thread's pieces of the K rows it just wrote (8 channels per row:
                 // the row half for part < 4), in place in LDS
                 if (kc0 == 0 && half == 0) __syncthreads();   // the cos / sin table is complete
-                for (int it = 2 * half; it < 2 * half + 2; ++it) {
+                for (int it = its * half; it < its * (half + 1); ++it) {
                     const int key = (tid >> 3) + 64 * it;
                     if (kc0 + key < n) {
                         int kr_, kc_;
@@ -295,7 +299,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 }
             }
             const int slot = n - kc0;
-            if (has_pad && slot >= KH * half && slot < KH * (half + 1)) {
+            if (has_pad && slot >= kh * half && slot < kh * (half + 1)) {
                 // the pad token is key n of the window: its slot was zero-filled above; after
                 // the barrier, 8 threads put its K row and its V^T column in place
                 __syncthreads();
@@ -327,13 +331,13 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         }
         // a tile needs masking only if it runs past the keys or holds the pad token
         if (nq > 0)
-            for (int t0 = 0; t0 < min(ck, KH); t0 += KT)
+            for (int t0 = 0; t0 < min(ck, kh); t0 += KT)
                 attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
                             a.scale_log2, lane);
-        if (ck > KH) {
+        if (ck > kh) {
             stage_half(1);
             if (nq > 0)
-                for (int t0 = KH; t0 < ck; t0 += KT)
+                for (int t0 = kh; t0 < ck; t0 += KT)
                     attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
                                 a.scale_log2, lane);
         }
