@@ -198,6 +198,7 @@ def swin_attn_ms(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, out=None,
     for t in (q, k, v):
         if t.dtype != q.dtype or not t.is_cuda or not t.is_contiguous():
             raise ValueError("q, k, v must share dtype and be contiguous device tensors")
+    _check_shapes(q, k, v, sum(int(h) * int(w) for h, w in grids), pad_mode, *([out] if out is not None else []))
     B, L, heads, d = q.shape
     if out is None:
         out = torch.empty_like(q)
@@ -207,20 +208,28 @@ def swin_attn_ms(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, out=None,
 
 
 def swin_attn(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, out=None, stream=None):
-    """Tensor-level convenience wrapper: q [B, L, heads, d] (bf16 or fp32, on the GPU,
-    contiguous), k/v [B, L(+1), heads, d].  Allocates ``out`` when not given."""
+    """Tensor-level convenience wrapper: q [B, L, heads, d] or [B, Hgrid, Wgrid, heads, d]
+    (bf16 or fp32, on the GPU, contiguous), k/v likewise ([B, L + 1, heads, d] in KV-token
+    mode).  Allocates ``out`` (q's shape) when not given."""
     import torch
     if q.dtype not in (torch.bfloat16, torch.float32):
         raise TypeError("q must be bfloat16 or float32")
     for t in (q, k, v):
         if t.dtype != q.dtype or not t.is_cuda or not t.is_contiguous():
             raise ValueError("q, k, v must share dtype and be contiguous device tensors")
-    B, L, heads, d = q.shape
+    shape = q.shape
+    flat = lambda t: t.reshape(t.shape[0], t.shape[1] * t.shape[2], t.shape[3], t.shape[4]) if t.dim() == 5 else t
+    q4, k4, v4 = flat(q), flat(k), flat(v)
+    if q.dim() == 5 and (q.shape[1], q.shape[2]) != (Hgrid, Wgrid):
+        raise ValueError("q is %s but the grid is %dx%d" % (tuple(q.shape), Hgrid, Wgrid))
+    _check_shapes(q4, k4, v4, Hgrid * Wgrid, pad_mode, *([flat(out)] if out is not None else []))
     if out is None:
         out = torch.empty_like(q)
+    out4 = flat(out)
+    B, L, heads, d = q4.shape
     fn = fla_swin_attn_fwd if q.dtype == torch.bfloat16 else fla_swin_attn_fwd_f32
-    fn(q, k, v, out, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, stream)
-    return out
+    fn(q4, k4, v4, out4, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, stream)
+    return out.reshape(shape)
 
 
 # ---- training: forward with log-sum-exp, backward ------------------------------------------
@@ -296,6 +305,22 @@ def fla_swin_attn_bwd_work(B, heads, grids, head_dim, window, shift, pad_mode, e
     return f.value, b.value
 
 
+def _check_shapes(q, k, v, L, pad_mode, *like_q):
+    """Raise ValueError unless q [B, L, heads, d] and k, v [B, L (+1 in KV-token mode), heads, d]
+    (and every tensor in like_q has q's shape): the C ABI trusts the sizes it is given, so a
+    mismatch here would read or write outside the tensors."""
+    if q.dim() != 4 or q.shape[1] != L:
+        raise ValueError("q must be [B, %d, heads, head_dim], got %s" % (L, tuple(q.shape)))
+    rows = L + (1 if pad_mode == FLA_PAD_KVTOKEN else 0)
+    want = (q.shape[0], rows, q.shape[2], q.shape[3])
+    for name, t in (("k", k), ("v", v)):
+        if tuple(t.shape) != want:
+            raise ValueError("%s must be %s, got %s" % (name, want, tuple(t.shape)))
+    for t in like_q:
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError("expected a tensor of q's shape %s, got %s" % (tuple(q.shape), tuple(t.shape)))
+
+
 def _check_tensors(*ts):
     import torch
     t0 = ts[0]
@@ -311,6 +336,7 @@ def swin_attn_fwd_train(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, st
     """Training forward over a grid list ((H, W), ...): returns (out, lse)."""
     import torch
     f32 = _check_tensors(q, k, v)
+    _check_shapes(q, k, v, sum(int(h) * int(w) for h, w in grids), pad_mode)
     B, L, heads, d = q.shape
     out = torch.empty_like(q)
     lse = torch.empty((B, heads, L), dtype=torch.float32, device=q.device)
@@ -325,7 +351,10 @@ def swin_attn_bwd(q, k, v, out, dout, lse, grids, window, shift, pad_mode=FLA_PA
     f32 = _check_tensors(q, k, v, out, dout)
     if lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 tensor")
+    _check_shapes(q, k, v, sum(int(h) * int(w) for h, w in grids), pad_mode, out, dout)
     B, L, heads, d = q.shape
+    if tuple(lse.shape) != (B, heads, L):
+        raise ValueError("lse must be [B, heads, L] = %s, got %s" % ((B, heads, L), tuple(lse.shape)))
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     nbytes = fla_swin_attn_bwd_workspace(B, heads, grids, window, shift, pad_mode)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
@@ -354,6 +383,7 @@ def swin_attn_rope(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, 
     """Tensor-level RoPE forward; allocates ``out`` when not given."""
     import torch
     f32 = _check_tensors(q, k, v)
+    _check_shapes(q, k, v, Hgrid * Wgrid, pad_mode, *([out] if out is not None else []))
     B, L, heads, d = q.shape
     if out is None:
         out = torch.empty_like(q)

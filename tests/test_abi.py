@@ -420,3 +420,47 @@ def test_rope_without_device_reports_arch(lib):
     for kw in (dict(), dict(scale=0.0), dict(scale=-2.0, theta=1.0), dict(pad_mode=1)):
         assert _call_rope(**kw) == codes["FLA_ERR_ARCH"]
         assert _call_rope(f32=True, **kw) == codes["FLA_ERR_ARCH"]
+
+
+# ---- tensor-level wrappers: shape checks before any device access -----------------------
+class _FakeCuda:
+    """Just enough of a tensor for the wrappers' checks (dtype, device flag, layout, shape)."""
+    def __init__(self, shape, dtype=None):
+        import torch
+        self.shape = torch.Size(shape)
+        self.dtype = dtype or torch.bfloat16
+        self.is_cuda = True
+
+    def is_contiguous(self):
+        return True
+
+    def dim(self):
+        return len(self.shape)
+
+    def reshape(self, *s):
+        return _FakeCuda(s, self.dtype)
+
+
+@pytest.mark.parametrize("qs,ks,pm", [
+    ((1, 63, 2, 64), (1, 64, 2, 64), 0),       # q rows != H*W
+    ((1, 64, 2, 64), (1, 64, 2, 64), 1),       # KV-token mode needs the pad row
+    ((1, 64, 2, 64), (1, 65, 2, 64), 0),       # extra row without KV-token mode
+    ((1, 64, 2, 64), (1, 64, 3, 64), 0),       # heads differ
+    ((2, 64, 2, 64), (1, 64, 2, 64), 0),       # batch differs
+])
+def test_wrappers_reject_mismatched_shapes(qs, ks, pm):
+    q, k = _FakeCuda(qs), _FakeCuda(ks)
+    with pytest.raises(ValueError):
+        fb.swin_attn(q, k, k, 8, 8, 4, 0, pm)
+    with pytest.raises(ValueError):
+        fb.swin_attn_ms(q, k, k, [(8, 8)], 4, 0, pm)
+    with pytest.raises(ValueError):
+        fb.swin_attn_fwd_train(q, k, k, [(8, 8)], 4, 0, pm)
+    with pytest.raises(ValueError):
+        fb.swin_attn_rope(q, k, k, 8, 8, 4, 0, pm)
+
+
+def test_swin_attn_grid_of_a_5d_tensor_must_match():
+    q = _FakeCuda((1, 8, 8, 2, 64))
+    with pytest.raises(ValueError):
+        fb.swin_attn(q, q, q, 8, 4, 4, 0)
