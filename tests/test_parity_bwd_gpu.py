@@ -11,7 +11,11 @@ so errors are measured against M = max |reference| of that tensor:
   * log-sum-exp, natural log: bf16 4e-3 absolute -- the bf16 forward sums probabilities
     rounded to bf16 (relative 2^-9 each, so the sum is off by at most 2^-9 relative and its
     log by at most 2^-9 ~ 1.95e-3), twice that for margin; fp32 1e-5.
-A reference that is exactly zero (one-token windows) instead needs |got| <= 1e-5.
+A reference that is exactly zero (one-token windows) instead needs |got| <= 1e-5.  The pad
+token's gradient row (64 values per head) is checked on its own scale with the max bound only:
+a mean over so few values is no bulk statistic, and when the pad token carries almost all of
+a query's weight (e.g. a 1 x 40 grid with window 16: multiplicity >= 240) its dS = P (dP - D)
+is a difference of nearly equal terms, where D = <dO, O> from the bf16 output dominates.
 Outputs start as NaN so that an unwritten element fails."""
 import numpy as np
 import pytest
@@ -61,7 +65,7 @@ def _train(wl, q, k, v, dout):
     return out, lse, dq, dk, dv
 
 
-def _check_grad(name, got, ref, f32):
+def _check_grad(name, got, ref, f32, bulk=True):
     got = synth.to_f64_numpy(got)
     assert np.isfinite(got).all(), "%s: non-finite element (unwritten?)" % name
     M = np.abs(ref).max()
@@ -74,13 +78,16 @@ def _check_grad(name, got, ref, f32):
     if f32:
         assert err.max() <= F32_MAX * M, (name, err.max() / M)
     else:
-        assert err.max() <= BF16_MAX * M and err.mean() <= BF16_MEAN * M, (name, err.max() / M, err.mean() / M)
+        assert err.max() <= BF16_MAX * M, (name, err.max() / M)
+        if bulk:
+            assert err.mean() <= BF16_MEAN * M, (name, err.mean() / M)
     return err.max() / M
 
 
 SHAPES = [  # B, heads, H, W, window, shift
     (2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 2, 23, 41, 12, 5),
     (1, 1, 9, 7, 16, 0), (1, 2, 5, 6, 1, 0), (1, 2, 16, 16, 16, 0), (1, 2, 33, 17, 5, 2),
+    (1, 1, 1, 1, 1, 0), (1, 1, 9, 300, 16, 15), (1, 2, 1, 40, 16, 7), (2, 1, 40, 1, 8, 7),
 ]
 F32_WIDE = [(1, 2, 40, 24, 20, 10), (1, 1, 40, 40, 32, 16)]   # windows of more than 256 tokens
 
@@ -119,9 +126,9 @@ def test_lse_and_backward(shape, dtype, pm):
     gq, gk, gv = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
     for name, got, ref in (("dq", dq, gq), ("dk", dk, gk), ("dv", dv, gv)):
         _check_grad(name, got, ref, f32)
-    if pm == 1:   # the pad row on its own scale
-        _check_grad("dk_pad", dk[:, -1], gk[:, -1], f32)
-        _check_grad("dv_pad", dv[:, -1], gv[:, -1], f32)
+    if pm == 1:   # the pad row on its own scale (64 values per head: the max bound only)
+        _check_grad("dk_pad", dk[:, -1], gk[:, -1], f32, bulk=False)
+        _check_grad("dv_pad", dv[:, -1], gv[:, -1], f32, bulk=False)
 
 
 @pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
@@ -243,5 +250,5 @@ def test_full_size_sampled_windows(name):
                 idx, (_, gk, gv) = _window_grads(qn, kn, vn, dn, H, W, rect, k, pm, L)
                 pk += gk[:, len(idx)]
                 pv += gv[:, len(idx)]
-        _check_grad("dk_pad", torch.from_numpy(dk[:, L]), pk, False)
-        _check_grad("dv_pad", torch.from_numpy(dv[:, L]), pv, False)
+        _check_grad("dk_pad", torch.from_numpy(dk[:, L]), pk, False, bulk=False)
+        _check_grad("dv_pad", torch.from_numpy(dv[:, L]), pv, False, bulk=False)

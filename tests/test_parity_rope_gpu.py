@@ -42,6 +42,7 @@ def _compare(got, ref, f32):
 
 SHAPES = [  # B, heads, H, W, window, shift
     (2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 7, 16, 0),
+    (1, 1, 9, 300, 16, 15), (1, 1, 1, 1, 1, 0), (1, 2, 40, 24, 32, 16),
 ]
 ROPES = [(10000.0, 1.0), (100.0, 0.5)]
 
