@@ -29,7 +29,14 @@ from .backward import (  # noqa: F401
     swin_attention_ms_bwd,
     swin_attention_ms_lse,
 )
-from .rope import apply_rope, rope_angles, swin_attention_rope, swin_attention_rope_at  # noqa: F401
+from .rope import (  # noqa: F401
+    apply_rope,
+    rope_angles,
+    swin_attention_rope,
+    swin_attention_rope_at,
+    swin_attention_rope_bwd,
+    swin_attention_rope_lse,
+)
 from .multiscale import (  # noqa: F401
     grid_offsets,
     ms_kv_padding_indices,

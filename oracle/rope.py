@@ -35,13 +35,16 @@ def rope_angles(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
     return np.concatenate([row, col], axis=1)
 
 
-def apply_rope(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
-    """Rotate the first H*W rows of x [B, rows, heads, d]; rows past H*W (the pad token)
-    are returned unchanged."""
+def apply_rope(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0, inverse=False):
+    """Rotate the first H*W rows of x [B, rows, heads, d] (by the opposite angles when
+    inverse: the transpose of the rotation); rows past H*W (the pad token) are returned
+    unchanged."""
     x = _f64(x)
     B, rows, heads, d = x.shape
     L = H * W
     ang = rope_angles(H, W, d, theta, scale, y0, x0)          # [L, d/2]
+    if inverse:
+        ang = -ang
     c, s = np.cos(ang)[None, :, None, :], np.sin(ang)[None, :, None, :]
     out = x.copy()
     even, odd = x[:, :L, :, 0::2], x[:, :L, :, 1::2]
@@ -66,4 +69,24 @@ def swin_attention_rope_at(q, k, v, H, W, window, shift, pad_mode, queries, thet
                              _f64(v), H, W, window, shift, pad_mode, queries)
 
 
-__all__ = ["rope_angles", "apply_rope", "swin_attention_rope", "swin_attention_rope_at", "PAD_KVTOKEN"]
+def swin_attention_rope_lse(q, k, v, H, W, window, shift, pad_mode=0, theta=10000.0, scale=1.0):
+    """Log-sum-exp of the RoPE attention: that of the rotated q and k."""
+    from .backward import swin_attention_lse
+    return swin_attention_lse(apply_rope(q, H, W, theta, scale), apply_rope(k, H, W, theta, scale), _f64(v),
+                              H, W, window, shift, pad_mode)
+
+
+def swin_attention_rope_bwd(q, k, v, dout, H, W, window, shift, pad_mode=0, theta=10000.0, scale=1.0):
+    """Gradients of the RoPE attention with respect to the unrotated q, k and v.  With
+    q' = R q and k' = R k per token (R a rotation), the chain rule gives dq = R^T dq' and
+    dk = R^T dk', where dq', dk' are the attention gradients at q', k'; dv is unchanged and
+    the unrotated pad token's gradient is dk'[L] itself."""
+    from .backward import swin_attention_bwd
+    dqr, dkr, dv = swin_attention_bwd(apply_rope(q, H, W, theta, scale), apply_rope(k, H, W, theta, scale),
+                                      _f64(v), _f64(dout), H, W, window, shift, pad_mode)
+    return (apply_rope(dqr, H, W, theta, scale, inverse=True),
+            apply_rope(dkr, H, W, theta, scale, inverse=True), dv)
+
+
+__all__ = ["rope_angles", "apply_rope", "swin_attention_rope", "swin_attention_rope_at",
+           "swin_attention_rope_lse", "swin_attention_rope_bwd", "PAD_KVTOKEN"]

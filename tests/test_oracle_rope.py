@@ -88,7 +88,36 @@ def pin_relative_positions(M):
         assert np.abs(base - SO.swin_attention_textbook(q, kk, v, H, W, k, s, 0)).max() > 1e-3
 
 
-PINS = [pin_golden, pin_complex_form, pin_norms_and_pad_row, pin_scale_zero_is_plain, pin_relative_positions]
+def pin_inverse(M):
+    rng = np.random.default_rng(35)
+    x = rng.standard_normal((2, 6 * 7 + 1, 3, 16))
+    back = M.apply_rope(M.apply_rope(x, 6, 7, 100.0, 0.7), 6, 7, 100.0, 0.7, inverse=True)
+    np.testing.assert_allclose(back, x, atol=1e-12)
+
+
+def pin_rope_bwd_fd(M):
+    """Gradients of the RoPE attention against central finite differences of its forward."""
+    rng = np.random.default_rng(36)
+    for H, W, k, s, pm in ((6, 5, 4, 2, 0), (6, 5, 4, 2, 1), (5, 7, 8, 3, 1)):
+        L = H * W
+        q = rng.standard_normal((1, L, 2, 8))
+        kk = rng.standard_normal((1, L + pm, 2, 8))
+        v = rng.standard_normal((1, L + pm, 2, 8))
+        do = rng.standard_normal((1, L, 2, 8))
+        dq, dk, dv = M.swin_attention_rope_bwd(q, kk, v, do, H, W, k, s, pm, 50.0, 0.8)
+        U = [rng.standard_normal(t.shape) for t in (q, kk, v)]
+        f = lambda t: float((do * M.swin_attention_rope(q + t * U[0], kk + t * U[1], v + t * U[2], H, W, k, s, pm,
+                                                        50.0, 0.8)).sum())
+        h = 1e-5
+        fd = (f(h) - f(-h)) / (2 * h)
+        an = float((dq * U[0]).sum() + (dk * U[1]).sum() + (dv * U[2]).sum())
+        assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), ((H, W, k, s, pm), fd, an)
+        lse = M.swin_attention_rope_lse(q, kk, v, H, W, k, s, pm, 50.0, 0.8)
+        assert lse.shape == (1, 2, L) and np.isfinite(lse).all()
+
+
+PINS = [pin_golden, pin_complex_form, pin_norms_and_pad_row, pin_scale_zero_is_plain, pin_relative_positions,
+        pin_inverse, pin_rope_bwd_fd]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -121,29 +150,42 @@ def _angles_no_scale(H, W, d, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
     return _orig_angles(H, W, d, theta, 1.0, y0, x0)
 
 
-def _apply_half_split(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+def _apply_half_split(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0, inverse=False):
     # pairs (j, j + d/4) within each half instead of adjacent channels
     x = np.asarray(x, dtype=np.float64)
     B, rows, heads, d = x.shape
     perm = np.concatenate([np.stack([np.arange(h0, h0 + d // 4), np.arange(h0 + d // 4, h0 + d // 2)], 1).ravel()
                            for h0 in (0, d // 2)])
     inv = np.argsort(perm)
-    return _orig_apply(x[..., perm], H, W, theta, scale, y0, x0)[..., inv]
+    return _orig_apply(x[..., perm], H, W, theta, scale, y0, x0, inverse)[..., inv]
 
 
-def _apply_rotates_pad(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0):
+def _apply_rotates_pad(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0, inverse=False):
     x = np.asarray(x, dtype=np.float64)
-    out = _orig_apply(x, H, W, theta, scale, y0, x0)
+    out = _orig_apply(x, H, W, theta, scale, y0, x0, inverse)
     if x.shape[1] > H * W:   # rotate the pad row as if it were the token after the grid
         ext = np.zeros((x.shape[0], (H + 1) * W) + x.shape[2:])
         ext[:, :H * W + 1] = x[:, :H * W + 1]
-        out[:, H * W] = _orig_apply(ext, H + 1, W, theta, scale, y0, x0)[:, H * W]
+        out[:, H * W] = _orig_apply(ext, H + 1, W, theta, scale, y0, x0, inverse)[:, H * W]
     return out
 
 
 _orig_apply = R.apply_rope
 
+def _apply_no_inverse(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0, inverse=False):
+    return _orig_apply(x, H, W, theta, scale, y0, x0)
+
+
+def _apply_inverse_skipped_on_pad(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=0.0, inverse=False):
+    out = _orig_apply(x, H, W, theta, scale, y0, x0, inverse)
+    if inverse and out.shape[1] > H * W:
+        out[:, H * W] = 0.0      # drops the pad token's gradient on the way back
+    return out
+
+
 MUTANTS = {
+    "inverse_is_forward": {"apply_rope": _apply_no_inverse},
+    "pad_gradient_dropped": {"apply_rope": _apply_inverse_skipped_on_pad},
     "axes_swapped": {"rope_angles": _angles_axes_swapped},
     "rotation_sign": {"rope_angles": _angles_sign},
     "frequency_exponent_over_d": {"rope_angles": _angles_freq_over_d},
