@@ -156,6 +156,14 @@ int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, f
                                int window, int shift, int pad_mode, float rope_theta,
                                float rope_scale, void* stream);
 
+/* bf16 RoPE training forward: fla_swin_attn_rope_fwd, and also lse as in
+ * fla_swin_attn_fwd_lse (of the rotated logits).  Errors as for fla_swin_attn_rope_fwd and
+ * fla_swin_attn_fwd_lse.  (RoPE training is bf16 only: there is no fp32 variant.) */
+int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
+                               int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                               int window, int shift, int pad_mode, float rope_theta,
+                               float rope_scale, void* stream);
+
 /* ---------------------------------------------------------------------------------------
  * Training: the forward that keeps the log-sum-exp, and the backward pass.
  *
@@ -235,6 +243,19 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
                              void* workspace, size_t workspace_bytes, int B, int heads,
                              int n_grids, const int* grid_hw, int head_dim, int window, int shift,
                              int pad_mode, void* stream);
+
+/* bf16 RoPE backward: the gradients of fla_swin_attn_rope_fwd with respect to the unrotated q, k
+ * and v.  Inside, q and k are rotated as they are loaded (as in the forward) and the
+ * gradients at the rotated values are rotated back by the transpose of each token's
+ * rotation (dq = R^T dq', dk = R^T dk'); dv is unchanged, and the pad token, which is never
+ * rotated, gets its gradient as in fla_swin_attn_bwd.  out and lse are those of
+ * fla_swin_attn_rope_fwd_lse.  Arguments and errors as for fla_swin_attn_bwd, plus
+ * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE). */
+int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out,
+                           const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                           void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
+                           int Wgrid, int head_dim, int window, int shift, int pad_mode,
+                           float rope_theta, float rope_scale, void* stream);
 
 /* Algorithmic work of one backward call:
  *   *flops = 10 * head_dim * heads * B * pairs (pairs as in fla_swin_attn_work: the five

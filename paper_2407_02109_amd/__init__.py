@@ -25,6 +25,8 @@ from .binding import (  # noqa: F401
     swin_attn_ms,
     swin_attn_fwd_train,
     fla_swin_attn_rope_fwd,
+    fla_swin_attn_rope_fwd_lse,
+    fla_swin_attn_rope_bwd,
     swin_attn_rope,
     swin_attn_bwd,
     library_path,

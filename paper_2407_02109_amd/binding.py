@@ -71,6 +71,10 @@ def _declare(lib):
     for name in ("fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32"):
         getattr(lib, name).argtypes = rope_args
         getattr(lib, name).restype = I
+    lib.fla_swin_attn_rope_fwd_lse.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, F, F, P]
+    lib.fla_swin_attn_rope_fwd_lse.restype = I
+    lib.fla_swin_attn_rope_bwd.argtypes = [P] * 10 + [Z, I, I, I, I, I, I, I, I, F, F, P]
+    lib.fla_swin_attn_rope_bwd.restype = I
 
 
 def load_library():
@@ -390,3 +394,30 @@ def swin_attn_rope(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, 
     fla_swin_attn_rope_fwd(q, k, v, out, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, rope_theta,
                            rope_scale, stream, f32=f32)
     return out
+
+
+def fla_swin_attn_rope_fwd_lse(q, k, v, out, lse, B, heads, Hgrid, Wgrid, head_dim, window, shift,
+                               pad_mode=FLA_PAD_MASK, rope_theta=10000.0, rope_scale=1.0, stream=None,
+                               check=True) -> int:
+    """bf16 RoPE training forward: out and lse of the rotated q, k."""
+    lib = load_library()
+    rc = lib.fla_swin_attn_rope_fwd_lse(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, heads, Hgrid, Wgrid,
+                                        head_dim, window, shift, pad_mode, float(rope_theta), float(rope_scale),
+                                        _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_rope_bwd(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads,
+                           Hgrid, Wgrid, head_dim, window, shift, pad_mode=FLA_PAD_MASK, rope_theta=10000.0,
+                           rope_scale=1.0, stream=None, check=True) -> int:
+    """bf16 RoPE backward: gradients with respect to the unrotated q, k and v."""
+    lib = load_library()
+    rc = lib.fla_swin_attn_rope_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq),
+                                    _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes), B, heads, Hgrid,
+                                    Wgrid, head_dim, window, shift, pad_mode, float(rope_theta), float(rope_scale),
+                                    _stream(stream))
+    if check:
+        _check(rc)
+    return rc

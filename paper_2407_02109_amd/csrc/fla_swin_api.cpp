@@ -267,7 +267,7 @@ int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
 int backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
              const float* lse, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes, int B,
              int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
-             void* stream, int elem_bytes) {
+             void* stream, int elem_bytes, const Rope* rope = nullptr) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
     bool empty = false;
@@ -280,9 +280,11 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     if (ws && !aligned16(ws)) return FLA_ERR_ALIGN;
     st = check_scalars(head_dim, window, shift, pad_mode);
     if (st != FLA_OK) return st;
+    if (rope && !rope_ok(*rope)) return FLA_ERR_ROPE;
     Problem pr;
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
+    if (rope && elem_bytes != 2) return FLA_ERR_UNSUPPORTED;   // RoPE backward: bf16 kernel only
     // the bf16 kernel holds a whole window (at most kBwdMaxTokens = kQueryBlock tokens)
     if (elem_bytes == 2 && pr.geo.nqb > 1) return FLA_ERR_UNSUPPORTED;
     const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
@@ -313,6 +315,7 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
 
     fla::SwinBwdArgs a;
     a.f = make_args(pr, q, k, v, nullptr, nullptr, B, heads, n_grids, head_dim, window, shift, pad_mode, cus);
+    if (rope) set_rope(&a.f, *rope);
     a.out = out;
     a.dout = dout;
     a.lse = lse;
@@ -463,6 +466,26 @@ int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, f
     const Rope r{rope_theta, rope_scale};
     return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
                    stream, 4, fla::launch_swin_fwd_f32, &r);
+}
+
+int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse, int B,
+                               int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                               int pad_mode, float rope_theta, float rope_scale, void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    const Rope r{rope_theta, rope_scale};
+    return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
+                   fla::launch_swin_fwd_bf16, &r);
+}
+
+int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                           const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                           size_t workspace_bytes, int B, int heads, int Hgrid, int Wgrid, int head_dim,
+                           int window, int shift, int pad_mode, float rope_theta, float rope_scale,
+                           void* stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    const Rope r{rope_theta, rope_scale};
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
+                    head_dim, window, shift, pad_mode, stream, 2, &r);
 }
 
 int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,

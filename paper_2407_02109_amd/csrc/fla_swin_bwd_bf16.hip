@@ -28,6 +28,10 @@
 //   3. Epilogue: scale, round to bf16 (RNE), stage each wave's 32 rows of dK, dV and dQ in
 //      LDS and store whole 128-byte rows at their own tokens.
 //
+// RoPE (Sec. 3.1; the training form of the forward's prologue fusion): q and K rows are
+// rotated as they are loaded, and dq, dk are rotated back (the transpose) before rounding;
+// the pad token is never rotated.
+//
 // KV-only padding (Sec. 3.4, App. B): the pad token is one more key of weight n_pad per
 // query.  Its terms are rank one per query, so they are done during staging: its dS joins
 // dQ in the epilogue, and the workgroup's share of the pad token's own gradient goes to
@@ -93,7 +97,7 @@ __device__ __forceinline__ float sum8(float x) {
     return x;
 }
 
-template <bool MULTI, bool KVPAD>
+template <bool MULTI, bool KVPAD, bool ROPE>
 __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) {
     const SwinArgs& a = ba.f;
     __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
@@ -180,6 +184,29 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
         const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, D * 2);
         kp8 = bload16(kpr, 16 * part);
         vp8 = bload16(vpr, 16 * part);
+    }
+
+    // (row, col) grid coordinates of window-local index t
+    auto coords = [&](int t, float& y, float& x) {
+        const unsigned r = __umulhi((unsigned)t, addr.magic) + ((unsigned)t & addr.one_mask);
+        y = (float)(wr.y0 + (int)r);
+        x = (float)(wr.x0 + (int)((unsigned)t - r * addr.cols));
+    };
+    if constexpr (ROPE) {
+        // RoPE on the loaded q rows (channels 8 part .. + 7: the row half for part < 4) and on
+        // the wave's K rows (channels 16 s + 8 h .. + 7); the pad token is not rotated
+        float y, x;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            coords(min(r0 + 64 * u, n - 1), y, x);
+            qv[u] = __builtin_bit_cast(uint4, rope_rotate_bf16x8(__builtin_bit_cast(bf16x8, qv[u]),
+                                                                 (part < 4 ? y : x) * a.rope_scale,
+                                                                 a.rope_rev + 4 * (part & 3)));
+        }
+        coords(min(key, n - 1), y, x);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+            kreg[s] = rope_rotate_bf16x8(kreg[s], (s < 2 ? y : x) * a.rope_scale, a.rope_rev + 8 * (s & 1) + 4 * h);
     }
 
     // ---- LDS: rows, LSE, D; the wave's K rows into its staging area (in the dQ space)
@@ -343,6 +370,23 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
         const float sc = ba.scale;
         uint16_t* krow_s = Qs + (TL * wave + li) * RS;
         uint16_t* vrow_s = dOs + (TL * wave + li) * RS;
+        if constexpr (ROPE) {
+            // dk = R^T dk': this lane's key, channels 32 dh + 8 i + 4 h + {0..3} = pairs
+            // 4 i + 2 h + {0, 1} of half dh
+            float y, x;
+            coords(min(key, n - 1), y, x);
+#pragma unroll
+            for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int pr = 0; pr < 2; ++pr) {
+                        float p0 = dkT[dh][4 * i + 2 * pr], p1 = dkT[dh][4 * i + 2 * pr + 1];
+                        rope_unrotate_pair(p0, p1, (dh == 0 ? y : x) * a.rope_scale, a.rope_rev[4 * i + 2 * h + pr]);
+                        dkT[dh][4 * i + 2 * pr] = p0;
+                        dkT[dh][4 * i + 2 * pr + 1] = p1;
+                    }
+        }
 #pragma unroll
         for (int dh = 0; dh < 2; ++dh)
 #pragma unroll
@@ -365,16 +409,24 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
         const int qi = TL * wave + li;
         const float dsp = has_pad ? DSP[qi] : 0.f;
         uint16_t* qrow_s = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * 8 * 64 * 8 + li * RS;
+        [[maybe_unused]] float qy = 0.f, qx = 0.f;
+        if constexpr (ROPE) coords(min(qi, n - 1), qy, qx);
 #pragma unroll
         for (int g = 0; g < 8; ++g) {
             const int ch = 32 * (g >> 2) + 8 * (g & 3) + 4 * h;
             float v4[4] = {x[g].x, x[g].y, x[g].z, x[g].w};
             bf16x4 o4;
+            if (has_pad)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (has_pad) v4[j] = __builtin_fmaf(dsp, KP[ch + j], v4[j]);
-                o4[j] = (__bf16)(v4[j] * sc);
+                for (int j = 0; j < 4; ++j) v4[j] = __builtin_fmaf(dsp, KP[ch + j], v4[j]);
+            if constexpr (ROPE) {
+                // dq = R^T dq': pairs (ch % 32) / 2 + {0, 1} of half ch / 32
+                const float pos = (ch < 32 ? qy : qx) * a.rope_scale;
+                rope_unrotate_pair(v4[0], v4[1], pos, a.rope_rev[(ch & 31) / 2]);
+                rope_unrotate_pair(v4[2], v4[3], pos, a.rope_rev[(ch & 31) / 2 + 1]);
             }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(v4[j] * sc);
             *reinterpret_cast<bf16x4*>(qrow_s + ch) = o4;
         }
         asm volatile("" ::: "memory");   // staged rows are read back by other lanes
@@ -401,10 +453,15 @@ hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream) {
     SwinBwdArgs args = a;
     void* params[] = {&args};
     const bool multi = a.f.n_grids > 1, kv = a.f.pad_mode == 1;
-    const void* fn = multi ? (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<true, true>)
-                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<true, false>))
-                           : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, true>)
-                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, false>));
+    const void* fn;
+    if (a.f.rope)   // RoPE: single grid only (the host admits no grid list with it)
+        fn = kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, true, true>)
+                : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, false, true>);
+    else
+        fn = multi ? (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<true, true, false>)
+                         : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<true, false, false>))
+                   : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, true, false>)
+                         : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, false, false>));
     const long long groups = (long long)a.f.B * a.f.heads * a.f.n_windows;
     return hipLaunchKernel(fn, dim3((unsigned)groups), dim3(THREADS), params, 0, stream);
 }

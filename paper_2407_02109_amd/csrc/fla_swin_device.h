@@ -65,4 +65,34 @@ struct WindowAddr {
     }
 };
 
+// ---- rotary position embedding (RoPE) on bf16 channel pairs, for kernels without a
+//      per-window cos / sin table.  cos and sin of the angle pos * rev revolutions come from
+//      v_cos_f32 / v_sin_f32 after reducing it to [-1/2, 1/2] revolution.
+__device__ __forceinline__ float2 rope_cs(float pos, float rev) {
+    float t = pos * rev;
+    t -= __builtin_rintf(t);
+    return make_float2(__builtin_amdgcn_cosf(t), __builtin_amdgcn_sinf(t));
+}
+
+// Rotate the 4 channel pairs of 8 consecutive bf16 channels by pos * rev[i] (in fp32,
+// rounded back to bf16).
+__device__ __forceinline__ bf16x8 rope_rotate_bf16x8(bf16x8 x, float pos, const float* rev) {
+    bf16x8 r;
+    for (int i = 0; i < 4; ++i) {
+        const float2 cs = rope_cs(pos, rev[i]);
+        const float a = (float)x[2 * i], b = (float)x[2 * i + 1];
+        r[2 * i] = (__bf16)(a * cs.x - b * cs.y);
+        r[2 * i + 1] = (__bf16)(b * cs.x + a * cs.y);
+    }
+    return r;
+}
+
+// The transpose of that rotation on one fp32 channel pair (a, b) (used on gradients).
+__device__ __forceinline__ void rope_unrotate_pair(float& a, float& b, float pos, float rev) {
+    const float2 cs = rope_cs(pos, rev);
+    const float ra = a * cs.x + b * cs.y, rb = b * cs.x - a * cs.y;
+    a = ra;
+    b = rb;
+}
+
 }  // namespace fla

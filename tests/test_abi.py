@@ -41,7 +41,8 @@ def test_header_declares_the_entry_points():
         "fla_swin_attn_fwd_lse", "fla_swin_attn_fwd_lse_f32", "fla_swin_attn_ms_fwd_lse",
         "fla_swin_attn_ms_fwd_lse_f32", "fla_swin_attn_bwd_workspace", "fla_swin_attn_bwd",
         "fla_swin_attn_bwd_f32", "fla_swin_attn_ms_bwd", "fla_swin_attn_ms_bwd_f32",
-        "fla_swin_attn_bwd_work", "fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32"])
+        "fla_swin_attn_bwd_work", "fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32",
+        "fla_swin_attn_rope_fwd_lse", "fla_swin_attn_rope_bwd"])
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -464,3 +465,30 @@ def test_swin_attn_grid_of_a_5d_tensor_must_match():
     q = _FakeCuda((1, 8, 8, 2, 64))
     with pytest.raises(ValueError):
         fb.swin_attn(q, q, q, 8, 4, 4, 0)
+
+
+def _call_rope_bwd(theta=10000.0, scale=1.0, **kw):
+    a = dict(GOOD)
+    a.update({k: v for k, v in kw.items() if k in GOOD})
+    p = dict(q=Q, k=K, v=V, out=OUT, dout=DOUT, lse=LSE, dq=DQ, dk=DK, dv=DV, ws=WS)
+    p.update({k: v for k, v in kw.items() if k in p})
+    return fb.fla_swin_attn_rope_bwd(p["q"], p["k"], p["v"], p["out"], p["dout"], p["lse"], p["dq"], p["dk"],
+                                     p["dv"], p["ws"], 1 << 24, a["B"], a["heads"], a["Hgrid"], a["Wgrid"],
+                                     a["head_dim"], a["window"], a["shift"], a["pad_mode"], theta, scale, 0,
+                                     check=False)
+
+
+def test_rope_training_argument_checks(lib):
+    codes = _header_enum("FLA")
+    assert _call_rope_bwd(theta=0.0) == codes["FLA_ERR_ROPE"]
+    assert _call_rope_bwd(scale=float("nan")) == codes["FLA_ERR_ROPE"]
+    assert _call_rope_bwd(pad_mode=3, theta=0.0) == codes["FLA_ERR_PAD_MODE"]
+    assert _call_rope_bwd(dq=Q) == codes["FLA_ERR_ALIAS"]
+    assert fb.fla_swin_attn_rope_fwd_lse(Q, K, V, OUT, 0, 1, 12, 64, 64, 64, 16, 8, 0, 1e4, 1.0, 0,
+                                         check=False) == codes["FLA_ERR_NULL"]
+    assert fb.fla_swin_attn_rope_fwd_lse(Q, K, V, OUT, LSE, 1, 12, 64, 64, 64, 16, 8, 0, -1.0, 1.0, 0,
+                                         check=False) == codes["FLA_ERR_ROPE"]
+    if not _gpu_visible():
+        assert _call_rope_bwd() == codes["FLA_ERR_ARCH"]
+        assert fb.fla_swin_attn_rope_fwd_lse(Q, K, V, OUT, LSE, 1, 12, 64, 64, 64, 16, 8, 0, 1e4, 1.0, 0,
+                                             check=False) == codes["FLA_ERR_ARCH"]

@@ -98,3 +98,74 @@ def test_full_size_rope_sampled():
     sel = got[pts[:, 0], pts[:, 1] * wl.W + pts[:, 2]]
     err = np.abs(sel - ref)
     assert err.max() <= BF16_MAX and err.mean() <= BF16_MEAN, (err.max(), err.mean())
+
+
+# ---- RoPE training: forward with log-sum-exp, backward (gradients of the unrotated q, k, v)
+BWD_SHAPES = [(2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 300, 16, 15)]
+
+
+def _check_grad(name, got, ref, f32, bulk=True):
+    """Gradient bounds relative to M = max |reference| (as for the plain backward)."""
+    got = synth.to_f64_numpy(got)
+    assert np.isfinite(got).all(), name
+    M = np.abs(ref).max()
+    err = np.abs(got - ref)
+    if f32:
+        assert err.max() <= F32_MAX * M, (name, err.max() / M)
+    else:
+        assert err.max() <= BF16_MAX * M, (name, err.max() / M)
+        if bulk:
+            assert err.mean() <= BF16_MEAN * M, (name, err.mean() / M)
+
+
+# fp32 RoPE training is withdrawn: its first GPU run (the fp32 backward kernels with the
+# rotation added, which made them use 528 bytes of scratch per lane) ended in a GPU memory
+# fault, while the same sources run on the CPU stayed in bounds and matched the oracle.
+# Without a cause shown the fp32 path is not offered and these cases stay skipped.
+_F32_WITHDRAWN = pytest.mark.skip(reason="fp32 RoPE training withdrawn: its first GPU run faulted, cause not "
+                                         "found (sources in bounds on the CPU)")
+
+
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+@pytest.mark.parametrize("dtype", ["bf16", pytest.param("f32", marks=_F32_WITHDRAWN)])
+@pytest.mark.parametrize("shape", BWD_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_rope_training(shape, dtype, pm):
+    B, heads, H, W, k, s = shape
+    theta, scale = 100.0, 0.5
+    f32 = dtype == "f32"
+    _say("rope training %s %s pad_mode=%d" % (shape, dtype, pm))
+    wl = synth.Workload("case", B, heads, H, W, 64, k, s, dtype, seed=300 + sum(shape) + pm, pad_mode=pm)
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    L = H * W
+    out = torch.full_like(q, float("nan"))
+    lse = torch.full((B, heads, L), float("nan"), dtype=torch.float32, device="cuda")
+    assert not f32
+    fb.fla_swin_attn_rope_fwd_lse(q, kk, v, out, lse, B, heads, H, W, 64, k, s, pm, theta, scale)
+    plain = torch.empty_like(q)
+    fb.fla_swin_attn_rope_fwd(q, kk, v, plain, B, heads, H, W, 64, k, s, pm, theta, scale, f32=f32)
+    dq, dk, dv = (torch.full_like(t, float("nan")) for t in (q, kk, v))
+    nws = fb.fla_swin_attn_bwd_workspace(B, heads, [(H, W)], k, s, pm)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    fb.fla_swin_attn_rope_bwd(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, 64, k, s, pm, theta,
+                              scale)
+    torch.cuda.synchronize()
+    assert torch.equal(out, plain)
+    qn, kn, vn, dn = (synth.to_f64_numpy(t) for t in (q, kk, v, dout))
+    lerr = np.abs(synth.to_f64_numpy(lse) - O.swin_attention_rope_lse(qn, kn, vn, H, W, k, s, pm, theta, scale))
+    if f32:
+        assert lerr.max() <= 1e-5, lerr.max()
+    else:
+        # the plain bound plus the bf16 rounding of the rotated q and k: each element moves by at
+        # most 2^-9 relative, so a logit c <q', k'> by at most 2 * 2^-9 * c |q| |k| (a rotation
+        # keeps norms); per query with the largest key norm of its batch entry and head
+        c = 1.0 / 8.0
+        qnorm = np.linalg.norm(qn, axis=-1).transpose(0, 2, 1)                  # [B, heads, L]
+        kmax = np.linalg.norm(kn, axis=-1).max(axis=1)[:, :, None]               # [B, heads, 1]
+        bound = 4e-3 + 2.0 * 2.0 ** -9 * c * qnorm * kmax
+        assert (lerr <= bound).all(), (lerr.max(), bound.min())
+    ref = O.swin_attention_rope_bwd(qn, kn, vn, dn, H, W, k, s, pm, theta, scale)
+    for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+        _check_grad(name, got, r, f32)
+    if pm == 1:
+        _check_grad("dk_pad", dk[:, -1], ref[1][:, -1], f32, bulk=False)
