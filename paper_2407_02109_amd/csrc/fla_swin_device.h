@@ -46,21 +46,21 @@ struct WindowAddr {
     unsigned tok_bytes;   // bytes between adjacent tokens of a row: heads * head_dim * 2
     unsigned magic, one_mask, cols;
 
-    __device__ __forceinline__ void init(int c, unsigned rowb, unsigned tokb) {
+    __host__ __device__ __forceinline__ void init(int c, unsigned rowb, unsigned tokb) {
         cols = (unsigned)c;
-        magic = c > 1 ? (unsigned)(((1ull << 32) + c - 1) / c) : 0u;
+        magic = c > 1 ? 0xffffffffu / (unsigned)c + 1u : 0u;   // ceil(2^32 / c), a 32-bit division
         one_mask = c > 1 ? 0u : 0xffffffffu;
         row_bytes = rowb;
         tok_bytes = tokb;
     }
-    __device__ __forceinline__ unsigned operator()(int t) const {
-        const unsigned r = __umulhi((unsigned)t, magic) + ((unsigned)t & one_mask);
+    __host__ __device__ __forceinline__ unsigned operator()(int t) const {
+        const unsigned r = mulhi_u32((unsigned)t, magic) + ((unsigned)t & one_mask);
         const unsigned c = (unsigned)t - r * cols;
         return r * row_bytes + c * tok_bytes;
     }
     // tokens from the window's first token to window-local index t, for a grid W wide
-    __device__ __forceinline__ unsigned token(int t, unsigned W) const {
-        const unsigned r = __umulhi((unsigned)t, magic) + ((unsigned)t & one_mask);
+    __host__ __device__ __forceinline__ unsigned token(int t, unsigned W) const {
+        const unsigned r = mulhi_u32((unsigned)t, magic) + ((unsigned)t & one_mask);
         return r * W + ((unsigned)t - r * cols);
     }
 };

@@ -13,16 +13,20 @@ __host__ __device__ inline unsigned mulhi_u32(unsigned a, unsigned b) {
 // Unsigned division by a divisor fixed at launch, exact for every n < 2^31.  Powers of two
 // shift; otherwise q = mulhi(n, m) >> s with s = floor(log2 d) and m = ceil(2^(32+s) / d)
 // (Granlund & Montgomery, 1994): m = 2^(32+s)/d + e with 0 <= e < 1, and the error term
-// n*e / 2^(32+s) stays below 1/d while n < 2^(32+s)/d, which exceeds 2^31.
+// n*e / 2^(32+s) stays below 1/d while n < 2^(32+s)/d, which exceeds 2^31.  Both cases are
+// one branch-free expression, (mulhi(n, m) + (n & one)) >> s, with m = 0 and one = ~0 for
+// powers of two and one = 0 otherwise, so the workgroup decode has no branch to wait on.
 struct FastDiv {
-    unsigned m, s;
-    __host__ __device__ unsigned div(unsigned n) const { return (m ? mulhi_u32(n, m) : n) >> s; }
+    unsigned m, s, one;
+    __host__ __device__ unsigned div(unsigned n) const { return (mulhi_u32(n, m) + (n & one)) >> s; }
     static __host__ FastDiv make(unsigned d) {
         FastDiv f;
         unsigned s = 0;
         while ((2ull << s) <= d) ++s;   // s = floor(log2 d)
         f.s = s;
-        f.m = (d & (d - 1)) == 0 ? 0u : (unsigned)((((unsigned long long)1 << (32 + s)) + d - 1) / d);
+        const bool pow2 = (d & (d - 1)) == 0;
+        f.m = pow2 ? 0u : (unsigned)((((unsigned long long)1 << (32 + s)) + d - 1) / d);
+        f.one = pow2 ? ~0u : 0u;
         return f;
     }
 };
