@@ -246,13 +246,25 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
     nws = binding.fla_swin_attn_bwd_workspace(B, heads, grids, wl.window, wl.shift, wl.pad_mode)
     ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=qd.device)
 
-    def fwd():
-        binding.fla_swin_attn_ms_fwd_lse(qd, kd, vd, out, lse, B, heads, grids, d, wl.window, wl.shift,
-                                         wl.pad_mode, stream)
+    if wl.rope:   # RoPE training: rotation fused into the training forward and the backward
+        theta, scale = wl.rope
+        (H, W), = grids
 
-    def bwd():
-        binding.fla_swin_attn_ms_bwd(qd, kd, vd, out, dout, lse, dq, dk, dv, ws, nws, B, heads, grids, d,
-                                     wl.window, wl.shift, wl.pad_mode, stream)
+        def fwd():
+            binding.fla_swin_attn_rope_fwd_lse(qd, kd, vd, out, lse, B, heads, H, W, d, wl.window, wl.shift,
+                                               wl.pad_mode, theta, scale, stream)
+
+        def bwd():
+            binding.fla_swin_attn_rope_bwd(qd, kd, vd, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, d,
+                                           wl.window, wl.shift, wl.pad_mode, theta, scale, stream)
+    else:
+        def fwd():
+            binding.fla_swin_attn_ms_fwd_lse(qd, kd, vd, out, lse, B, heads, grids, d, wl.window, wl.shift,
+                                             wl.pad_mode, stream)
+
+        def bwd():
+            binding.fla_swin_attn_ms_bwd(qd, kd, vd, out, dout, lse, dq, dk, dv, ws, nws, B, heads, grids, d,
+                                         wl.window, wl.shift, wl.pad_mode, stream)
 
     def mean_us(fn, n):
         for _ in range(max(n // 4, 10)):
@@ -418,7 +430,7 @@ def main() -> int:
                      "cold_p10_us": c10, "cold_p50_us": c50, "cold_p90_us": c90,
                      "launch_one_token_p50_us": l50}
     rec["device"] = device_info(torch)
-    if not args.no_backward and not wl.rope:   # the backward has no RoPE form
+    if not args.no_backward:
         print("[bench] backward", file=sys.stderr, flush=True)
         rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps)
     if args.copy_calibration:
