@@ -19,6 +19,7 @@
 //      row sum adds the rounded values with v_dot2_f32_bf16.  O^T += V^T . P^T.
 //      The running max is raised only when a tile exceeds it by more than 2^8 (in the
 //      exp2 domain), so the O^T rescale runs on a handful of tiles, not on every one.
+//      Tiles that end at or before the window's last key run a variant with no mask code.
 //      The kernel is held to 128 VGPRs so that 4 waves share each SIMD (2 workgroups per
 //      CU): while one wave waits on the matrix core, another runs its softmax on the
 //      vector ALU, which is the busier of the two units.
@@ -52,10 +53,11 @@ constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
 constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
 constexpr float kLn2 = 0.693147180559945309f;
 
+template <bool MASKED>
 __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, const uint16_t* __restrict__ Vt,
-                                            bool masked, int t0, int kc0, int nk, int n, float pad_bias_raw,
+                                            int t0, int kc0, int nk, int n, float pad_bias_raw,
                                             const bf16x8 (&qop)[4], floatx16 (&o)[2],
-                                            float& m_run, float& l_run, float c_log2, int lane) {
+                                            float& m_run, float& neg_mc, float& l_run, float c_log2, int lane) {
     const int li = lane & 31;
     const int h = lane >> 5;
     // ---- S^T = K . Q^T for 32 keys x 32 queries: s[r] holds key 8*(r/4) + 4*h + r%4
@@ -65,7 +67,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
     for (int st = 0; st < 4; ++st)
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * st),
                                                     qop[st], s, 0, 0, 0);
-    if (masked) {
+    if constexpr (MASKED) {
         // entry r holds key base + 8*(r/4) + r%4 with base = kc0 + t0 + 4*h
         const int lim = nk - (kc0 + t0 + 4 * h);    // entries below lim are keys of the window
         const int pad = n - (kc0 + t0 + 4 * h);     // the entry that is the pad token (if any)
@@ -75,9 +77,15 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
             s[r] = off < lim ? x : -INFINITY;
         }
     }
-    float mx = fmaxf(s[0], s[1]);
-    for (int r = 2; r < 16; r += 2) mx = fmaxf(mx, fmaxf(s[r], s[r + 1]));
-    mx = xhalf_max(mx);
+    // 16 values -> 1 in 8 operations (v_max3_f32 takes three)
+    float m0 = __builtin_fmaxf(__builtin_fmaxf(s[0], s[1]), s[2]);
+    float m1 = __builtin_fmaxf(__builtin_fmaxf(s[3], s[4]), s[5]);
+    float m2 = __builtin_fmaxf(__builtin_fmaxf(s[6], s[7]), s[8]);
+    float m3 = __builtin_fmaxf(__builtin_fmaxf(s[9], s[10]), s[11]);
+    float m4 = __builtin_fmaxf(__builtin_fmaxf(s[12], s[13]), s[14]);
+    m0 = __builtin_fmaxf(__builtin_fmaxf(m0, m1), m2);
+    m3 = __builtin_fmaxf(__builtin_fmaxf(m3, m4), s[15]);
+    const float mx = xhalf_max(__builtin_fmaxf(m0, m3));
     const bool raise = mx > m_run + kLazyThreshold / c_log2;
     if (__builtin_amdgcn_ballot_w64(raise)) {
         const float m_new = raise ? mx : m_run;
@@ -86,8 +94,8 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         l_run *= alpha;
         o[0] *= alpha;
         o[1] *= alpha;
+        neg_mc = -m_run * c_log2;
     }
-    const float neg_mc = -m_run * c_log2;
     bf16x8 pb[2];
     for (int sg = 0; sg < 2; ++sg) {
         bf16x8 v8;
@@ -96,12 +104,9 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         pb[sg] = v8;
     }
     const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
-    float l0 = l_run, l1 = 0.f;
-    for (int j = 0; j < 8; j += 2) {
-        l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[0][j], pb[0][j + 1]}, ones, l0, false);
-        l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[1][j], pb[1][j + 1]}, ones, l1, false);
-    }
-    l_run = l0 + l1;
+    for (int sg = 0; sg < 2; ++sg)
+        for (int j = 0; j < 8; j += 2)
+            l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[sg][j], pb[sg][j + 1]}, ones, l_run, false);
     for (int sg = 0; sg < 2; ++sg)
         for (int db = 0; db < 2; ++db) {
             const uint16_t* vrow = Vt + (32 * db + li) * VS + t0 + 16 * sg + 4 * h;
@@ -219,6 +224,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
             qop[st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
     }
     float m_run = -INFINITY, l_run = 0.f;
+    float neg_mc = 0.f;   // -m_run * log2(e) / sqrt(d); the first tile always raises the max and sets it
     floatx16 o[2] = {floatx16{}, floatx16{}};   // O^T: [channel block]
 
     for (int kc0 = 0; kc0 < nk; kc0 += KC) {
@@ -329,17 +335,21 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 }
             }
         }
-        // a tile needs masking only if it runs past the keys or holds the pad token
-        if (nq > 0)
-            for (int t0 = 0; t0 < min(ck, kh); t0 += KT)
-                attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
-                            a.scale_log2, lane);
+        // tiles [t_begin, t_end) of the chunk: those that end at or before key n need no mask,
+        // the rest (at most the last two: past the keys, or holding the pad token) do
+        auto attend_range = [&](int t_begin, int t_end) {
+            const int t_plain = min(t_end, t_begin + max(0, (n - kc0 - t_begin) / KT) * KT);
+            for (int t0 = t_begin; t0 < t_plain; t0 += KT)
+                attend_tile<false>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
+                                   a.scale_log2, lane);
+            for (int t0 = t_plain; t0 < t_end; t0 += KT)
+                attend_tile<true>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
+                                  a.scale_log2, lane);
+        };
+        if (nq > 0) attend_range(0, min(ck, kh));
         if (ck > kh) {
             stage_half(1);
-            if (nq > 0)
-                for (int t0 = kh; t0 < ck; t0 += KT)
-                    attend_tile(Ks, Vt, kc0 + t0 + KT > n, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, l_run,
-                                a.scale_log2, lane);
+            if (nq > 0) attend_range(kh, ck);
         }
     }
 
