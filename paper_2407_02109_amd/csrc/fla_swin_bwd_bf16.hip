@@ -22,9 +22,11 @@
 //                                             rows by transposing reads)
 //        dQ^T += K_w^T dS^T                   (dS goes through a per-wave LDS scratch to
 //                                             put queries on the lanes)
-//      The dQ^T tile is added to an fp32 accumulator in LDS (stored at step 0); since no
-//      two waves share a tile within a step, one barrier per step orders the updates and
-//      the sum order is fixed.
+//      The matrix cores do the bookkeeping adds as well: keys past the window's end get -inf
+//      through the C operand of S (so P = 0), -D enters as the C operand of dP, and the tile's
+//      fp32 dQ^T accumulator in LDS is read into the C operand of the dQ^T product and
+//      written back (stored at step 0).  Since no two waves share a tile within a step, one
+//      barrier per step orders the updates and the sum order is fixed.
 //   3. Epilogue: scale, round to bf16 (RNE), stage each wave's 32 rows of dK, dV and dQ in
 //      LDS and store whole 128-byte rows at their own tokens.
 //
@@ -220,7 +222,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
         const float dd = sum8(dot8(gv[u], ov[u]));
         const float lse2 = lse_raw[u] * kLog2e;
         if (part == 0) {
-            Ds[r] = dd;
+            Ds[r] = -dd;   // stored negated: it is the C operand of dP - D
             Ls[r] = lse2;
         }
         if (has_pad) {
@@ -287,11 +289,37 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
     floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
     uint16_t* dst = DST + wave * TL * SS;
     const float c2 = a.scale_log2;
+    // C operand of S = Q K^T: 0, or -inf for a key past the window's last (its P is then 0)
+    floatx16 s_init;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s_init[r] = key_ok ? 0.f : -INFINITY;
     for (int t = 0; t < nt; ++t) {
         if (wave < nt) {
             const int T = wave + t < nt ? wave + t : wave + t - nt;
             const int q0 = TL * T;
-            floatx16 sacc = {}, pacc = {};
+            // the dQ^T accumulator of tile T (written by earlier steps) becomes the C operand of
+            // this step's dQ^T product; fetched first so that the read is long done by then
+            float4* acc = DQ + T * 8 * 64 + lane;
+            floatx16 dq[2];
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                const float4 y = t > 0 ? acc[g * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
+                const int dh = g >> 2, i = g & 3;
+                dq[dh][4 * i] = y.x;
+                dq[dh][4 * i + 1] = y.y;
+                dq[dh][4 * i + 2] = y.z;
+                dq[dh][4 * i + 3] = y.w;
+            }
+            // dP - D in one go: the MFMA's C operand holds -D of each entry's query
+            floatx16 sacc = s_init, pacc;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
+                pacc[4 * i] = d4.x;
+                pacc[4 * i + 1] = d4.y;
+                pacc[4 * i + 2] = d4.z;
+                pacc[4 * i + 3] = d4.w;
+            }
             const uint16_t* qrow = Qs + (q0 + li) * RS + 8 * h;
             const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
 #pragma unroll
@@ -306,15 +334,12 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float4 l4 = *reinterpret_cast<const float4*>(Ls + q0 + 8 * i + 4 * h);
-                const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
                 const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-                const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int r = 4 * i + j;
-                    float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
-                    p = key_ok ? p : 0.f;
-                    const float ds = p * (pacc[r] - dv[j]);
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
+                    const float ds = p * pacc[r];
                     pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
                     sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
                 }
@@ -336,8 +361,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
                     bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
                            sb[i >> 1][4 * (i & 1) + 3]};
             asm volatile("" ::: "memory");   // the scratch reads below follow these writes
-            // dQ^T = K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
-            floatx16 dq[2] = {floatx16{}, floatx16{}};
+            // dQ^T += K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
                 const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
@@ -345,19 +369,10 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
                 for (int dh = 0; dh < 2; ++dh)
                     dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
             }
-            float4* acc = DQ + T * 8 * 64 + lane;
 #pragma unroll
             for (int g = 0; g < 8; ++g) {
                 const int dh = g >> 2, i = g & 3;
-                float4 x = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
-                if (t > 0) {
-                    const float4 y = acc[g * 64];
-                    x.x += y.x;
-                    x.y += y.y;
-                    x.z += y.z;
-                    x.w += y.w;
-                }
-                acc[g * 64] = x;
+                acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
             }
         }
         __syncthreads();
