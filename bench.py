@@ -48,8 +48,9 @@ def kernel_hash(leg: str = "fwd") -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_path(leg: str, workload: str) -> str:
-    return os.path.join(ROOT, "profiles", "traffic_%s%s.json" % ("" if leg == "fwd" else "bwd_", workload))
+def traffic_path(leg: str, workload: str, out_dir: str = "") -> str:
+    return os.path.join(out_dir or os.path.join(ROOT, "profiles"),
+                        "traffic_%s%s.json" % ("" if leg == "fwd" else "bwd_", workload))
 
 
 def measured_traffic(workload: str, leg: str = "fwd"):
@@ -76,10 +77,11 @@ def copy_calibration(nbytes: int = 512 << 20, reps: int = 3):
     torch.cuda.synchronize()
 
 
-def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd"):
+def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_dir: str = ""):
     """Turn rocprofv3 CSV output (kernel trace + FETCH_SIZE + WRITE_SIZE passes) into the
-    committed summaries under profiles/: a markdown table and the traffic JSON of the leg's
-    kernel (swin_fwd_bf16 or swin_bwd_bf16)."""
+    committed summaries under profiles/ (or out_dir): a markdown table and the traffic JSON
+    of the leg's kernel (swin_fwd_bf16 or swin_bwd_bf16)."""
+    out_dir = out_dir or os.path.join(ROOT, "profiles")
     kname = KERNELS[leg][0]
     import csv
     import glob
@@ -136,11 +138,11 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd"):
               "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (fetch_scale, write_scale),
               "Traffic per launch (scaled): %s bytes" % (None if traffic is None else int(traffic)),
               "Kernel source hash: %s" % kernel_hash(leg), ""]
-    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", "%s_%s.md" % (kname, workload)), "w") as f:
+    os.makedirs(out_dir, exist_ok=True)
+    with open(os.path.join(out_dir, "%s_%s.md" % (kname, workload)), "w") as f:
         f.write("\n".join(lines))
     if traffic is not None:
-        with open(traffic_path(leg, workload), "w") as f:
+        with open(traffic_path(leg, workload, out_dir), "w") as f:
             json.dump({"workload": workload, "kernel": kname, "kernel_hash": kernel_hash(leg),
                        "bytes_per_launch": int(traffic),
                        "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],

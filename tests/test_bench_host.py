@@ -1,0 +1,63 @@
+"""Host-side checks of bench.py: the single-GPU guard and the rocprofv3 summary that turns
+FETCH_SIZE / WRITE_SIZE counters into HBM bytes per launch (scaled by what the same
+counters read for a 512 MiB device copy).  No GPU is involved."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def _write(path, header, rows):
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+@pytest.mark.parametrize("leg", ["fwd", "bwd"])
+def test_summary_scales_counters_by_the_copy(tmp_path, leg):
+    kname = bench.KERNELS[leg][0]
+    prof = tmp_path / "prof"
+    # three launches of the workload's grid (durations 10, 12, 14 us) and one tiny launch that
+    # the summary must leave out
+    trace = [["void fla::%s_kernel<false>(x)" % kname, "3468", 1000, 11000],
+             ["void fla::%s_kernel<false>(x)" % kname, "3468", 20000, 32000],
+             ["void fla::%s_kernel<false>(x)" % kname, "3468", 40000, 54000],
+             ["void fla::%s_kernel<false>(x)" % kname, "1", 60000, 60500]]
+    _write(str(prof / "trace" / "run_kernel_trace.csv"), ["Kernel_Name", "Grid_Size_X", "Start_Timestamp",
+                                                          "End_Timestamp"], trace)
+    _write(str(prof / "trace" / "run_kernel_stats.csv"), ["Name", "Calls", "TotalDurationNs", "AverageNs",
+                                                          "Percentage"], [[kname, 4, 36500, 9125, 100.0]])
+    # counters in KiB per dispatch, split over two rows (two XCD groups) for dispatch 7; the
+    # 512 MiB copy reads FETCH_SIZE = 256 MiB (half the bytes) and WRITE_SIZE = 512 MiB
+    hdr = ["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"]
+    _write(str(prof / "fetch_size" / "run_counter_collection.csv"), hdr,
+           [[7, kname, 887808, "FETCH_SIZE", 1000.0], [7, kname, 887808, "FETCH_SIZE", 500.0],
+            [9, "__amd_rocclr_copyBuffer", 1 << 20, "FETCH_SIZE", 262144.0]])
+    _write(str(prof / "write_size" / "run_counter_collection.csv"), hdr,
+           [[7, kname, 887808, "WRITE_SIZE", 2000.0],
+            [9, "__amd_rocclr_copyBuffer", 1 << 20, "WRITE_SIZE", 524288.0]])
+    out = tmp_path / "out"
+    bench.summarize(str(prof), "synthetic", "rocprofv3 ...", leg, out_dir=str(out))
+    rec = json.loads((out / os.path.basename(bench.traffic_path(leg, "synthetic"))).read_text())
+    assert rec["fetch_scale"] == pytest.approx(2.0) and rec["write_scale"] == pytest.approx(1.0)
+    assert rec["bytes_per_launch"] == int(1500 * 1024 * 2.0 + 2000 * 1024)
+    assert rec["avg_duration_us"] == pytest.approx(12.0)   # the tiny launch is not averaged in
+    assert rec["kernel_hash"] == bench.kernel_hash(leg)
+    md = (out / ("%s_synthetic.md" % kname)).read_text()
+    assert "3 dispatches" in md and "rocprofv3 ..." in md
