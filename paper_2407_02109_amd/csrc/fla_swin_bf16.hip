@@ -33,9 +33,9 @@
 // the window and its logit is raised by log2(n_pad)/scale, so in the softmax it carries
 // the weight of the n_pad = window^2 - n virtual slots it stands for.
 //
-// Optional prologue fusion of 2-D RoPE (Sec. 3.1): q in registers and each K row before its
-// LDS write are rotated by their token's grid coordinates, with the cos / sin of the
-// window's row and column positions in a per-workgroup LDS table, so a rotated copy
+// Optional prologue fusion of 2-D RoPE (Sec. 3.1): q in registers, and each K row in place in
+// LDS right after its write, are rotated by their token's grid coordinates, with the cos / sin
+// of the window's row and column positions in a per-workgroup LDS table, so a rotated copy
 // of q and k never goes through HBM.  The pad token has no position and is not rotated.
 #include "fla_swin_device.h"
 
@@ -279,9 +279,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         };
         // K rows of this half (and all of V^T with the first); RoPE on the K rows in place;
         // the pad token if its slot falls in this half; then the barrier
-        // (with RoPE the whole chunk is one "half": deferring half of K would need more than
-        // the 128-VGPR budget next to the rotation)
-        constexpr int kh = ROPE ? KC : KH;
+        constexpr int kh = KH;
         constexpr int its = kh / 64;   // K rows per thread in one half
         auto stage_half = [&](int half) {
             for (int it = its * half; it < its * (half + 1); ++it)
