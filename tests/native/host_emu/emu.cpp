@@ -1,0 +1,53 @@
+// The launch emulation behind hip_runtime.h (see there), a device that reports gfx950, and
+// stand-ins for the bf16 launchers (which the host build does not contain).
+#include <barrier>
+#include <thread>
+#include <vector>
+
+#include "fla_swin_internal.h"
+
+thread_local emu_index threadIdx, blockIdx;
+static std::barrier<>* g_block_barrier = nullptr;
+void __syncthreads() { g_block_barrier->arrive_and_wait(); }
+
+hipError_t hipGetDevice(int* device) {
+    *device = 0;
+    return hipSuccess;
+}
+hipError_t hipGetDeviceProperties(hipDeviceProp_t* prop, int) {
+    std::strcpy(prop->gcnArchName, "gfx950:sramecc+:xnack-");
+    prop->multiProcessorCount = 256;
+    return hipSuccess;
+}
+hipError_t hipGetLastError() { return hipSuccess; }
+
+// every kernel the host build launches takes one argument struct; which one is told by the
+// caller (emu_kernel_args) before each API call
+int emu_kernel_args = 0;   // 0: SwinArgs, 1: SwinBwdArgs
+
+hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, size_t, hipStream_t) {
+    std::barrier<> bar((std::ptrdiff_t)block.x);
+    g_block_barrier = &bar;
+    for (unsigned b = 0; b < grid.x; ++b) {
+        std::vector<std::thread> threads;
+        threads.reserve(block.x);
+        for (unsigned t = 0; t < block.x; ++t)
+            threads.emplace_back([=]() {
+                threadIdx = {t, 0, 0};
+                blockIdx = {b, 0, 0};
+                if (emu_kernel_args == 0)
+                    reinterpret_cast<void (*)(fla::SwinArgs)>(const_cast<void*>(fn))(*static_cast<fla::SwinArgs*>(args[0]));
+                else
+                    reinterpret_cast<void (*)(fla::SwinBwdArgs)>(const_cast<void*>(fn))(
+                        *static_cast<fla::SwinBwdArgs*>(args[0]));
+            });
+        for (auto& th : threads) th.join();
+    }
+    g_block_barrier = nullptr;
+    return hipSuccess;
+}
+
+namespace fla {
+hipError_t launch_swin_fwd_bf16(const SwinArgs&, hipStream_t) { return 1; }
+hipError_t launch_swin_bwd_bf16(const SwinBwdArgs&, hipStream_t) { return 1; }
+}  // namespace fla

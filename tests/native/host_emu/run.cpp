@@ -1,0 +1,74 @@
+// Runs the fp32 training forward and backward of one problem through the C ABI on the host
+// emulation, with every buffer an exact-size heap allocation (AddressSanitizer reports any
+// access outside), and writes inputs and outputs as raw float32 files for the test to compare
+// with the oracle.
+#include <cstdio>
+#include <cstdlib>
+#include <random>
+
+#include "fla_swin.h"
+
+extern int emu_kernel_args;
+
+static float* alloc_random(size_t n, std::mt19937& g) {
+    float* p = static_cast<float*>(std::aligned_alloc(16, ((n * 4 + 15) / 16) * 16));
+    std::normal_distribution<float> d(0.f, 1.f);
+    for (size_t i = 0; i < n; ++i) p[i] = d(g);
+    return p;
+}
+
+static void dump(const char* dir, const char* name, const float* p, size_t n) {
+    char path[1024];
+    std::snprintf(path, sizeof path, "%s/%s.f32", dir, name);
+    FILE* f = std::fopen(path, "wb");
+    std::fwrite(p, 4, n, f);
+    std::fclose(f);
+}
+
+int main(int argc, char** argv) {
+    if (argc != 9) {
+        std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
+        return 2;
+    }
+    const int B = std::atoi(argv[1]), heads = std::atoi(argv[2]), H = std::atoi(argv[3]), W = std::atoi(argv[4]);
+    const int k = std::atoi(argv[5]), s = std::atoi(argv[6]), pm = std::atoi(argv[7]);
+    const char* dir = argv[8];
+    const size_t L = (size_t)H * W, rows = L + (pm ? 1 : 0), tok = (size_t)heads * 64;
+    std::mt19937 g(1234);
+    float* q = alloc_random(B * L * tok, g);
+    float* kk = alloc_random(B * rows * tok, g);
+    float* v = alloc_random(B * rows * tok, g);
+    float* dout = alloc_random(B * L * tok, g);
+    float* out = alloc_random(B * L * tok, g);
+    float* lse = alloc_random((size_t)B * heads * L, g);
+    float* dq = alloc_random(B * L * tok, g);
+    float* dk = alloc_random(B * rows * tok, g);
+    float* dv = alloc_random(B * rows * tok, g);
+    const int hw[2] = {H, W};
+    size_t nws = 0;
+    if (fla_swin_attn_bwd_workspace(B, heads, 1, hw, k, s, pm, &nws) != 0) return 1;
+    void* ws = nws ? std::aligned_alloc(16, ((nws + 15) / 16) * 16) : nullptr;
+    emu_kernel_args = 0;
+    int rc = fla_swin_attn_fwd_lse_f32(q, kk, v, out, lse, B, heads, H, W, 64, k, s, pm, nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "forward: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    emu_kernel_args = 1;
+    rc = fla_swin_attn_bwd_f32(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, 64, k, s, pm, nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "backward: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    dump(dir, "q", q, B * L * tok);
+    dump(dir, "k", kk, B * rows * tok);
+    dump(dir, "v", v, B * rows * tok);
+    dump(dir, "dout", dout, B * L * tok);
+    dump(dir, "out", out, B * L * tok);
+    dump(dir, "lse", lse, (size_t)B * heads * L);
+    dump(dir, "dq", dq, B * L * tok);
+    dump(dir, "dk", dk, B * rows * tok);
+    dump(dir, "dv", dv, B * rows * tok);
+    std::printf("ok\n");
+    return 0;
+}

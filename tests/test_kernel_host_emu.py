@@ -1,0 +1,89 @@
+"""The fp32 kernels and the C ABI, built for the CPU and run against the oracle.
+
+The unmodified sources of the fp32 forward and backward kernels and of the C ABI (launch
+geometry, workgroup decode, window rectangles, workspace layout, pad-token reduction) are
+compiled as host C++ against a small stand-in for the HIP runtime (tests/native/host_emu: a
+launch runs each block's work items as host threads with a barrier for __syncthreads), with
+AddressSanitizer and exact-size buffers.  A run must stay inside every buffer and reproduce
+the fp64 oracle's output, log-sum-exp and gradients to fp32 accuracy.  No GPU is involved;
+the bf16 kernels (matrix-core builtins) are not part of this build."""
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2407_02109_amd", "csrc")
+EMU = os.path.join(ROOT, "tests", "native", "host_emu")
+
+
+def _compiler():
+    for cand in ("/opt/rocm/llvm/bin/clang++", shutil.which("clang++")):
+        if cand and os.path.exists(cand):
+            return cand
+    return None
+
+
+@pytest.fixture(scope="module")
+def emu_binary(tmp_path_factory):
+    cxx = _compiler()
+    if cxx is None:
+        pytest.skip("no clang++ for the host build")
+    d = tmp_path_factory.mktemp("host_emu")
+    src = d / "src"
+    src.mkdir()
+    # sources as they are; the stub device header sits next to them so that their quoted
+    # include finds it first
+    shutil.copy(os.path.join(CSRC, "fla_swin_bwd_f32.hip"), src / "fla_swin_bwd_f32.cpp")
+    shutil.copy(os.path.join(CSRC, "fla_swin_f32.hip"), src / "fla_swin_f32.cpp")
+    shutil.copy(os.path.join(CSRC, "fla_swin_api.cpp"), src / "fla_swin_api.cpp")
+    shutil.copy(os.path.join(CSRC, "fla_swin_internal.h"), src / "fla_swin_internal.h")
+    shutil.copy(os.path.join(EMU, "fla_swin_device.h"), src / "fla_swin_device.h")
+    exe = str(d / "run")
+    cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-pthread",
+           "-I", EMU, "-I", str(src), "-I", os.path.join(ROOT, "include"),
+           str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_swin_api.cpp"),
+           os.path.join(EMU, "emu.cpp"), os.path.join(EMU, "run.cpp"), "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+    if r.returncode != 0:
+        pytest.fail("host build failed:\n" + r.stderr[-4000:])
+    return exe
+
+
+CASES = [  # B, heads, H, W, window, shift, pad_mode
+    (2, 2, 20, 13, 8, 3, 0),    # ragged grid, split windows on every border
+    (1, 3, 37, 29, 16, 8, 1),   # KV-token mode: pad token, workspace and its reduction
+    (1, 1, 9, 40, 16, 15, 1),   # windows of a few rows, shift next to the window size
+    (1, 2, 24, 40, 32, 16, 0),  # windows of more than 256 tokens: several query blocks
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
+def test_fp32_kernels_on_the_host(emu_binary, tmp_path, case):
+    B, heads, H, W, k, s, pm = case
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
+    r = subprocess.run([emu_binary, *map(str, case), str(tmp_path)], capture_output=True, text=True, timeout=900,
+                       env=env)
+    assert r.returncode == 0 and "ok" in r.stdout, r.stderr[-4000:]
+    L = H * W
+    rows = L + (1 if pm else 0)
+
+    def ld(name, r_):
+        a = np.fromfile(str(tmp_path / (name + ".f32")), dtype=np.float32).astype(np.float64)
+        return a.reshape(B, r_, heads, 64)
+
+    q, kk, v, dout = ld("q", L), ld("k", rows), ld("v", rows), ld("dout", L)
+    out = ld("out", L)
+    lse = np.fromfile(str(tmp_path / "lse.f32"), dtype=np.float32).astype(np.float64).reshape(B, heads, L)
+    ref_out = O.swin_attention_textbook(q, kk, v, H, W, k, s, pm)
+    ref_lse = O.swin_attention_lse(q, kk, v, H, W, k, s, pm)
+    assert np.abs(out - ref_out).max() <= 1e-5
+    assert np.abs(lse - ref_lse).max() <= 1e-5
+    refs = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
+    for name, got, ref in zip(("dq", "dk", "dv"), (ld("dq", L), ld("dk", rows), ld("dv", rows)), refs):
+        m = max(1.0, np.abs(ref).max())
+        assert np.abs(got - ref).max() <= 2e-5 * m, name
