@@ -252,3 +252,52 @@ def test_full_size_sampled_windows(name):
                 pv += gv[:, len(idx)]
         _check_grad("dk_pad", torch.from_numpy(dk[:, L]), pk, False, bulk=False)
         _check_grad("dv_pad", torch.from_numpy(dv[:, L]), pv, False, bulk=False)
+
+
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+def test_backward_tensors_beyond_2gib(pm):
+    """Training forward and backward on 24 batch entries of the 4096^2 layer (2.4 GB per
+    tensor): the last entry's windows and pad row lie past 2^31 bytes from the tensor start.
+    Inputs are drawn on the GPU from a seeded generator; windows of the last entry (corner,
+    border, interior) and, in KV-token mode, its pad row are checked against the oracle run on
+    that entry alone."""
+    B, heads, H, W, k, s = 24, 12, 256, 256, 16, 8
+    L = H * W
+    _say("bwd beyond 2 GiB pm=%d" % pm)
+    wl = synth.Workload("big", B, heads, H, W, 64, k, s, "bf16", seed=0, pad_mode=pm)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(21 + pm)
+    rows = L + (1 if pm else 0)
+    q = torch.randn(B, L, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    kk = torch.randn(B, rows, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn(B, rows, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    dout = torch.randn(B, L, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    assert kk.numel() * 2 > (1 << 31)
+    _, _, dq, dk, dv = _train(wl, q, kk, v, dout)
+    last = slice(B - 1, B)
+    qn, kn, vn, dn = (synth.to_f64_numpy(t[last]) for t in (q, kk, v, dout))
+    dqn, dkn, dvn = (synth.to_f64_numpy(t[last]) for t in (dq, dk, dv))
+    rects = _window_rects(H, W, k, s)
+    nwx = len(np.unique(SO._region(np.arange(W), k, s)))
+    pick = sorted({0, nwx - 1, len(rects) - 1, nwx + 1, len(rects) // 2})
+    got = {"dq": [], "dk": [], "dv": []}
+    ref = {"dq": [], "dk": [], "dv": []}
+    for i in pick:
+        idx, (gq, gk, gv) = _window_grads(qn, kn, vn, dn, H, W, rects[i], k, pm, L)
+        n = len(idx)
+        for key, gt, rf in (("dq", dqn[:, idx], gq), ("dk", dkn[:, idx], gk[:, :n]), ("dv", dvn[:, idx], gv[:, :n])):
+            got[key].append(gt)
+            ref[key].append(rf)
+    for key in ref:
+        _check_grad(key, torch.from_numpy(np.concatenate(got[key], axis=1)), np.concatenate(ref[key], axis=1),
+                    False)
+    if pm == 1:
+        pk = np.zeros_like(dkn[:, L])
+        pv = np.zeros_like(dvn[:, L])
+        for rect in rects:
+            if (rect[1] - rect[0]) * (rect[3] - rect[2]) < k * k:
+                idx, (_, gk, gv) = _window_grads(qn, kn, vn, dn, H, W, rect, k, pm, L)
+                pk += gk[:, len(idx)]
+                pv += gv[:, len(idx)]
+        _check_grad("dk_pad", torch.from_numpy(dkn[:, L]), pk, False, bulk=False)
+        _check_grad("dv_pad", torch.from_numpy(dvn[:, L]), pv, False, bulk=False)

@@ -174,3 +174,31 @@ def test_swin_attn_wrapper():
     ref = O.swin_attention_textbook(synth.to_f64_numpy(q), synth.to_f64_numpy(k), synth.to_f64_numpy(v),
                                     12, 12, 8, 4, 1)
     _compare(out, ref, torch.bfloat16)
+
+
+@pytest.mark.parametrize("pad_mode", [0, 1], ids=["mask", "kvtoken"])
+def test_tensors_beyond_2gib(pad_mode):
+    """q, k, v and out of 2.4 GB each (24 batch entries of the 4096^2 layer): windows of the
+    last batch entries sit past 2^31 bytes from the tensor start, so their addressing (64-bit
+    bases, 32-bit offsets within a window) and the pad row of the last entry are exercised.
+    Inputs are drawn on the GPU from a seeded generator; sampled queries of the first, a middle
+    and the last batch entry are checked against the oracle on that entry alone."""
+    B, heads, H, W, k, s = 24, 12, 256, 256, 16, 8
+    L = H * W
+    _say("beyond 2 GiB pad_mode=%d" % pad_mode)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11 + pad_mode)
+    rows = L + (1 if pad_mode else 0)
+    q = torch.randn(B, L, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    kk = torch.randn(B, rows, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn(B, rows, heads, 64, generator=g, device="cuda", dtype=torch.bfloat16)
+    assert q.numel() * 2 > (1 << 31)
+    out = _run(q, kk, v, H, W, k, s, pad_mode)
+    wl1 = synth.Workload("one", 1, heads, H, W, 64, k, s, "bf16", seed=0, pad_mode=pad_mode)
+    for b in (0, 12, B - 1):
+        pts = synth.random_queries(wl1, 64, seed=b).numpy()
+        ref = O.swin_attention_at(synth.to_f64_numpy(q[b:b + 1]), synth.to_f64_numpy(kk[b:b + 1]),
+                                  synth.to_f64_numpy(v[b:b + 1]), H, W, k, s, pad_mode, pts)
+        got = out[b:b + 1].cpu()[pts[:, 0], pts[:, 1] * W + pts[:, 2]]
+        _compare(got, ref, torch.bfloat16)
+    assert torch.isfinite(out[B - 1].float()).all()
