@@ -29,6 +29,9 @@ from .binding import (  # noqa: F401
     fla_swin_attn_rope_bwd,
     swin_attn_rope,
     swin_attn_bwd,
+    swin_attn_rope_fwd_train,
+    swin_attn_rope_bwd,
+    swin_attention,
     library_path,
     load_library,
 )

@@ -421,3 +421,90 @@ def fla_swin_attn_rope_bwd(q, k, v, out, dout, lse, dq, dk, dv, workspace, works
     if check:
         _check(rc)
     return rc
+
+
+def swin_attn_rope_fwd_train(q, k, v, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK, rope_theta=10000.0,
+                             rope_scale=1.0, stream=None):
+    """bf16 RoPE training forward on one grid: returns (out, lse)."""
+    import torch
+    if _check_tensors(q, k, v):
+        raise ValueError("RoPE training takes bf16 tensors")
+    _check_shapes(q, k, v, int(Hgrid) * int(Wgrid), pad_mode)
+    B, L, heads, d = q.shape
+    out = torch.empty_like(q)
+    lse = torch.empty((B, heads, L), dtype=torch.float32, device=q.device)
+    fla_swin_attn_rope_fwd_lse(q, k, v, out, lse, B, heads, Hgrid, Wgrid, d, window, shift, pad_mode, rope_theta,
+                               rope_scale, stream)
+    return out, lse
+
+
+def swin_attn_rope_bwd(q, k, v, out, dout, lse, Hgrid, Wgrid, window, shift, pad_mode=FLA_PAD_MASK,
+                       rope_theta=10000.0, rope_scale=1.0, stream=None):
+    """bf16 RoPE backward on one grid: returns (dq, dk, dv) of the unrotated q, k, v."""
+    import torch
+    if _check_tensors(q, k, v, out, dout):
+        raise ValueError("RoPE training takes bf16 tensors")
+    _check_shapes(q, k, v, int(Hgrid) * int(Wgrid), pad_mode, out, dout)
+    B, L, heads, d = q.shape
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, heads, L) or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 [B, heads, L] tensor")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    nbytes = fla_swin_attn_bwd_workspace(B, heads, [(Hgrid, Wgrid)], window, shift, pad_mode)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=q.device)
+    fla_swin_attn_rope_bwd(q, k, v, out, dout, lse, dq, dk, dv, ws, nbytes, B, heads, Hgrid, Wgrid, d, window,
+                           shift, pad_mode, rope_theta, rope_scale, stream)
+    return dq, dk, dv
+
+
+_autograd_fn = None
+
+
+def _swin_attention_function():
+    """torch.autograd.Function over the training forward (keeps out and lse) and the backward
+    kernels; built on first use so that importing the package does not import torch."""
+    global _autograd_fn
+    if _autograd_fn is not None:
+        return _autograd_fn
+    import torch
+
+    class SwinAttention(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, q, k, v, grids, window, shift, pad_mode, rope):
+            q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+            if rope is None:
+                out, lse = swin_attn_fwd_train(q, k, v, grids, window, shift, pad_mode)
+            else:
+                (H, W), = grids
+                out, lse = swin_attn_rope_fwd_train(q, k, v, H, W, window, shift, pad_mode, rope[0], rope[1])
+            ctx.save_for_backward(q, k, v, out, lse)
+            ctx.cfg = (grids, window, shift, pad_mode, rope)
+            return out
+
+        @staticmethod
+        def backward(ctx, dout):
+            q, k, v, out, lse = ctx.saved_tensors
+            grids, window, shift, pad_mode, rope = ctx.cfg
+            dout = dout.contiguous()
+            if rope is None:
+                dq, dk, dv = swin_attn_bwd(q, k, v, out, dout, lse, grids, window, shift, pad_mode)
+            else:
+                (H, W), = grids
+                dq, dk, dv = swin_attn_rope_bwd(q, k, v, out, dout, lse, H, W, window, shift, pad_mode, rope[0],
+                                                rope[1])
+            return dq, dk, dv, None, None, None, None, None
+
+    _autograd_fn = SwinAttention
+    return SwinAttention
+
+
+def swin_attention(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, rope=None):
+    """Differentiable Flash Swin attention (torch autograd): q [B, L, heads, 64], k and v the
+    same (one more row, the pad token, in KV-token mode), on the current stream.  grids is
+    [(H, W)] or a multi-scale grid list; rope = (theta, scale) fuses 2-D RoPE of q and k
+    (bf16, one grid).  The forward keeps each query's log-sum-exp for the backward."""
+    grids = [(int(h), int(w)) for h, w in grids]
+    if rope is not None:
+        if len(grids) != 1:
+            raise ValueError("RoPE takes a single grid")
+        rope = (float(rope[0]), float(rope[1]))
+    return _swin_attention_function().apply(q, k, v, grids, int(window), int(shift), int(pad_mode), rope)

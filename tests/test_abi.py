@@ -492,3 +492,19 @@ def test_rope_training_argument_checks(lib):
         assert _call_rope_bwd() == codes["FLA_ERR_ARCH"]
         assert fb.fla_swin_attn_rope_fwd_lse(Q, K, V, OUT, LSE, 1, 12, 64, 64, 64, 16, 8, 0, 1e4, 1.0, 0,
                                              check=False) == codes["FLA_ERR_ARCH"]
+
+
+def test_rope_training_wrappers_check_before_launching():
+    import torch
+    q = _FakeCuda((1, 64, 2, 64), torch.float32)
+    with pytest.raises(ValueError):   # RoPE training is bf16 only
+        fb.swin_attn_rope_fwd_train(q, q, q, 8, 8, 4, 0)
+    qb, kb = _FakeCuda((1, 63, 2, 64)), _FakeCuda((1, 64, 2, 64))
+    with pytest.raises(ValueError):   # q rows != H*W
+        fb.swin_attn_rope_fwd_train(qb, kb, kb, 8, 8, 4, 0)
+
+
+def test_swin_attention_rope_takes_one_grid():
+    q = _FakeCuda((1, 80, 2, 64))
+    with pytest.raises(ValueError):
+        fb.swin_attention(q, q, q, [(8, 8), (4, 4)], 4, 0, 0, rope=(1e4, 1.0))
