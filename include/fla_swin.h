@@ -68,10 +68,9 @@ typedef enum {
                               or another output                                          */
     FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
     FLA_ERR_LAUNCH = 11,   /* the HIP runtime refused the kernel launch                    */
-    FLA_ERR_UNSUPPORTED = 12, /* bf16 backward with a window of more than 256 tokens
-                                 (min(window, H) * min(window, W) > 256 for some grid), or
-                                 bf16 RoPE forward with min(window, H) or min(window, W)
-                                 above 32                                                 */
+    FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE backward with a window of more than 256 tokens
+                                 (min(window, H) * min(window, W) > 256), or bf16 RoPE
+                                 forward with min(window, H) or min(window, W) above 32   */
     FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
                                fla_swin_attn_bwd_workspace() reports                      */
     FLA_ERR_ROPE = 14      /* RoPE entry points: rope_theta not finite and > 0, or
@@ -214,11 +213,14 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
  * S = Q.K^T, dP = dO.V^T, dV = P^T.dO, dK = dS^T.Q and dQ = dS.K run on bf16 matrix cores
  * with fp32 accumulation (P and dS rounded to bf16 before their products); outputs are
  * rounded to bf16 (RNE).  The result does not depend on scheduling (fixed summation
- * order).  Windows are limited to 256 tokens (FLA_ERR_UNSUPPORTED), i.e. window <= 16
- * covers every grid.  Errors: checked in the order of the status codes (after the size
- * checks), then FLA_ERR_UNSUPPORTED, FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS,
+ * order).  That is the path for windows of up to 256 tokens (window <= 16 covers every
+ * grid); wider windows (min(window, H) * min(window, W) > 256 for some grid) run on fp32
+ * vector-ALU kernels instead: bf16 inputs widened exactly, every product and sum in fp32,
+ * outputs rounded to bf16 (RNE) once, slower.  Errors: checked in the order of the status
+ * codes (after the size checks), then FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS,
  * FLA_ERR_ARCH; nothing is launched and no output is touched on error.  Asynchronous on
- * `stream`: one kernel (two in FLA_PAD_KVTOKEN mode). */
+ * `stream`: one kernel (three for windows over 256 tokens), and the pad-gradient
+ * reduction in FLA_PAD_KVTOKEN mode. */
 int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                       const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
@@ -250,7 +252,9 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
  * rotation (dq = R^T dq', dk = R^T dk'); dv is unchanged, and the pad token, which is never
  * rotated, gets its gradient as in fla_swin_attn_bwd.  out and lse are those of
  * fla_swin_attn_rope_fwd_lse.  Arguments and errors as for fla_swin_attn_bwd, plus
- * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE). */
+ * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE) and FLA_ERR_UNSUPPORTED for windows of
+ * more than 256 tokens (checked after FLA_ERR_TOO_LARGE): the matrix-core kernel is the
+ * only one with the rotation. */
 int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,

@@ -285,8 +285,10 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
     if (rope && elem_bytes != 2) return FLA_ERR_UNSUPPORTED;   // RoPE backward: bf16 kernel only
-    // the bf16 kernel holds a whole window (at most kBwdMaxTokens = kQueryBlock tokens)
-    if (elem_bytes == 2 && pr.geo.nqb > 1) return FLA_ERR_UNSUPPORTED;
+    // the bf16 matrix-core kernel holds a whole window (at most kBwdMaxTokens = kQueryBlock
+    // tokens); wider bf16 windows go to the fp32-arithmetic kernels, which have no RoPE form
+    const bool wide = pr.geo.nqb > 1;
+    if (elem_bytes == 2 && wide && rope) return FLA_ERR_UNSUPPORTED;
     const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
     if (need > 0 && (!ws || ws_bytes < uint64_t(need))) return FLA_ERR_WORKSPACE;
 
@@ -325,7 +327,7 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.ws = static_cast<float*>(ws);
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = elem_bytes == 2 ? fla::launch_swin_bwd_bf16(a, s) : fla::launch_swin_bwd_f32(a, s);
+    hipError_t e = elem_bytes == 2 && !wide ? fla::launch_swin_bwd_bf16(a, s) : fla::launch_swin_bwd_vec(a, elem_bytes, s);
     if (e == hipSuccess && pad_mode == FLA_PAD_KVTOKEN) e = fla::launch_swin_bwd_pad_reduce(a, elem_bytes, s);
     if (e != hipSuccess) {
         (void)hipGetLastError();
@@ -558,7 +560,7 @@ const char* fla_status_string(int status) {
         case FLA_ERR_ALIAS: return "an output overlaps an input or another output";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";
-        case FLA_ERR_UNSUPPORTED: return "window too large for this bf16 entry point (backward: 256 tokens; RoPE forward: 32 x 32)";
+        case FLA_ERR_UNSUPPORTED: return "window too large for this bf16 entry point (RoPE backward: 256 tokens; RoPE forward: 32 x 32)";
         case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
         case FLA_ERR_ROPE: return "rope_theta must be finite and > 0, rope_scale finite";
         default: return "unknown status";

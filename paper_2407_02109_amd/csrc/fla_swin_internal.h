@@ -105,7 +105,8 @@ struct SwinBwdArgs {
 };
 
 hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
-hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
+// fp32 arithmetic on the vector ALU, any window size; elem_bytes 4: fp32 tensors, 2: bf16
+hipError_t launch_swin_bwd_vec(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
 // sums the partials of ws into row L of dk and dv (elem_bytes 2: bf16, 4: fp32)
 hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
 

@@ -327,13 +327,15 @@ def test_bwd_argument_checks(lib, f32, status, kw):
     assert _call_bwd(f32=f32, **kw) == _header_enum("FLA")[status]
 
 
-def test_bwd_unsupported_window_only_for_bf16(lib):
+def test_bwd_wide_windows_supported_except_rope(lib):
     codes = _header_enum("FLA")
-    # 17 x 17 = 289 tokens per window: over the bf16 kernel's 256
-    assert _call_bwd(window=17, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
+    # 17 x 17 = 289 tokens per window: over the bf16 matrix-core kernel's 256, served by the
+    # fp32-arithmetic kernels in both storage types; only the RoPE backward refuses it
+    assert _call_bwd(window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
     assert _call_bwd(f32=True, window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    # a 32-wide window on a 4-row grid holds 128 tokens: fine
-    assert _call_bwd(Hgrid=4, window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_rope_bwd(window=17, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
+    # a 32-wide window on a 4-row grid holds 128 tokens: fine for RoPE too
+    assert _call_rope_bwd(Hgrid=4, window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
 
 
 def test_bwd_mask_mode_needs_no_workspace(lib):

@@ -89,7 +89,7 @@ SHAPES = [  # B, heads, H, W, window, shift
     (1, 1, 9, 7, 16, 0), (1, 2, 5, 6, 1, 0), (1, 2, 16, 16, 16, 0), (1, 2, 33, 17, 5, 2),
     (1, 1, 1, 1, 1, 0), (1, 1, 9, 300, 16, 15), (1, 2, 1, 40, 16, 7), (2, 1, 40, 1, 8, 7),
 ]
-F32_WIDE = [(1, 2, 40, 24, 20, 10), (1, 1, 40, 40, 32, 16)]   # windows of more than 256 tokens
+WIDE = [(1, 2, 40, 24, 20, 10), (1, 1, 40, 40, 32, 16), (2, 1, 37, 45, 17, 6)]   # windows over 256 tokens
 
 
 def _case(B, heads, H, W, k, s, dtype, pm, seed):
@@ -132,30 +132,41 @@ def test_lse_and_backward(shape, dtype, pm):
 
 
 @pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
-@pytest.mark.parametrize("shape", F32_WIDE, ids=lambda s: "x".join(map(str, s)))
-def test_f32_backward_wide_windows(shape, pm):
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", WIDE, ids=lambda s: "x".join(map(str, s)))
+def test_backward_wide_windows(shape, dtype, pm):
+    """Windows of more than 256 tokens take the three fp32-arithmetic kernels in both storage
+    types (bf16 operands widened exactly, one rounding of each gradient element)."""
     B, heads, H, W, k, s = shape
-    _say("bwd f32 wide %s pad_mode=%d" % (shape, pm))
-    wl, ins, outs = _case(B, heads, H, W, k, s, "f32", pm, seed=7 + pm)
+    _say("bwd wide %s %s pad_mode=%d" % (shape, dtype, pm))
+    f32 = dtype == "f32"
+    wl, ins, outs = _case(B, heads, H, W, k, s, dtype, pm, seed=7 + pm + sum(shape))
     q, kk, v, dout = (synth.to_f64_numpy(t) for t in ins)
     _, lse, dq, dk, dv = outs
-    assert np.abs(synth.to_f64_numpy(lse) - O.swin_attention_lse(q, kk, v, H, W, k, s, pm)).max() <= LSE_F32
-    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)):
-        _check_grad(name, got, ref, True)
+    lerr = np.abs(synth.to_f64_numpy(lse) - O.swin_attention_lse(q, kk, v, H, W, k, s, pm)).max()
+    assert lerr <= (LSE_F32 if f32 else LSE_BF16), lerr
+    gq, gk, gv = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
+    for name, got, ref in (("dq", dq, gq), ("dk", dk, gk), ("dv", dv, gv)):
+        _check_grad(name, got, ref, f32)
+    if pm == 1:
+        _check_grad("dk_pad", dk[:, -1], gk[:, -1], f32, bulk=False)
+        _check_grad("dv_pad", dv[:, -1], gv[:, -1], f32, bulk=False)
 
 
-def test_bf16_backward_rejects_windows_over_256_tokens():
+def test_bf16_rope_backward_rejects_windows_over_256_tokens():
     B, heads, H, W = 1, 1, 40, 24
     wl = _wl(B, heads, H, W, 20, 10, "bf16", 0, 1)
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
     z = torch.zeros_like(q)
     lse = torch.zeros((B, heads, H * W), dtype=torch.float32, device="cuda")
-    rc = fb.fla_swin_attn_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
-                              torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, check=False)
+    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
+                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, 1e4, 1.0, 0,
+                                   check=False)
     assert rc == 12   # FLA_ERR_UNSUPPORTED
     # a 16-wide window on a grid only 16 tokens tall but wide is fine
-    rc = fb.fla_swin_attn_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
-                              torch.empty_like(v), None, 0, B, heads, H, W, 64, 16, 0, 0, check=False)
+    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
+                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 16, 0, 0, 1e4, 1.0, 0,
+                                   check=False)
     torch.cuda.synchronize()
     assert rc == 0
 
