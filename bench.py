@@ -53,6 +53,19 @@ def traffic_path(leg: str, workload: str, out_dir: str = "") -> str:
                         "traffic_%s%s.json" % ("" if leg == "fwd" else "bwd_", workload))
 
 
+def roofline(flops: float, nbytes: float, us: float, traffic):
+    """The roofline that bounds a launch of the given algorithmic work: HBM when its
+    arithmetic intensity is below the ridge (peak FLOP/s / peak B/s = 312.5 FLOP/B), the
+    bf16 matrix cores above it (windows of 1024 tokens and more)."""
+    if flops / nbytes > PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        tf = flops / (us * 1e-6) / 1e12
+        return {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": traffic}
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic}
+
+
 def measured_traffic(workload: str, leg: str = "fwd"):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
     or None when it is missing or was taken on another version of the kernel source."""
@@ -237,7 +250,8 @@ def per_call_us(step, stream, calls: int, before=None):
 def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
     """Training on the same layer: the forward that keeps the log-sum-exp, then the backward
     (dq, dk, dv for a seeded upstream gradient), each timed with events on the stream.  The
-    roofline is that of swin_bwd_bf16_kernel, the backward's dominant kernel."""
+    roofline is that of swin_bwd_bf16_kernel, the backward's dominant kernel (windows of more
+    than 256 tokens: swin_bwd_bf16_wide_kernel and the dq reduction)."""
     import torch
     grids = list(wl.grid_list)
     B, L, heads, d = qd.shape
@@ -286,12 +300,9 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
     assert torch.isfinite(dq[:, :64].float()).all() and torch.isfinite(dk[:, :64].float()).all()
     flops, nbytes = binding.fla_swin_attn_bwd_work(B, heads, grids, d, wl.window, wl.shift, wl.pad_mode, 2)
     tflops = flops / (us * 1e-6) / 1e12
-    gbs = nbytes / (us * 1e-6) / 1e9
     return {"us_per_layer": round(us, 3), "steps": steps, "fwd_lse_us": round(fwd_us, 3),
             "tflops": round(tflops, 2), "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": round(gbs / PEAK_HBM_GBS, 4),
-                         "traffic": measured_traffic(wl.name, "bwd")},
+            "roofline": roofline(flops, nbytes, us, measured_traffic(wl.name, "bwd")),
             "alg_flops": flops, "alg_bytes": nbytes,
             "timing": {"p10_us": p10, "p50_us": p50, "p90_us": p90}}
 
@@ -387,7 +398,6 @@ def main() -> int:
     gpu_ms = ev0.elapsed_time(ev1)
     us = gpu_ms * 1e3 / args.steps
     tflops = flops / (us * 1e-6) / 1e12
-    gbs = nbytes / (us * 1e-6) / 1e9
     assert torch.isfinite(out[:, :64].float()).all()
 
     traffic = measured_traffic(wl.name)
@@ -410,9 +420,7 @@ def main() -> int:
                    "pad_mode": wl.pad_mode, "parallelism": "none (1 GPU)"},
         "tflops": round(tflops, 2),
         "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "traffic": traffic},
+        "roofline": roofline(flops, nbytes, us, traffic),
         "alg_flops": flops,
         "alg_bytes": nbytes,
     }

@@ -195,11 +195,16 @@ int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v,
                                  float* lse, int B, int heads, int n_grids, const int* grid_hw,
                                  int head_dim, int window, int shift, int pad_mode, void* stream);
 
-/* Workspace the backward needs, in bytes (host arithmetic only): in FLA_PAD_KVTOKEN mode
- * 512 bytes per (batch entry, head, window, block of 256 window tokens), holding each
- * block's share of the pad token's gradient; 0 in FLA_PAD_MASK mode.  Single-grid callers
- * pass n_grids = 1 and grid_hw = {Hgrid, Wgrid}.  Argument errors as for the forward;
- * bytes must be non-NULL (FLA_ERR_NULL). */
+/* Workspace the backward needs, in bytes (host arithmetic only).  With nqb = the number of
+ * 256-token blocks of the largest window (1 when every window has at most 256 tokens):
+ *   - FLA_PAD_KVTOKEN mode: 512 bytes per (batch entry, head, window, block), each block's
+ *     share of the pad token's gradient;
+ *   - nqb > 1 (the bf16 kernels; the fp32 ones need only the part above): nqb * 256 * 64 * 4
+ *     bytes per (batch entry, head, window, key block), each key block's fp32 share of dq.
+ * So 0 in FLA_PAD_MASK mode for windows of up to 256 tokens.  The largest amount is that of
+ * the bf16 entry points; the fp32 ones accept it.  Single-grid callers pass n_grids = 1 and
+ * grid_hw = {Hgrid, Wgrid}.  Argument errors as for the forward; bytes must be non-NULL
+ * (FLA_ERR_NULL). */
 int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,
                                 int shift, int pad_mode, size_t* bytes);
 
@@ -213,14 +218,14 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
  * S = Q.K^T, dP = dO.V^T, dV = P^T.dO, dK = dS^T.Q and dQ = dS.K run on bf16 matrix cores
  * with fp32 accumulation (P and dS rounded to bf16 before their products); outputs are
  * rounded to bf16 (RNE).  The result does not depend on scheduling (fixed summation
- * order).  That is the path for windows of up to 256 tokens (window <= 16 covers every
- * grid); wider windows (min(window, H) * min(window, W) > 256 for some grid) run on fp32
- * vector-ALU kernels instead: bf16 inputs widened exactly, every product and sum in fp32,
- * outputs rounded to bf16 (RNE) once, slower.  Errors: checked in the order of the status
- * codes (after the size checks), then FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS,
- * FLA_ERR_ARCH; nothing is launched and no output is touched on error.  Asynchronous on
- * `stream`: one kernel (three for windows over 256 tokens), and the pad-gradient
- * reduction in FLA_PAD_KVTOKEN mode. */
+ * order).  One workgroup holds a window of up to 256 tokens (window <= 16 covers every
+ * grid); wider windows (min(window, H) * min(window, W) > 256 for some grid) are taken in
+ * key blocks of 256, each writing its fp32 share of dq to the workspace, and a second
+ * kernel sums the shares in block order and rounds dq once.  Errors: checked in the order
+ * of the status codes (after the size checks), then FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE,
+ * FLA_ERR_ALIAS, FLA_ERR_ARCH; nothing is launched and no output is touched on error.
+ * Asynchronous on `stream`: one kernel (two for windows over 256 tokens), and the
+ * pad-gradient reduction in FLA_PAD_KVTOKEN mode. */
 int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                       const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
@@ -253,8 +258,8 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
  * rotated, gets its gradient as in fla_swin_attn_bwd.  out and lse are those of
  * fla_swin_attn_rope_fwd_lse.  Arguments and errors as for fla_swin_attn_bwd, plus
  * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE) and FLA_ERR_UNSUPPORTED for windows of
- * more than 256 tokens (checked after FLA_ERR_TOO_LARGE): the matrix-core kernel is the
- * only one with the rotation. */
+ * more than 256 tokens (checked after FLA_ERR_TOO_LARGE): only the kernel that holds a
+ * whole window has the rotation. */
 int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,

@@ -257,11 +257,18 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
     return FLA_OK;
 }
 
-// Workspace bytes of a backward call: one pad-gradient partial per (b, head, window, query
-// block) in KV-token mode, none otherwise.  Assumes the geometry is valid.
-int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
+// Workspace bytes of a backward call: one pad-gradient partial per (b, head, window, block)
+// in KV-token mode; for the bf16 kernels on windows of more than 256 tokens (dq_shares)
+// also each key block's fp32 share of the window's dq.  Assumes the geometry is valid.
+int64_t pad_partial_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
     if (pad_mode != FLA_PAD_KVTOKEN) return 0;
     return int64_t(B) * heads * geo.n_windows * geo.nqb * fla::kPadPartial * 4;
+}
+int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode, bool dq_shares) {
+    int64_t n = pad_partial_bytes(B, heads, geo, pad_mode);
+    if (dq_shares)
+        n += int64_t(B) * heads * geo.n_windows * geo.nqb * geo.nqb * fla::kQueryBlock * fla::kHeadDim * 4;
+    return n;
 }
 
 int backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
@@ -284,12 +291,12 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     Problem pr;
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
-    if (rope && elem_bytes != 2) return FLA_ERR_UNSUPPORTED;   // RoPE backward: bf16 kernel only
-    // the bf16 matrix-core kernel holds a whole window (at most kBwdMaxTokens = kQueryBlock
-    // tokens); wider bf16 windows go to the fp32-arithmetic kernels, which have no RoPE form
+    // windows of more than kBwdMaxTokens = kQueryBlock tokens take several key blocks; the
+    // RoPE backward exists only for the bf16 kernel that holds a whole window
     const bool wide = pr.geo.nqb > 1;
-    if (elem_bytes == 2 && wide && rope) return FLA_ERR_UNSUPPORTED;
-    const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
+    if (rope && (elem_bytes != 2 || wide)) return FLA_ERR_UNSUPPORTED;
+    const bool dq_shares = elem_bytes == 2 && wide;
+    const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode, dq_shares);
     if (need > 0 && (!ws || ws_bytes < uint64_t(need))) return FLA_ERR_WORKSPACE;
 
     const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
@@ -325,9 +332,12 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.dk = dk;
     a.dv = dv;
     a.ws = static_cast<float*>(ws);
+    a.ws_dq = dq_shares ? a.ws + pad_partial_bytes(B, heads, pr.geo, pad_mode) / 4 : nullptr;
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = elem_bytes == 2 && !wide ? fla::launch_swin_bwd_bf16(a, s) : fla::launch_swin_bwd_vec(a, elem_bytes, s);
+    hipError_t e = elem_bytes != 2 ? fla::launch_swin_bwd_f32(a, s)
+                   : wide         ? fla::launch_swin_bwd_bf16_wide(a, s)
+                                  : fla::launch_swin_bwd_bf16(a, s);
     if (e == hipSuccess && pad_mode == FLA_PAD_KVTOKEN) e = fla::launch_swin_bwd_pad_reduce(a, elem_bytes, s);
     if (e != hipSuccess) {
         (void)hipGetLastError();
@@ -506,7 +516,7 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
     Problem pr;
     st = check_limits(B, heads, n_grids, grid_hw, fla::kHeadDim, window, shift, pad_mode, 2, &pr);
     if (st != FLA_OK) return st;
-    *bytes = (size_t)workspace_bytes(B, heads, pr.geo, pad_mode);
+    *bytes = (size_t)workspace_bytes(B, heads, pr.geo, pad_mode, pr.geo.nqb > 1);
     return FLA_OK;
 }
 

@@ -7,6 +7,9 @@
 //   dV = P^T dO,  dK = c dS^T Q,  dQ = c dS K
 // P is recomputed, never stored.  A window of window <= 16 has at most 256 tokens, so one
 // workgroup takes a whole (batch entry, window, head) and no gradient leaves it half done.
+// Wider windows take swin_bwd_bf16_wide_kernel (further down): the same steps per key
+// block of 256, with the queries streamed in chunks and dq summed over the key blocks by
+// a second kernel.
 //
 // Per workgroup (512 threads = 8 waves):
 //   1. Q and dO rows of the window -> LDS (row-major, 144-byte rows); LSE and D per query
@@ -462,6 +465,378 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
     }
 }
 
+// ---- windows of more than 256 tokens (window > 16 on grids that hold such a window)
+//
+// One workgroup per (batch entry, window, key block of 256 tokens, head).  The block's keys
+// stay with the waves as above (32 per wave, dK and dV accumulated in registers over the
+// whole window), and the window's queries stream through LDS in chunks of 256 with the same
+// step rotation, over max(query tiles, key tiles) steps so that the two counts may differ.
+// dQ of a chunk then holds only this key block's share: it goes, unscaled, to the workspace
+// as fp32, and swin_bwd_dq_reduce_kernel sums the key blocks' shares in block order,
+// scales by c and rounds once.  In KV-token mode key block 0 also takes the pad token's
+// per-query terms (its dS k_pad joins that block's dQ share).
+constexpr int OFF_PP = LDS_BYTES;                       // pad-token P  [256] fp32
+constexpr int WIDE_LDS_BYTES = OFF_PP + NMAX * 4;
+static_assert(WIDE_LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
+
+template <bool MULTI, bool KVPAD>
+__global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs ba) {
+    const SwinArgs& a = ba.f;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[WIDE_LDS_BYTES];
+    uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_Q);
+    uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_DO);
+    float4* DQ = reinterpret_cast<float4*>(smem + OFF_DQ);
+    float* Ls = reinterpret_cast<float*>(smem + OFF_LSE);
+    float* Ds = reinterpret_cast<float*>(smem + OFF_DD);
+    float* DSP = reinterpret_cast<float*>(smem + OFF_DSP);
+    float* KP = reinterpret_cast<float*>(smem + OFF_KP);
+    uint16_t* DST = reinterpret_cast<uint16_t*>(smem + OFF_DST);
+    float* PP = reinterpret_cast<float*>(smem + OFF_PP);
+
+    // ---- workgroup -> (b, window, key block, head), heads fastest
+    const unsigned id0 = blockIdx.x;
+    const unsigned id1 = a.div_heads.div(id0);
+    const int head = (int)(id0 - id1 * (unsigned)a.heads);
+    const unsigned id2 = a.div_nqb.div(id1);
+    const int kb = (int)(id1 - id2 * (unsigned)a.nqb);
+    const unsigned id3 = a.div_nwin.div(id2);
+    const int win = (int)(id2 - id3 * (unsigned)a.n_windows);
+    const int b = (int)id3;
+
+    const WindowRect wr = window_rect<MULTI>(a, win);
+    const int n = wr.rows * wr.cols;
+    const long long n_pad = (long long)a.window * a.window - n;
+    const int tid = threadIdx.x;
+    // this block's entries: pad-gradient partial and dQ share
+    const long long e = (((long long)b * a.heads + head) * a.n_windows + win) * a.nqb + kb;
+    const int key0 = NMAX * kb;
+    if (key0 >= n) {   // the window has fewer key blocks; its pad partial is still read
+        if (KVPAD && tid < kPadPartial) ba.ws[e * kPadPartial + tid] = 0.f;
+        return;
+    }
+    const int nkeys = min(NMAX, n - key0);
+    const int nkt = (nkeys + TL - 1) / TL;
+    const bool pad_here = KVPAD && n_pad > 0 && kb == 0;
+
+    const long long win_elems = wr.tok0 * a.tok_stride + head * D;
+    const long long q_base = (long long)b * a.q_batch_stride + win_elems;
+    const long long kv_base = (long long)b * a.kv_batch_stride + win_elems;
+    const long long q_bytes = ((long long)a.B * a.q_batch_stride - q_base) * 2;
+    const long long kv_bytes = ((long long)a.B * a.kv_batch_stride - kv_base) * 2;
+    const __amdgpu_buffer_rsrc_t qr = make_rsrc(static_cast<const uint16_t*>(a.q) + q_base, q_bytes);
+    const __amdgpu_buffer_rsrc_t orr = make_rsrc(static_cast<const uint16_t*>(ba.out) + q_base, q_bytes);
+    const __amdgpu_buffer_rsrc_t dor = make_rsrc(static_cast<const uint16_t*>(ba.dout) + q_base, q_bytes);
+    const __amdgpu_buffer_rsrc_t kr = make_rsrc(static_cast<const uint16_t*>(a.k) + kv_base, kv_bytes);
+    const __amdgpu_buffer_rsrc_t vr = make_rsrc(static_cast<const uint16_t*>(a.v) + kv_base, kv_bytes);
+    const __amdgpu_buffer_rsrc_t dkr = make_rsrc(static_cast<uint16_t*>(ba.dk) + kv_base, kv_bytes);
+    const __amdgpu_buffer_rsrc_t dvr = make_rsrc(static_cast<uint16_t*>(ba.dv) + kv_base, kv_bytes);
+    const long long lse_base = ((long long)b * a.heads + head) * a.L + wr.tok0;
+    const long long lse_total = (long long)a.B * a.heads * a.L;
+    const __amdgpu_buffer_rsrc_t lr = make_rsrc(ba.lse + lse_base, (lse_total - lse_base) * 4);
+
+    WindowAddr addr;
+    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
+
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 31;
+    const int h = lane >> 5;
+
+    // ---- K_w and V_w rows (B operands), lane: key key0 + 32 wave + li
+    const int key = TL * wave + li;
+    const bool key_ok = key < nkeys;
+    const unsigned krow = key_ok ? addr(key0 + key) : kOutside;
+    bf16x8 kreg[4], vreg[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        kreg[s] = __builtin_bit_cast(bf16x8, bload16(kr, krow + 32 * s + 16 * h));
+        vreg[s] = __builtin_bit_cast(bf16x8, bload16(vr, krow + 32 * s + 16 * h));
+    }
+    const int part = tid & 7;
+    const int r0 = tid >> 3;
+    // pad row (key block 0 in KV-token mode), read again per chunk so that it does not stay
+    // in registers through the steps
+    const long long pad_elems = (long long)b * a.kv_batch_stride + a.L * a.tok_stride + head * D;
+    const __amdgpu_buffer_rsrc_t kpr = make_rsrc(static_cast<const uint16_t*>(a.k) + pad_elems, pad_here ? D * 2 : 0);
+    const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, pad_here ? D * 2 : 0);
+    // K_w^T (A operand of dQ^T = K^T dS^T) through the staging rows in the dQ space
+    uint16_t* kstage = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * TL * RS;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+        *reinterpret_cast<bf16x8*>(kstage + li * RS + 16 * s + 8 * h) = kreg[s];
+    if (pad_here && tid < 8) {
+        const bf16x8 k8 = __builtin_bit_cast(bf16x8, bload16(kpr, 16 * part));
+        for (int j = 0; j < 8; ++j) KP[8 * part + j] = (float)k8[j];
+    }
+    __syncthreads();
+    bf16x8 kt[2][2];
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) kt[dh][s2] = tr_operand(kstage, RS, 16 * s2, 32 * dh, lane);
+    __syncthreads();   // the staging rows are the accumulators of the first chunk
+
+    // key block 0, KV-token mode: thread c < 64 sums channel c of the pad token's dk, thread
+    // 64 + c channel c of its dv, over the chunks
+    float pad_acc = 0.f;
+    floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
+    uint16_t* dst = DST + wave * TL * SS;
+    const float c2 = a.scale_log2;
+    // C operand of S: 0, or -inf past the block's last key (one register, spread per step)
+    const float s0 = key_ok ? 0.f : -INFINITY;
+    float* wsq = ba.ws_dq + e * ((long long)a.nqb * kQueryBlock * D);   // [query of the window][64]
+
+    const int nqc = (n + NMAX - 1) / NMAX;
+    for (int qc = 0; qc < nqc; ++qc) {
+        const int qbase = NMAX * qc;
+        const int nq = min(NMAX, n - qbase);
+        const int nqt = (nq + TL - 1) / TL;
+        // ---- the chunk's Q, dO, O rows (zero past its end) and LSE; zero accumulators
+        uint4 qv[4], gv[4], ov[4], kp8 = {0u, 0u, 0u, 0u}, vp8 = {0u, 0u, 0u, 0u};
+        if (pad_here) {
+            kp8 = bload16(kpr, 16 * part);
+            vp8 = bload16(vpr, 16 * part);
+        }
+        float lse_raw[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int r = r0 + 64 * u;
+            const unsigned off = r < nq ? addr(qbase + r) + 16 * part : kOutside;
+            qv[u] = bload16(qr, off);
+            gv[u] = bload16(dor, off);
+            ov[u] = bload16(orr, off);
+            lse_raw[u] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(
+                           lr, r < nq ? 4 * addr.token(qbase + r, (unsigned)wr.W) : kOutside, 0, 0));
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) DQ[tid + THREADS * i] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int r = r0 + 64 * u;
+            *reinterpret_cast<uint4*>(Qs + r * RS + 8 * part) = qv[u];
+            *reinterpret_cast<uint4*>(dOs + r * RS + 8 * part) = gv[u];
+            const float dd = sum8(dot8(gv[u], ov[u]));
+            const float lse2 = lse_raw[u] * kLog2e;
+            if (part == 0) {
+                Ds[r] = -dd;
+                Ls[r] = lse2;
+            }
+            if (pad_here) {
+                const float zp = sum8(dot8(qv[u], kp8));
+                const float dp = sum8(dot8(gv[u], vp8));
+                const float p = r < nq ? __builtin_amdgcn_exp2f(__builtin_fmaf(zp, c2, log2f((float)n_pad) - lse2))
+                                       : 0.f;
+                if (part == 0) {
+                    DSP[r] = p * (dp - dd);
+                    PP[r] = p;
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- steps: wave w takes query tile (w + t) mod M; with w < nkt <= M no two waves
+        //      share a tile within a step, and each wave meets every tile once
+        const int M = nqt > nkt ? nqt : nkt;
+        for (int t = 0; t < M; ++t) {
+            const int T = wave + t < M ? wave + t : wave + t - M;
+            if (wave < nkt && T < nqt) {
+                const int q0 = TL * T;
+                float4* acc = DQ + T * 8 * 64 + lane;
+                floatx16 dq[2];
+#pragma unroll
+                for (int g = 0; g < 8; ++g) {
+                    const float4 y = acc[g * 64];
+                    const int dh = g >> 2, i = g & 3;
+                    dq[dh][4 * i] = y.x;
+                    dq[dh][4 * i + 1] = y.y;
+                    dq[dh][4 * i + 2] = y.z;
+                    dq[dh][4 * i + 3] = y.w;
+                }
+                floatx16 sacc, pacc;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) sacc[r] = s0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
+                    pacc[4 * i] = d4.x;
+                    pacc[4 * i + 1] = d4.y;
+                    pacc[4 * i + 2] = d4.z;
+                    pacc[4 * i + 3] = d4.w;
+                }
+                const uint16_t* qrow = Qs + (q0 + li) * RS + 8 * h;
+                const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s),
+                                                                  kreg[s], sacc, 0, 0, 0);
+                    pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s),
+                                                                  vreg[s], pacc, 0, 0, 0);
+                }
+                bf16x8 pb[2], sb[2];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float4 l4 = *reinterpret_cast<const float4*>(Ls + q0 + 8 * i + 4 * h);
+                    const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int r = 4 * i + j;
+                        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
+                        const float ds = p * pacc[r];
+                        pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
+                        sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
+                    }
+                }
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                    for (int dh = 0; dh < 2; ++dh) {
+                        const bf16x8 ga = tr_operand(dOs, RS, q0 + 16 * sg, 32 * dh, lane);
+                        const bf16x8 qa = tr_operand(Qs, RS, q0 + 16 * sg, 32 * dh, lane);
+                        dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
+                        dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
+                    }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
+                        bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
+                               sb[i >> 1][4 * (i & 1) + 3]};
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
+#pragma unroll
+                    for (int dh = 0; dh < 2; ++dh)
+                        dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
+                }
+#pragma unroll
+                for (int g = 0; g < 8; ++g) {
+                    const int dh = g >> 2, i = g & 3;
+                    acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
+                }
+            }
+            __syncthreads();
+        }
+
+        // ---- this key block's dQ share of the chunk -> workspace, 16 lanes per 256-byte row;
+        //      accumulator entry (tile T, g, lane) holds query 32 T + (lane & 31), channels
+        //      32 (g >> 2) + 8 (g & 3) + 4 (lane >> 5) + {0..3}
+#pragma unroll
+        for (int it = 0; it < NMAX / 32; ++it) {
+            const int row = 32 * it + (tid >> 4);
+            const int ch = 4 * (tid & 15);
+            if (row < nq) {
+                float4 x = DQ[(row >> 5) * 8 * 64 + (4 * (ch >> 5) + ((ch & 31) >> 3)) * 64 + (row & 31) +
+                              32 * ((ch >> 2) & 1)];
+                if (pad_here) {
+                    const float d = DSP[row];
+                    x.x = __builtin_fmaf(d, KP[ch], x.x);
+                    x.y = __builtin_fmaf(d, KP[ch + 1], x.y);
+                    x.z = __builtin_fmaf(d, KP[ch + 2], x.z);
+                    x.w = __builtin_fmaf(d, KP[ch + 3], x.w);
+                }
+                *reinterpret_cast<float4*>(wsq + (long long)(qbase + row) * D + ch) = x;
+            }
+        }
+        // pad token's gradient over the chunk's queries (rows past the chunk have dS = P = 0):
+        // dk_pad += sum dS_p q, dv_pad += sum P_p dO, in row order
+        if (pad_here && tid < kPadPartial) {
+            const float* w = tid < D ? DSP : PP;
+            const uint16_t* col = (tid < D ? Qs : dOs) + (tid & (D - 1));
+            for (int r = 0; r < nq; ++r)
+                pad_acc = __builtin_fmaf(w[r], __uint_as_float((unsigned)col[r * RS] << 16), pad_acc);
+        }
+        __syncthreads();   // the next chunk overwrites rows, D, LSE, pad terms and accumulators
+    }
+
+    // ---- pad-gradient partial: key block 0's sums, zero from the others
+    if (KVPAD && tid < kPadPartial) ba.ws[e * kPadPartial + tid] = tid < D ? pad_acc * ba.scale : pad_acc;
+
+    // ---- dK, dV of the block's keys: stage each wave's 32 rows, store whole 128-byte rows
+    if (wave < nkt) {
+        const float sc = ba.scale;
+        uint16_t* krow_s = Qs + (TL * wave + li) * RS;
+        uint16_t* vrow_s = dOs + (TL * wave + li) * RS;
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                bf16x4 k4, v4;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    k4[j] = (__bf16)(dkT[dh][4 * i + j] * sc);
+                    v4[j] = (__bf16)dvT[dh][4 * i + j];
+                }
+                *reinterpret_cast<bf16x4*>(krow_s + 32 * dh + 8 * i + 4 * h) = k4;
+                *reinterpret_cast<bf16x4*>(vrow_s + 32 * dh + 8 * i + 4 * h) = v4;
+            }
+        asm volatile("" ::: "memory");   // staged rows are read back by other lanes
+        const int sp = lane & 7;
+#pragma unroll
+        for (int it = 0; it < TL / 8; ++it) {
+            const int rl = TL * wave + 8 * it + (lane >> 3);
+            const unsigned off = rl < nkeys ? addr(key0 + rl) + 16 * sp : kOutside;
+            const uint4 kx = *reinterpret_cast<const uint4*>(Qs + rl * RS + 8 * sp);
+            const uint4 vx = *reinterpret_cast<const uint4*>(dOs + rl * RS + 8 * sp);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, kx), dkr, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, vx), dvr, off, 0, 0);
+        }
+    }
+}
+
+// dq of windows of more than 256 tokens: one workgroup per (batch entry, window, query block
+// of 256, head) sums the key blocks' fp32 shares of its queries in block order, scales by c,
+// rounds to bf16 once and stores whole rows (8 threads per 128-byte row).
+template <bool MULTI>
+__global__ __launch_bounds__(THREADS) void swin_bwd_dq_reduce_kernel(SwinBwdArgs ba) {
+    const SwinArgs& a = ba.f;
+    const unsigned id0 = blockIdx.x;
+    const unsigned id1 = a.div_heads.div(id0);
+    const int head = (int)(id0 - id1 * (unsigned)a.heads);
+    const unsigned id2 = a.div_nqb.div(id1);
+    const int qb = (int)(id1 - id2 * (unsigned)a.nqb);
+    const unsigned id3 = a.div_nwin.div(id2);
+    const int win = (int)(id2 - id3 * (unsigned)a.n_windows);
+    const int b = (int)id3;
+    const WindowRect wr = window_rect<MULTI>(a, win);
+    const int n = wr.rows * wr.cols;
+    const int q0 = NMAX * qb;
+    if (q0 >= n) return;
+    const int nq = min(NMAX, n - q0);
+    const int nkb = (n + NMAX - 1) / NMAX;
+    const long long q_base = (long long)b * a.q_batch_stride + wr.tok0 * a.tok_stride + head * D;
+    const __amdgpu_buffer_rsrc_t dqr =
+        make_rsrc(static_cast<uint16_t*>(ba.dq) + q_base, ((long long)a.B * a.q_batch_stride - q_base) * 2);
+    WindowAddr addr;
+    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
+    const long long blk = (long long)a.nqb * kQueryBlock * D;
+    const float* src0 = ba.ws_dq + ((((long long)b * a.heads + head) * a.n_windows + win) * a.nqb) * blk;
+    const int part = threadIdx.x & 7;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int r = (threadIdx.x >> 3) + 64 * u;
+        if (r >= nq) break;
+        const float* src = src0 + (long long)(q0 + r) * D + 8 * part;
+        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+        for (int k = 0; k < nkb; ++k) {
+            const float4 y0 = *reinterpret_cast<const float4*>(src + k * blk);
+            const float4 y1 = *reinterpret_cast<const float4*>(src + k * blk + 4);
+            x0.x += y0.x;
+            x0.y += y0.y;
+            x0.z += y0.z;
+            x0.w += y0.w;
+            x1.x += y1.x;
+            x1.y += y1.y;
+            x1.z += y1.z;
+            x1.w += y1.w;
+        }
+        const float c = ba.scale;
+        const bf16x8 o = {(__bf16)(x0.x * c), (__bf16)(x0.y * c), (__bf16)(x0.z * c), (__bf16)(x0.w * c),
+                          (__bf16)(x1.x * c), (__bf16)(x1.y * c), (__bf16)(x1.z * c), (__bf16)(x1.w * c)};
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), dqr, addr(q0 + r) + 16 * part, 0, 0);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream) {
@@ -479,6 +854,22 @@ hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream) {
                          : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, false, false>));
     const long long groups = (long long)a.f.B * a.f.heads * a.f.n_windows;
     return hipLaunchKernel(fn, dim3((unsigned)groups), dim3(THREADS), params, 0, stream);
+}
+
+hipError_t launch_swin_bwd_bf16_wide(const SwinBwdArgs& a, hipStream_t stream) {
+    SwinBwdArgs args = a;
+    void* params[] = {&args};
+    const bool multi = a.f.n_grids > 1, kv = a.f.pad_mode == 1;
+    const void* fn = multi ? (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<true, true>)
+                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<true, false>))
+                           : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<false, true>)
+                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<false, false>));
+    const dim3 grid((unsigned)a.f.n_groups);
+    hipError_t e = hipLaunchKernel(fn, grid, dim3(THREADS), params, 0, stream);
+    if (e != hipSuccess) return e;
+    const void* red = multi ? reinterpret_cast<const void*>(&swin_bwd_dq_reduce_kernel<true>)
+                            : reinterpret_cast<const void*>(&swin_bwd_dq_reduce_kernel<false>);
+    return hipLaunchKernel(red, grid, dim3(THREADS), params, 0, stream);
 }
 
 }  // namespace fla

@@ -1,5 +1,4 @@
-// Flash Swin attention backward in fp32 arithmetic on the vector ALU, for fp32 tensors and
-// for bf16 tensors whose windows exceed the matrix-core kernel's 256 tokens, and the
+// Flash Swin attention backward, fp32 storage and arithmetic (vector ALU), and the
 // reduction of the pad token's gradient shared with the bf16 path.
 //
 // The gradients of Eq. 1 inside each window (the paper trains through Flash Swin, App. D),
@@ -25,28 +24,6 @@ constexpr int D = kHeadDim;
 constexpr int THREADS = kQueryBlock;   // one token per thread
 constexpr int CH = 64;                 // tokens per LDS chunk
 constexpr float kLog2e = 1.4426950408889634f;
-
-// Element access of the two storage types: float, or bf16 held as uint16_t (widened exactly
-// to fp32 on load, rounded to nearest even on store).
-__device__ __forceinline__ float ld1(const float* p) { return *p; }
-__device__ __forceinline__ float ld1(const uint16_t* p) { return __uint_as_float((unsigned)*p << 16); }
-__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ __forceinline__ float4 ld4(const uint16_t* p) {
-    const uint2 u = *reinterpret_cast<const uint2*>(p);
-    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
-                       __uint_as_float(u.y & 0xffff0000u));
-}
-__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
-__device__ __forceinline__ unsigned bf16_bits(float x) {
-    const __bf16 r = (__bf16)x;
-    return __builtin_bit_cast(uint16_t, r);
-}
-__device__ __forceinline__ void st4(uint16_t* p, float4 v) {
-    uint2 u;
-    u.x = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
-    u.y = bf16_bits(v.z) | (bf16_bits(v.w) << 16);
-    *reinterpret_cast<uint2*>(p) = u;
-}
 
 struct Block {
     int head, blk, win, b;
@@ -75,7 +52,6 @@ __device__ __forceinline__ long long token_index(const WindowRect& wr, int t) {
     return wr.tok0 + (long long)r * wr.W + (t - r * wr.cols);
 }
 
-template <typename T>
 __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba) {
     const SwinArgs& a = ba.f;
     __shared__ __attribute__((aligned(16))) float Kf[CH * D];
@@ -100,12 +76,12 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
 
     const long long qoff = (long long)blk.b * a.q_batch_stride + blk.head * D;
     const long long kvoff = (long long)blk.b * a.kv_batch_stride + blk.head * D;
-    const T* qg = static_cast<const T*>(a.q) + qoff;
-    const T* og = static_cast<const T*>(ba.out) + qoff;
-    const T* dog = static_cast<const T*>(ba.dout) + qoff;
-    T* dqg = static_cast<T*>(ba.dq) + qoff;
-    const T* kg = static_cast<const T*>(a.k) + kvoff;
-    const T* vg = static_cast<const T*>(a.v) + kvoff;
+    const float* qg = static_cast<const float*>(a.q) + qoff;
+    const float* og = static_cast<const float*>(ba.out) + qoff;
+    const float* dog = static_cast<const float*>(ba.dout) + qoff;
+    float* dqg = static_cast<float*>(ba.dq) + qoff;
+    const float* kg = static_cast<const float*>(a.k) + kvoff;
+    const float* vg = static_cast<const float*>(a.v) + kvoff;
     const long long lse0 = ((long long)blk.b * a.heads + blk.head) * a.L;
 
     const int tid = threadIdx.x;
@@ -116,13 +92,13 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
     float qv[D], dov[D], dq[D];
     float Dv = 0.f;
     {
-        const T* qr = qg + token_elems(a, wr, tq);
-        const T* orow = og + token_elems(a, wr, tq);
-        const T* dr = dog + token_elems(a, wr, tq);
+        const float* qr = qg + token_elems(a, wr, tq);
+        const float* orow = og + token_elems(a, wr, tq);
+        const float* dr = dog + token_elems(a, wr, tq);
         for (int i = 0; i < D; ++i) {
-            qv[i] = ld1(qr + i) * a.scale_log2;   // logits in the exp2 domain
-            dov[i] = ld1(dr + i);
-            Dv = fmaf(dov[i], ld1(orow + i), Dv);
+            qv[i] = qr[i] * a.scale_log2;   // logits in the exp2 domain
+            dov[i] = dr[i];
+            Dv = fmaf(dr[i], orow[i], Dv);
             dq[i] = 0.f;
         }
     }
@@ -136,8 +112,8 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
             float4 kx = make_float4(0.f, 0.f, 0.f, 0.f), vx = kx;
             if (key < ck) {
                 const long long off = token_elems(a, wr, kc0 + key) + part * 4;
-                kx = ld4(kg + off);
-                vx = ld4(vg + off);
+                kx = *reinterpret_cast<const float4*>(kg + off);
+                vx = *reinterpret_cast<const float4*>(vg + off);
             }
             *reinterpret_cast<float4*>(&Kf[key * D + part * 4]) = kx;
             *reinterpret_cast<float4*>(&Vf[key * D + part * 4]) = vx;
@@ -159,23 +135,23 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
     float p_pad = 0.f, ds_pad = 0.f;
     if (has_pad) {
         const long long prow = (long long)blk.b * a.kv_batch_stride + a.L * a.tok_stride + blk.head * D;
-        const T* kp = static_cast<const T*>(a.k) + prow;
-        const T* vp = static_cast<const T*>(a.v) + prow;
+        const float* kp = static_cast<const float*>(a.k) + prow;
+        const float* vp = static_cast<const float*>(a.v) + prow;
         float s = 0.f, dp = 0.f;
         for (int i = 0; i < D; ++i) {
-            s = fmaf(qv[i], ld1(kp + i), s);
-            dp = fmaf(dov[i], ld1(vp + i), dp);
+            s = fmaf(qv[i], kp[i], s);
+            dp = fmaf(dov[i], vp[i], dp);
         }
         p_pad = exp2f(s + log2f((float)n_pad) - lse2);
         ds_pad = p_pad * (dp - Dv);
-        for (int i = 0; i < D; ++i) dq[i] = fmaf(ds_pad, ld1(kp + i), dq[i]);
+        for (int i = 0; i < D; ++i) dq[i] = fmaf(ds_pad, kp[i], dq[i]);
     }
 
     if (active) {
-        T* row = dqg + token_elems(a, wr, t);
+        float* row = dqg + token_elems(a, wr, t);
         for (int i = 0; i < D; i += 4)
-            st4(row + i, make_float4(dq[i] * ba.scale, dq[i + 1] * ba.scale, dq[i + 2] * ba.scale,
-                                     dq[i + 3] * ba.scale));
+            *reinterpret_cast<float4*>(row + i) =
+                make_float4(dq[i] * ba.scale, dq[i + 1] * ba.scale, dq[i + 2] * ba.scale, dq[i + 3] * ba.scale);
     }
 
     if (has_pad) {
@@ -187,17 +163,17 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dq_kernel(SwinBwdArgs ba
         if (tid < kPadPartial) {
             const bool is_k = tid < D;
             const int ch = is_k ? tid : tid - D;
-            const T* src = is_k ? qg : dog;
+            const float* src = is_k ? qg : dog;
             const float* wgt = is_k ? Sp : Pp;
             float acc = 0.f;
-            for (int i = 0; i < nq; ++i) acc = fmaf(wgt[i], ld1(src + token_elems(a, wr, q_begin + i) + ch), acc);
+            for (int i = 0; i < nq; ++i) acc = fmaf(wgt[i], src[token_elems(a, wr, q_begin + i) + ch], acc);
             ws_entry[tid] = is_k ? acc * ba.scale : acc;
         }
     }
 }
 
 // KIND 0: dv_j = sum_i P_ij dO_i;  KIND 1: dk_j = c sum_i dS_ij q_i
-template <typename T, int KIND>
+template <int KIND>
 __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs ba) {
     const SwinArgs& a = ba.f;
     __shared__ __attribute__((aligned(16))) float Qf[CH * D];
@@ -212,12 +188,12 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
 
     const long long qoff = (long long)blk.b * a.q_batch_stride + blk.head * D;
     const long long kvoff = (long long)blk.b * a.kv_batch_stride + blk.head * D;
-    const T* qg = static_cast<const T*>(a.q) + qoff;
-    const T* og = static_cast<const T*>(ba.out) + qoff;
-    const T* dog = static_cast<const T*>(ba.dout) + qoff;
-    const T* kg = static_cast<const T*>(a.k) + kvoff;
-    const T* vg = static_cast<const T*>(a.v) + kvoff;
-    T* outg = static_cast<T*>(KIND == 0 ? ba.dv : ba.dk) + kvoff;
+    const float* qg = static_cast<const float*>(a.q) + qoff;
+    const float* og = static_cast<const float*>(ba.out) + qoff;
+    const float* dog = static_cast<const float*>(ba.dout) + qoff;
+    const float* kg = static_cast<const float*>(a.k) + kvoff;
+    const float* vg = static_cast<const float*>(a.v) + kvoff;
+    float* outg = static_cast<float*>(KIND == 0 ? ba.dv : ba.dk) + kvoff;
     const long long lse0 = ((long long)blk.b * a.heads + blk.head) * a.L;
 
     const int tid = threadIdx.x;
@@ -227,14 +203,14 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
 
     float kv[D], vv[KIND == 1 ? D : 1], acc[D];
     {
-        const T* kr = kg + token_elems(a, wr, tk);
+        const float* kr = kg + token_elems(a, wr, tk);
         for (int i = 0; i < D; ++i) {
-            kv[i] = ld1(kr + i) * a.scale_log2;
+            kv[i] = kr[i] * a.scale_log2;
             acc[i] = 0.f;
         }
         if constexpr (KIND == 1) {
-            const T* vr = vg + token_elems(a, wr, tk);
-            for (int i = 0; i < D; ++i) vv[i] = ld1(vr + i);
+            const float* vr = vg + token_elems(a, wr, tk);
+            for (int i = 0; i < D; ++i) vv[i] = vr[i];
         }
     }
 
@@ -246,8 +222,8 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
             float4 qx = make_float4(0.f, 0.f, 0.f, 0.f), gx = qx;
             if (qi < cq) {
                 const long long off = token_elems(a, wr, qc0 + qi) + part * 4;
-                qx = ld4(qg + off);
-                gx = ld4(dog + off);
+                qx = *reinterpret_cast<const float4*>(qg + off);
+                gx = *reinterpret_cast<const float4*>(dog + off);
             }
             *reinterpret_cast<float4*>(&Qf[qi * D + part * 4]) = qx;
             *reinterpret_cast<float4*>(&Gf[qi * D + part * 4]) = gx;
@@ -258,7 +234,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
                 lse2 = ba.lse[lse0 + token_index(wr, qc0 + tid)] * kLog2e;
                 if constexpr (KIND == 1) {
                     const long long off = token_elems(a, wr, qc0 + tid);
-                    for (int i = 0; i < D; ++i) dd = fmaf(ld1(dog + off + i), ld1(og + off + i), dd);
+                    for (int i = 0; i < D; ++i) dd = fmaf(dog[off + i], og[off + i], dd);
                 }
             }
             Lf[tid] = lse2;
@@ -284,9 +260,10 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_f32_dkv_kernel(SwinBwdArgs b
 
     if (active) {
         const float sc = KIND == 1 ? ba.scale : 1.f;
-        T* row = outg + token_elems(a, wr, t);
+        float* row = outg + token_elems(a, wr, t);
         for (int i = 0; i < D; i += 4)
-            st4(row + i, make_float4(acc[i] * sc, acc[i + 1] * sc, acc[i + 2] * sc, acc[i + 3] * sc));
+            *reinterpret_cast<float4*>(row + i) =
+                make_float4(acc[i] * sc, acc[i + 1] * sc, acc[i + 2] * sc, acc[i + 3] * sc);
     }
 }
 
@@ -335,22 +312,18 @@ __global__ __launch_bounds__(kRedSlices * kPadPartial) void swin_bwd_pad_reduce_
 
 }  // namespace
 
-hipError_t launch_swin_bwd_vec(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream) {
+hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream) {
     SwinBwdArgs args = a;
     void* params[] = {&args};
     const dim3 grid((unsigned)a.f.n_groups), block(THREADS);
-    const bool h = elem_bytes == 2;
-    const void* fq = h ? reinterpret_cast<const void*>(&swin_bwd_f32_dq_kernel<uint16_t>)
-                       : reinterpret_cast<const void*>(&swin_bwd_f32_dq_kernel<float>);
-    const void* fv = h ? reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<uint16_t, 0>)
-                       : reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<float, 0>);
-    const void* fk = h ? reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<uint16_t, 1>)
-                       : reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<float, 1>);
-    hipError_t e = hipLaunchKernel(fq, grid, block, params, 0, stream);
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&swin_bwd_f32_dq_kernel), grid, block,
+                                   params, 0, stream);
     if (e != hipSuccess) return e;
-    e = hipLaunchKernel(fv, grid, block, params, 0, stream);
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<0>), grid, block, params, 0,
+                        stream);
     if (e != hipSuccess) return e;
-    return hipLaunchKernel(fk, grid, block, params, 0, stream);
+    return hipLaunchKernel(reinterpret_cast<const void*>(&swin_bwd_f32_dkv_kernel<1>), grid, block, params,
+                           0, stream);
 }
 
 hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream) {

@@ -83,15 +83,18 @@ struct SwinArgs {
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
-constexpr int kBwdMaxTokens = 256;   // window tokens the bf16 backward kernel holds (window <= 16)
+constexpr int kBwdMaxTokens = 256;   // window tokens one bf16 backward workgroup holds (window <= 16)
 constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: dk then dv
 constexpr int kRopeMaxSide = 32;   // bf16 RoPE forward: window rows and columns it takes
 
 // Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
 // out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,
-// window, query block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * nqb
-// + qblk][0:64] = dk part, [64:128] = dv part.  Every block writes its entry (zero when its
-// window has no virtual slots), and the pad reduce kernel sums them.
+// window, block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * nqb
+// + blk][0:64] = dk part, [64:128] = dv part.  Every block writes its entry (zero when its
+// window has no virtual slots), and the pad reduce kernel sums them.  ws_dq (bf16 windows
+// of more than 256 tokens only) holds each key block's fp32 share of dq, unscaled:
+// ws_dq[(((b * heads + head) * n_windows + win) * nqb + kb) * nqb * 256 * 64 + t * 64 + ch]
+// for window-local query t.
 struct SwinBwdArgs {
     SwinArgs f;
     const void* out;
@@ -101,12 +104,14 @@ struct SwinBwdArgs {
     void* dk;
     void* dv;
     float* ws;
+    float* ws_dq;
     float scale;                // 1 / sqrt(head_dim)
 };
 
 hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
-// fp32 arithmetic on the vector ALU, any window size; elem_bytes 4: fp32 tensors, 2: bf16
-hipError_t launch_swin_bwd_vec(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
+// bf16, windows of more than kBwdMaxTokens tokens: key-block kernel, then the dq reduction
+hipError_t launch_swin_bwd_bf16_wide(const SwinBwdArgs& a, hipStream_t stream);
+hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
 // sums the partials of ws into row L of dk and dv (elem_bytes 2: bf16, 4: fp32)
 hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
 

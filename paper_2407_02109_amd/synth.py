@@ -83,6 +83,12 @@ WORKLOADS = {
                            pad_mode=PAD_KVTOKEN, grids=((128, 128), (32, 32)),
                            note="multi-scale (HRSAM++): the 2048^2 image's 128x128 tokens followed by "
                                 "the 512^2 anchor map's 32x32, one shared pad token"),
+    "img1024_w32": Workload("img1024_w32", 1, 12, 64, 64, 64, 32, 16, "bf16", seed=8,
+                            note="64x64 tokens, 12 heads x 64, window 32, shift 16 (windows of 256, 512 "
+                                 "and 1024 tokens): the paper's speedup shape at the wider window"),
+    "img1024_w64": Workload("img1024_w64", 1, 12, 64, 64, 64, 64, 32, "bf16", seed=9,
+                            note="64x64 tokens, 12 heads x 64, window 64, shift 32 (four 32x32 windows "
+                                 "of 1024 tokens): the paper's speedup shape at the widest window"),
     "ragged150x203": Workload("ragged150x203", 4, 12, 150, 203, 64, 16, 8, "bf16", seed=4,
                               note="non-divisible 150x203 grid, B=4, 12 heads x 64, window 16, "
                                    "shift 8, padded keys masked"),

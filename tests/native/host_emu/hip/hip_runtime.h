@@ -37,20 +37,6 @@ struct alignas(8) float2 {
 };
 inline float2 make_float2(float a, float b) { return float2{a, b}; }
 
-struct alignas(8) uint2 {
-    unsigned x, y;
-};
-inline float __uint_as_float(unsigned u) {
-    float f;
-    std::memcpy(&f, &u, 4);
-    return f;
-}
-inline unsigned __float_as_uint(float f) {
-    unsigned u;
-    std::memcpy(&u, &f, 4);
-    return u;
-}
-
 typedef int hipError_t;
 constexpr hipError_t hipSuccess = 0;
 typedef void* hipStream_t;

@@ -2,10 +2,8 @@
 // emulation, with every buffer an exact-size heap allocation (AddressSanitizer reports any
 // access outside), and writes inputs and outputs as raw float32 files for the test to compare
 // with the oracle.
-#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
-#include <cstring>
 #include <random>
 
 #include "fla_swin.h"
@@ -19,23 +17,6 @@ static float* alloc_random(size_t n, std::mt19937& g) {
     return p;
 }
 
-static uint16_t to_bf16(float x) {
-    const __bf16 r = (__bf16)x;
-    return __builtin_bit_cast(uint16_t, r);
-}
-static float to_f32(uint16_t h) {
-    const unsigned u = (unsigned)h << 16;
-    float f;
-    std::memcpy(&f, &u, 4);
-    return f;
-}
-// an exact-size bf16 copy (the input's values rounded to nearest even)
-static uint16_t* narrow(const float* p, size_t n) {
-    uint16_t* h = static_cast<uint16_t*>(std::aligned_alloc(16, ((n * 2 + 15) / 16) * 16));
-    for (size_t i = 0; i < n; ++i) h[i] = to_bf16(p[i]);
-    return h;
-}
-
 static void dump(const char* dir, const char* name, const float* p, size_t n) {
     char path[1024];
     std::snprintf(path, sizeof path, "%s/%s.f32", dir, name);
@@ -45,11 +26,10 @@ static void dump(const char* dir, const char* name, const float* p, size_t n) {
 }
 
 int main(int argc, char** argv) {
-    if (argc != 9 && argc != 10) {
-        std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir [bf16]\n");
+    if (argc != 9) {
+        std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
         return 2;
     }
-    const bool bf16 = argc == 10;   // backward through the bf16 entry point (windows over 256 tokens)
     const int B = std::atoi(argv[1]), heads = std::atoi(argv[2]), H = std::atoi(argv[3]), W = std::atoi(argv[4]);
     const int k = std::atoi(argv[5]), s = std::atoi(argv[6]), pm = std::atoi(argv[7]);
     const char* dir = argv[8];
@@ -64,11 +44,6 @@ int main(int argc, char** argv) {
     float* dq = alloc_random(B * L * tok, g);
     float* dk = alloc_random(B * rows * tok, g);
     float* dv = alloc_random(B * rows * tok, g);
-    if (bf16)   // inputs that bf16 holds exactly, so that both entry points see the same values
-        for (float* p : {q, kk, v, dout}) {
-            const size_t n = p == kk || p == v ? B * rows * tok : B * L * tok;
-            for (size_t i = 0; i < n; ++i) p[i] = to_f32(to_bf16(p[i]));
-        }
     const int hw[2] = {H, W};
     size_t nws = 0;
     if (fla_swin_attn_bwd_workspace(B, heads, 1, hw, k, s, pm, &nws) != 0) return 1;
@@ -80,20 +55,7 @@ int main(int argc, char** argv) {
         return 1;
     }
     emu_kernel_args = 1;
-    if (bf16) {
-        // out rounded to bf16 as a bf16 training forward would store it; the gradients come
-        // back as bf16 and are widened for the dump
-        const size_t nq = B * L * tok, nk = B * rows * tok;
-        for (size_t i = 0; i < nq; ++i) out[i] = to_f32(to_bf16(out[i]));
-        uint16_t *hq = narrow(q, nq), *hk = narrow(kk, nk), *hv = narrow(v, nk), *ho = narrow(out, nq),
-                 *hd = narrow(dout, nq), *gq = narrow(dq, nq), *gk = narrow(dk, nk), *gv = narrow(dv, nk);
-        rc = fla_swin_attn_bwd(hq, hk, hv, ho, hd, lse, gq, gk, gv, ws, nws, B, heads, H, W, 64, k, s, pm, nullptr);
-        for (size_t i = 0; i < nq; ++i) dq[i] = to_f32(gq[i]);
-        for (size_t i = 0; i < nk; ++i) dk[i] = to_f32(gk[i]), dv[i] = to_f32(gv[i]);
-    } else {
-        rc = fla_swin_attn_bwd_f32(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, 64, k, s, pm,
-                                   nullptr);
-    }
+    rc = fla_swin_attn_bwd_f32(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, 64, k, s, pm, nullptr);
     if (rc != 0) {
         std::fprintf(stderr, "backward: %s\n", fla_status_string(rc));
         return 1;

@@ -342,6 +342,22 @@ def test_bwd_mask_mode_needs_no_workspace(lib):
     codes = _header_enum("FLA")
     st = _call_bwd(ws=0, ws_bytes=0)
     assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"])
+    # windows of more than 256 tokens: the bf16 kernels keep each key block's dq share there
+    # (the fp32 kernels do not)
+    assert _call_bwd(ws=0, ws_bytes=0, window=17, shift=0) == codes["FLA_ERR_WORKSPACE"]
+    assert _call_bwd(ws_bytes=16, window=17, shift=0) == codes["FLA_ERR_WORKSPACE"]
+    st = _call_bwd(f32=True, ws=0, ws_bytes=0, window=17, shift=0)
+    assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"])
+
+
+def test_bwd_workspace_size_examples(lib):
+    # 64 x 64 grid, 12 heads: window 16 shift 8 in KV-token mode: 25 windows x 12 heads of one
+    # 512-byte pad partial; window 32 shift 16 in mask mode: 9 windows (nqb = 4 query blocks of
+    # 256) x 12 heads x 4 key blocks x 4 x 256 queries x 64 channels x 4 bytes
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 16, 8, 1) == 25 * 12 * 512
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 16, 8, 0) == 0
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 0) == 9 * 12 * 4 * 4 * 256 * 64 * 4
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 1) == 9 * 12 * 4 * (512 + 4 * 256 * 64 * 4)
 
 
 @pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
@@ -364,9 +380,12 @@ def test_bwd_workspace_size(lib, grids, k, s, pm):
     B, heads = 2, 3
     n_win = sum(len(O.window_sizes(h, w, k, s)) for h, w in grids)
     nqb = max(-(-max(sz for h, w in grids for sz in O.window_sizes(h, w, k, s)) // 256), 1)
-    want = B * heads * n_win * nqb * 128 * 4 if pm == 1 else 0
+    # pad partials (KV-token mode), then, for windows of more than 256 tokens, every key
+    # block's fp32 dq share of its window's queries
+    shares = B * heads * n_win * nqb * nqb * 256 * 64 * 4 if nqb > 1 else 0
+    want = (B * heads * n_win * nqb * 128 * 4 if pm == 1 else 0) + shares
     assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, pm) == want
-    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, 0) == 0
+    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, 0) == shares
 
 
 def test_bwd_workspace_errors(lib):

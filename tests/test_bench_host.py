@@ -61,3 +61,14 @@ def test_summary_scales_counters_by_the_copy(tmp_path, leg):
     assert rec["kernel_hash"] == bench.kernel_hash(leg)
     md = (out / ("%s_synthetic.md" % kname)).read_text()
     assert "3 dispatches" in md and "rocprofv3 ..." in md
+
+
+def test_roofline_follows_arithmetic_intensity():
+    # 120 FLOP/B (full 16 x 16 windows): below the 312.5 FLOP/B ridge, HBM-bound
+    r = bench.roofline(48e9, 400e6, 100.0, 123)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["traffic"] == 123
+    assert r["achieved"] == pytest.approx(4000.0) and r["frac"] == pytest.approx(0.5)
+    # 512 FLOP/B (1024-token windows): matrix-core bound
+    r = bench.roofline(512e9, 1e9, 1000.0, None)
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s" and r["achieved"] == pytest.approx(512.0)
+    assert r["frac"] == pytest.approx(512.0 / 2500.0)

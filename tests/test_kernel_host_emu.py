@@ -5,8 +5,7 @@ geometry, workgroup decode, window rectangles, workspace layout, pad-token reduc
 compiled as host C++ against a small stand-in for the HIP runtime (tests/native/host_emu: a
 launch runs each block's work items as host threads with a barrier for __syncthreads), with
 AddressSanitizer and exact-size buffers.  A run must stay inside every buffer and reproduce
-the fp64 oracle's output, log-sum-exp and gradients to fp32 accuracy; the bf16 backward of
-windows over 256 tokens, which runs the same kernels on bf16 tensors, to bf16 accuracy.  No GPU is involved;
+the fp64 oracle's output, log-sum-exp and gradients to fp32 accuracy.  No GPU is involved;
 the bf16 kernels (matrix-core builtins) are not part of this build."""
 import os
 import shutil
@@ -63,19 +62,12 @@ CASES = [  # B, heads, H, W, window, shift, pad_mode
 ]
 
 
-BF16_CASES = [  # windows of more than 256 tokens: the bf16 backward runs the fp32-arithmetic kernels
-    (1, 2, 24, 40, 32, 16, 0),
-    (1, 2, 40, 37, 32, 8, 1),
-]
-
-
-@pytest.mark.parametrize("case,bf16", [(c, False) for c in CASES] + [(c, True) for c in BF16_CASES],
-                         ids=lambda c: "x".join(map(str, c)) if isinstance(c, tuple) else ("bf16" if c else "f32"))
-def test_fp32_kernels_on_the_host(emu_binary, tmp_path, case, bf16):
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
+def test_fp32_kernels_on_the_host(emu_binary, tmp_path, case):
     B, heads, H, W, k, s, pm = case
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
-    r = subprocess.run([emu_binary, *map(str, case), str(tmp_path)] + (["bf16"] if bf16 else []),
-                       capture_output=True, text=True, timeout=900, env=env)
+    r = subprocess.run([emu_binary, *map(str, case), str(tmp_path)], capture_output=True, text=True, timeout=900,
+                       env=env)
     assert r.returncode == 0 and "ok" in r.stdout, r.stderr[-4000:]
     L = H * W
     rows = L + (1 if pm else 0)
@@ -89,16 +81,9 @@ def test_fp32_kernels_on_the_host(emu_binary, tmp_path, case, bf16):
     lse = np.fromfile(str(tmp_path / "lse.f32"), dtype=np.float32).astype(np.float64).reshape(B, heads, L)
     ref_out = O.swin_attention_textbook(q, kk, v, H, W, k, s, pm)
     ref_lse = O.swin_attention_lse(q, kk, v, H, W, k, s, pm)
-    if bf16:   # out as the bf16 backward received it: rounded to bf16
-        assert np.abs(out - ref_out).max() <= 2e-2 and np.abs(out - ref_out).mean() <= 2e-3
-    else:
-        assert np.abs(out - ref_out).max() <= 1e-5
+    assert np.abs(out - ref_out).max() <= 1e-5
     assert np.abs(lse - ref_lse).max() <= 1e-5
     refs = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
     for name, got, ref in zip(("dq", "dk", "dv"), (ld("dq", L), ld("dk", rows), ld("dv", rows)), refs):
         m = max(1.0, np.abs(ref).max())
-        err = np.abs(got - ref)
-        if bf16:   # one bf16 rounding of the stored out and of each gradient
-            assert err.max() <= 2e-2 * m and err.mean() <= 2e-3 * m, name
-        else:
-            assert err.max() <= 2e-5 * m, name
+        assert np.abs(got - ref).max() <= 2e-5 * m, name

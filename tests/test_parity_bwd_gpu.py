@@ -153,6 +153,23 @@ def test_backward_wide_windows(shape, dtype, pm):
         _check_grad("dv_pad", dv[:, -1], gv[:, -1], f32, bulk=False)
 
 
+@pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
+def test_bf16_backward_wide_windows_multi_scale(pm):
+    """A grid list whose first grid has windows of more than 256 tokens and whose second has
+    small ones: one launch of the key-block kernel and the dq reduction over both."""
+    grids = ((40, 37), (9, 9))
+    wl = _wl(1, 2, 40, 37, 20, 10, "bf16", pm, 31 + pm, grids=grids)
+    _say("bwd wide multi-scale %s pad_mode=%d" % (grids, pm))
+    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
+    dout = synth.make_grad(wl).cuda()
+    _, lse, dq, dk, dv = _train(wl, q, kk, v, dout)
+    qn, kn, vn, gn = (synth.to_f64_numpy(t) for t in (q, kk, v, dout))
+    assert np.abs(synth.to_f64_numpy(lse) - O.swin_attention_ms_lse(qn, kn, vn, grids, 20, 10, pm)).max() <= LSE_BF16
+    gq, gk, gv = O.swin_attention_ms_bwd(qn, kn, vn, gn, grids, 20, 10, pm)
+    for name, got, ref in (("dq", dq, gq), ("dk", dk, gk), ("dv", dv, gv)):
+        _check_grad(name, got, ref, False)
+
+
 def test_bf16_rope_backward_rejects_windows_over_256_tokens():
     B, heads, H, W = 1, 1, 40, 24
     wl = _wl(B, heads, H, W, 20, 10, "bf16", 0, 1)
@@ -188,17 +205,22 @@ def test_multiscale_backward(dtype, pm):
         _check_grad(name, got, r, dtype == "f32")
 
 
-def test_workspace_contents_are_ignored():
-    wl = _wl(1, 2, 37, 29, 16, 8, "bf16", 1, 5)
+@pytest.mark.parametrize("k,s,pm", [(16, 8, 1), (20, 10, 1), (20, 10, 0)])
+def test_workspace_contents_are_ignored(k, s, pm):
+    """Every workspace element a call reads was written by that call (pad partials; dq shares
+    of windows over 256 tokens), and the result is the same bits run to run."""
+    wl = _wl(1, 2, 37, 29, k, s, "bf16", pm, 5)
+    _say("bwd workspace k=%d s=%d pad_mode=%d" % (k, s, pm))
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
     dout = synth.make_grad(wl).cuda()
     first = _train(wl, q, kk, v, dout)   # workspace starts as NaN inside _train
     B, L, heads, d = q.shape
-    nbytes = fb.fla_swin_attn_bwd_workspace(B, heads, wl.grid_list, 16, 8, 1)
+    nbytes = fb.fla_swin_attn_bwd_workspace(B, heads, wl.grid_list, k, s, pm)
+    assert nbytes > 0
     ws = torch.full((nbytes // 4,), 1e30, dtype=torch.float32, device="cuda")
     dq, dk, dv = (torch.empty_like(t) for t in (q, kk, v))
     fb.fla_swin_attn_bwd(q, kk, v, first[0], dout, first[1], dq, dk, dv, ws, nbytes, B, heads, wl.H, wl.W,
-                         d, 16, 8, 1)
+                         d, k, s, pm)
     torch.cuda.synchronize()
     for a, b in zip((dq, dk, dv), first[2:]):
         assert torch.equal(a, b)
