@@ -19,6 +19,7 @@ import collections
 import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -113,6 +114,10 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
     grids = collections.Counter(r["Grid_Size_X"] for r in trace)
     main_grid = grids.most_common(1)[0][0] if grids else None
     durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace if r["Grid_Size_X"] == main_grid]
+    # the kernel those launches ran (swin_bwd_bf16_wide_kernel for windows of more than 256 tokens)
+    found = sorted({m.group(1) for r in trace if r["Grid_Size_X"] == main_grid
+                    for m in [re.search(r"(%s\w*_kernel)" % kname, r["Kernel_Name"])] if m})
+    title = ", ".join(found) or kname + "_kernel"
     stats = rows("trace/**/*kernel_stats.csv")
     counters = {}
     copies = {}
@@ -135,7 +140,7 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
     traffic = None
     if counters["FETCH_SIZE"] and counters["WRITE_SIZE"] and fetch_scale and write_scale:
         traffic = (counters["FETCH_SIZE"] * 1024 * fetch_scale + counters["WRITE_SIZE"] * 1024 * write_scale)
-    lines = ["# rocprofv3 summary: %s_kernel, workload %s" % (kname, workload), "",
+    lines = ["# rocprofv3 summary: %s, workload %s" % (title, workload), "",
              "Command (run from the repository root on the GPU host):", "", "```", command, "```", ""]
     if durs:
         lines += ["Kernel trace: %d dispatches, duration avg %.2f us, median %.2f us, min %.2f us, max %.2f us"
@@ -156,7 +161,7 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
         f.write("\n".join(lines))
     if traffic is not None:
         with open(traffic_path(leg, workload, out_dir), "w") as f:
-            json.dump({"workload": workload, "kernel": kname, "kernel_hash": kernel_hash(leg),
+            json.dump({"workload": workload, "kernel": title, "kernel_hash": kernel_hash(leg),
                        "bytes_per_launch": int(traffic),
                        "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],
                        "fetch_scale": fetch_scale, "write_scale": write_scale,
