@@ -245,9 +245,17 @@ def _window_grads(q, kk, v, dout, H, W, rect, k, pm, L):
     return idx, g
 
 
-@pytest.mark.parametrize("name", ["img4096", "img4096_kv"])
+FULL_SIZE = {   # the 4096^2 layer; with window 32 every window but the border ones has 1024 tokens
+    "img4096": synth.WORKLOADS["img4096"],
+    "img4096_kv": synth.WORKLOADS["img4096_kv"],
+    "img4096_w32": synth.WORKLOADS["img4096"].with_(name="img4096_w32", window=32, shift=16),
+    "img4096_kv_w32": synth.WORKLOADS["img4096_kv"].with_(name="img4096_kv_w32", window=32, shift=16),
+}
+
+
+@pytest.mark.parametrize("name", list(FULL_SIZE))
 def test_full_size_sampled_windows(name):
-    wl = synth.WORKLOADS[name]
+    wl = FULL_SIZE[name]
     _say("bwd full size %s" % name)
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
     dout = synth.make_grad(wl).cuda()
