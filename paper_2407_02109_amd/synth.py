@@ -89,6 +89,9 @@ WORKLOADS = {
     "img1024_w64": Workload("img1024_w64", 1, 12, 64, 64, 64, 64, 32, "bf16", seed=9,
                             note="64x64 tokens, 12 heads x 64, window 64, shift 32 (four 32x32 windows "
                                  "of 1024 tokens): the paper's speedup shape at the widest window"),
+    "img4096_w32": Workload("img4096_w32", 1, 12, 256, 256, 64, 32, 16, "bf16", seed=10,
+                            note="256x256 tokens, 12 heads x 64, window 32, shift 16 (1024-token windows "
+                                 "inside, 512 and 256 on the border)"),
     "ragged150x203": Workload("ragged150x203", 4, 12, 150, 203, 64, 16, 8, "bf16", seed=4,
                               note="non-divisible 150x203 grid, B=4, 12 heads x 64, window 16, "
                                    "shift 8, padded keys masked"),
