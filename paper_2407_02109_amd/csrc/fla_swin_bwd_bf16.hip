@@ -102,6 +102,94 @@ __device__ __forceinline__ float sum8(float x) {
     return x;
 }
 
+// One step of a wave: the query tile whose rows start at q0 (Q, dO rows, -D and LSE*log2(e)
+// in LDS) against the wave's 32 keys (kreg, vreg, kt in registers).  dK^T and dV^T add up in
+// registers; the tile's fp32 dQ^T accumulator in LDS (acc, lane-major, 8 float4 per lane)
+// is read (read_acc; else taken as zero), advanced by this step's product and written back.
+__device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dOs, const float* Ds, const float* Ls,
+                                          float4* acc, uint16_t* dst, const bf16x8 (&kreg)[4],
+                                          const bf16x8 (&vreg)[4], const bf16x8 (&kt)[2][2],
+                                          const floatx16& s_init, floatx16 (&dkT)[2], floatx16 (&dvT)[2], int q0,
+                                          bool read_acc, float c2, int lane) {
+    const int li = lane & 31, h = lane >> 5;
+    // the tile's dQ^T accumulator (written by earlier steps) becomes the C operand of
+    // this step's dQ^T product; fetched first so that the read is long done by then
+    floatx16 dq[2];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const float4 y = read_acc ? acc[g * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const int dh = g >> 2, i = g & 3;
+        dq[dh][4 * i] = y.x;
+        dq[dh][4 * i + 1] = y.y;
+        dq[dh][4 * i + 2] = y.z;
+        dq[dh][4 * i + 3] = y.w;
+    }
+    // dP - D in one go: the MFMA's C operand holds -D of each entry's query
+    floatx16 sacc = s_init, pacc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
+        pacc[4 * i] = d4.x;
+        pacc[4 * i + 1] = d4.y;
+        pacc[4 * i + 2] = d4.z;
+        pacc[4 * i + 3] = d4.w;
+    }
+    const uint16_t* qrow = Qs + (q0 + li) * RS + 8 * h;
+    const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s),
+                                                      kreg[s], sacc, 0, 0, 0);
+        pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s),
+                                                      vreg[s], pacc, 0, 0, 0);
+    }
+    // entry r: query q0 + 8 (r / 4) + 4 h + r % 4, the wave's key li
+    bf16x8 pb[2], sb[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float4 l4 = *reinterpret_cast<const float4*>(Ls + q0 + 8 * i + 4 * h);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 4 * i + j;
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
+            const float ds = p * pacc[r];
+            pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
+            sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
+        }
+    }
+    // dV^T += dO^T P, dK^T += Q^T dS
+#pragma unroll
+    for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh) {
+            const bf16x8 ga = tr_operand(dOs, RS, q0 + 16 * sg, 32 * dh, lane);
+            const bf16x8 qa = tr_operand(Qs, RS, q0 + 16 * sg, 32 * dh, lane);
+            dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
+            dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
+        }
+    // dS^T -> scratch (row = key li, 4 consecutive queries per write)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
+            bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
+                   sb[i >> 1][4 * (i & 1) + 3]};
+    asm volatile("" ::: "memory");   // the scratch reads below follow these writes
+    // dQ^T += K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+        const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh)
+            dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
+    }
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        const int dh = g >> 2, i = g & 3;
+        acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
+    }
+}
+
 template <bool MULTI, bool KVPAD, bool ROPE>
 __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) {
     const SwinArgs& a = ba.f;
@@ -299,84 +387,8 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
     for (int t = 0; t < nt; ++t) {
         if (wave < nt) {
             const int T = wave + t < nt ? wave + t : wave + t - nt;
-            const int q0 = TL * T;
-            // the dQ^T accumulator of tile T (written by earlier steps) becomes the C operand of
-            // this step's dQ^T product; fetched first so that the read is long done by then
-            float4* acc = DQ + T * 8 * 64 + lane;
-            floatx16 dq[2];
-#pragma unroll
-            for (int g = 0; g < 8; ++g) {
-                const float4 y = t > 0 ? acc[g * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-                const int dh = g >> 2, i = g & 3;
-                dq[dh][4 * i] = y.x;
-                dq[dh][4 * i + 1] = y.y;
-                dq[dh][4 * i + 2] = y.z;
-                dq[dh][4 * i + 3] = y.w;
-            }
-            // dP - D in one go: the MFMA's C operand holds -D of each entry's query
-            floatx16 sacc = s_init, pacc;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
-                pacc[4 * i] = d4.x;
-                pacc[4 * i + 1] = d4.y;
-                pacc[4 * i + 2] = d4.z;
-                pacc[4 * i + 3] = d4.w;
-            }
-            const uint16_t* qrow = Qs + (q0 + li) * RS + 8 * h;
-            const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s),
-                                                              kreg[s], sacc, 0, 0, 0);
-                pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s),
-                                                              vreg[s], pacc, 0, 0, 0);
-            }
-            // entry r: query q0 + 8 (r / 4) + 4 h + r % 4, key TL * wave + li
-            bf16x8 pb[2], sb[2];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float4 l4 = *reinterpret_cast<const float4*>(Ls + q0 + 8 * i + 4 * h);
-                const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int r = 4 * i + j;
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
-                    const float ds = p * pacc[r];
-                    pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
-                    sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
-                }
-            }
-            // dV^T += dO^T P, dK^T += Q^T dS
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                for (int dh = 0; dh < 2; ++dh) {
-                    const bf16x8 ga = tr_operand(dOs, RS, q0 + 16 * sg, 32 * dh, lane);
-                    const bf16x8 qa = tr_operand(Qs, RS, q0 + 16 * sg, 32 * dh, lane);
-                    dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
-                    dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
-                }
-            // dS^T -> scratch (row = key li, 4 consecutive queries per write)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
-                    bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
-                           sb[i >> 1][4 * (i & 1) + 3]};
-            asm volatile("" ::: "memory");   // the scratch reads below follow these writes
-            // dQ^T += K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
-#pragma unroll
-            for (int s2 = 0; s2 < 2; ++s2) {
-                const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
-#pragma unroll
-                for (int dh = 0; dh < 2; ++dh)
-                    dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
-            }
-#pragma unroll
-            for (int g = 0; g < 8; ++g) {
-                const int dh = g >> 2, i = g & 3;
-                acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
-            }
+            wave_step(Qs, dOs, Ds, Ls, DQ + T * 8 * 64 + lane, dst, kreg, vreg, kt, s_init, dkT, dvT, TL * T, t > 0,
+                      c2, lane);
         }
         __syncthreads();
     }
@@ -582,8 +594,10 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs
     floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
     uint16_t* dst = DST + wave * TL * SS;
     const float c2 = a.scale_log2;
-    // C operand of S: 0, or -inf past the block's last key (one register, spread per step)
-    const float s0 = key_ok ? 0.f : -INFINITY;
+    // C operand of S = Q K^T: 0, or -inf for a key past the block's last (its P is then 0)
+    floatx16 s_init;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s_init[r] = key_ok ? 0.f : -INFINITY;
     float* wsq = ba.ws_dq + e * ((long long)a.nqb * kQueryBlock * D);   // [query of the window][64]
 
     const int nqc = (n + NMAX - 1) / NMAX;
@@ -640,81 +654,9 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs
         const int M = nqt > nkt ? nqt : nkt;
         for (int t = 0; t < M; ++t) {
             const int T = wave + t < M ? wave + t : wave + t - M;
-            if (wave < nkt && T < nqt) {
-                const int q0 = TL * T;
-                float4* acc = DQ + T * 8 * 64 + lane;
-                floatx16 dq[2];
-#pragma unroll
-                for (int g = 0; g < 8; ++g) {
-                    const float4 y = acc[g * 64];
-                    const int dh = g >> 2, i = g & 3;
-                    dq[dh][4 * i] = y.x;
-                    dq[dh][4 * i + 1] = y.y;
-                    dq[dh][4 * i + 2] = y.z;
-                    dq[dh][4 * i + 3] = y.w;
-                }
-                floatx16 sacc, pacc;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) sacc[r] = s0;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
-                    pacc[4 * i] = d4.x;
-                    pacc[4 * i + 1] = d4.y;
-                    pacc[4 * i + 2] = d4.z;
-                    pacc[4 * i + 3] = d4.w;
-                }
-                const uint16_t* qrow = Qs + (q0 + li) * RS + 8 * h;
-                const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s),
-                                                                  kreg[s], sacc, 0, 0, 0);
-                    pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s),
-                                                                  vreg[s], pacc, 0, 0, 0);
-                }
-                bf16x8 pb[2], sb[2];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float4 l4 = *reinterpret_cast<const float4*>(Ls + q0 + 8 * i + 4 * h);
-                    const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int r = 4 * i + j;
-                        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
-                        const float ds = p * pacc[r];
-                        pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
-                        sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
-                    }
-                }
-#pragma unroll
-                for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                    for (int dh = 0; dh < 2; ++dh) {
-                        const bf16x8 ga = tr_operand(dOs, RS, q0 + 16 * sg, 32 * dh, lane);
-                        const bf16x8 qa = tr_operand(Qs, RS, q0 + 16 * sg, 32 * dh, lane);
-                        dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
-                        dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
-                    }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
-                        bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
-                               sb[i >> 1][4 * (i & 1) + 3]};
-                asm volatile("" ::: "memory");
-#pragma unroll
-                for (int s2 = 0; s2 < 2; ++s2) {
-                    const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
-#pragma unroll
-                    for (int dh = 0; dh < 2; ++dh)
-                        dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
-                }
-#pragma unroll
-                for (int g = 0; g < 8; ++g) {
-                    const int dh = g >> 2, i = g & 3;
-                    acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
-                }
-            }
+            if (wave < nkt && T < nqt)
+                wave_step(Qs, dOs, Ds, Ls, DQ + T * 8 * 64 + lane, dst, kreg, vreg, kt, s_init, dkT, dvT, TL * T,
+                          true, c2, lane);
             __syncthreads();
         }
 
