@@ -30,6 +30,8 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+SIMDS = 256 * 4               # MI355X: 256 compute units of 4 SIMDs
+XCDS = 8                      # accelerator complex dies; rocprofv3 sums GRBM_GUI_ACTIVE over them
 # the kernel each leg's roofline is about, and the sources its hash covers
 KERNELS = {
     "fwd": ("swin_fwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
@@ -134,6 +136,24 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
                 per_copy[key] = per_copy.get(key, 0.0) + float(r["Counter_Value"])
         counters[name] = st.median(per_dispatch.values()) if per_dispatch else None
         copies[name] = st.median(per_copy.values()) if per_copy else None
+    # optional matrix-core pass: SQ_INSTS_VALU_MFMA_MOPS_BF16 (units of 512 FLOP) and
+    # SQ_VALU_MFMA_BUSY_CYCLES summed over the rows of a dispatch, GRBM_GUI_ACTIVE its max
+    # (the reported value is the sum over the XCDs: divided by XCDS it is the kernel's cycles)
+    mfma = {}
+    mrows = [r for r in rows("mfma/**/*counter_collection.csv") if kname in r["Kernel_Name"]]
+    mgrid = collections.Counter(r["Grid_Size"] for r in mrows).most_common(1)[0][0] if mrows else None
+    for r in mrows:
+        if r["Grid_Size"] != mgrid:   # the workload's own launches only
+            continue
+        d = mfma.setdefault(r["Dispatch_Id"], {})
+        name, val = r["Counter_Name"], float(r["Counter_Value"])
+        d[name] = max(d.get(name, 0.0), val) if name == "GRBM_GUI_ACTIVE" else d.get(name, 0.0) + val
+    mfma_flop = mfma_busy = None
+    full = [d for d in mfma.values()
+            if {"SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"} <= set(d)]
+    if full:
+        mfma_flop = st.median(512.0 * d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] for d in full)
+        mfma_busy = st.median(d["SQ_VALU_MFMA_BUSY_CYCLES"] / (d["GRBM_GUI_ACTIVE"] / XCDS * SIMDS) for d in full)
     copy_bytes = 512 << 20
     fetch_scale = copy_bytes / (copies["FETCH_SIZE"] * 1024) if copies["FETCH_SIZE"] else None
     write_scale = copy_bytes / (copies["WRITE_SIZE"] * 1024) if copies["WRITE_SIZE"] else None
@@ -156,6 +176,12 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
               "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (fetch_scale, write_scale),
               "Traffic per launch (scaled): %s bytes" % (None if traffic is None else int(traffic)),
               "Kernel source hash: %s" % kernel_hash(leg), ""]
+    if mfma_flop is not None:
+        lines[-1:-1] = ["Matrix cores (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, median per dispatch): %.4g FLOP per launch%s"
+                        % (mfma_flop, ", %.1f TFLOP/s over the average duration" % (mfma_flop / st.mean(durs) / 1e3)
+                           if durs else ""),
+                        "MFMA busy (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs), median, "
+                        "kernels serialised by the counter pass): %.3f" % (XCDS, SIMDS, mfma_busy)]
     os.makedirs(out_dir, exist_ok=True)
     with open(os.path.join(out_dir, "%s_%s.md" % (kname, workload)), "w") as f:
         f.write("\n".join(lines))
@@ -165,6 +191,7 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
                        "bytes_per_launch": int(traffic),
                        "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],
                        "fetch_scale": fetch_scale, "write_scale": write_scale,
+                       "mfma_flop_per_launch": mfma_flop, "mfma_busy": mfma_busy,
                        "avg_duration_us": st.mean(durs) / 1e3 if durs else None}, f, indent=1)
     print("\n".join(lines))
 

@@ -52,6 +52,17 @@ def test_summary_scales_counters_by_the_copy(tmp_path, leg):
     _write(str(prof / "write_size" / "run_counter_collection.csv"), hdr,
            [[7, kname, 887808, "WRITE_SIZE", 2000.0],
             [9, "__amd_rocclr_copyBuffer", 1 << 20, "WRITE_SIZE", 524288.0]])
+    # matrix-core pass: MOPS and busy cycles summed over two rows, GRBM_GUI_ACTIVE their max
+    _write(str(prof / "mfma" / "run_counter_collection.csv"), hdr,
+           [[7, kname, 887808, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 1000.0],
+            [7, kname, 887808, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 3000.0],
+            [7, kname, 887808, "SQ_VALU_MFMA_BUSY_CYCLES", 204800.0],
+            [7, kname, 887808, "SQ_VALU_MFMA_BUSY_CYCLES", 204800.0],
+            [7, kname, 887808, "GRBM_GUI_ACTIVE", 1600.0], [7, kname, 887808, "GRBM_GUI_ACTIVE", 2000.0],
+            [8, kname, 887808, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 4000.0],
+            [8, kname, 887808, "SQ_VALU_MFMA_BUSY_CYCLES", 409600.0], [8, kname, 887808, "GRBM_GUI_ACTIVE", 2000.0],
+            [11, kname, 512, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 8.0],   # a one-token launch: left out
+            [11, kname, 512, "SQ_VALU_MFMA_BUSY_CYCLES", 4.0], [11, kname, 512, "GRBM_GUI_ACTIVE", 9000.0]])
     out = tmp_path / "out"
     bench.summarize(str(prof), "synthetic", "rocprofv3 ...", leg, out_dir=str(out))
     rec = json.loads((out / os.path.basename(bench.traffic_path(leg, "synthetic"))).read_text())
@@ -59,6 +70,8 @@ def test_summary_scales_counters_by_the_copy(tmp_path, leg):
     assert rec["bytes_per_launch"] == int(1500 * 1024 * 2.0 + 2000 * 1024)
     assert rec["avg_duration_us"] == pytest.approx(12.0)   # the tiny launch is not averaged in
     assert rec["kernel_hash"] == bench.kernel_hash(leg)
+    assert rec["mfma_flop_per_launch"] == pytest.approx(4000 * 512)
+    assert rec["mfma_busy"] == pytest.approx(409600 / (2000 / 8 * 1024))
     md = (out / ("%s_synthetic.md" % kname)).read_text()
     assert "3 dispatches" in md and "rocprofv3 ..." in md
 
