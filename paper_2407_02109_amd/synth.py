@@ -118,8 +118,10 @@ def make_inputs(wl: Workload, device: str | torch.device = "cpu"):
         n_rows = wl.B * wl.L * wl.heads
         n_hot = int(round(wl.stress_keys * n_rows))
         hot = torch.randperm(n_rows, generator=g)[:n_hot]
-        kv = k[:, : wl.L].reshape(n_rows, wl.head_dim)   # view over the real key rows
-        kv[hot] *= 8.0
+        # hot indexes the real key rows in (b, token, head) order; scaled in place through
+        # explicit indices, since k[:, :L] is not contiguous when k carries a pad row
+        b, rem = hot // (wl.L * wl.heads), hot % (wl.L * wl.heads)
+        k[b, rem // wl.heads, rem % wl.heads] *= 8.0
     dt = wl.torch_dtype
     out = []
     for t in (q, k, v):

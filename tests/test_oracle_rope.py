@@ -4,12 +4,17 @@ Pins: hand-derived rotations (tests/golden/rope_small.txt); the same rotation wr
 complex multiplication of channel pairs with positions and frequencies computed here; norm
 preservation per channel pair; scale 0 reduces to the plain textbook attention; and the
 property RoPE exists for -- attention logits depend only on relative positions, so shifting
-every coordinate by a constant leaves the MASK-mode output unchanged."""
+every coordinate by a constant leaves the MASK-mode output unchanged.  The sampled-query form
+and the log-sum-exp are pinned against the whole-grid form and against facts computed here from
+this file's own complex-form rotation: the one-hot readout (values e_j make out[i, j] the
+attention probability, so LSE_i = z_ij + log w_j - log P_ij) and, in the global case, scipy's
+logsumexp (Sec. 3.1 RoPE; Eq. 1)."""
 import math
 import os
 
 import numpy as np
 import pytest
+import scipy.special
 
 import oracle.rope as R
 from oracle import swin_oracle as SO
@@ -116,8 +121,75 @@ def pin_rope_bwd_fd(M):
         assert lse.shape == (1, 2, L) and np.isfinite(lse).all()
 
 
+def _rotate_here(x, H, W, theta, scale):
+    """RoPE written independently of the oracle: each adjacent channel pair of the first (second)
+    half of a head is a complex number turned by scale * row (column) * theta^(-2j / (d/2));
+    rows past H * W (the pad token) stay as they are."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    freqs = np.array([theta ** (-(2.0 * j) / half) for j in range(half // 2)])
+    out = x.copy()
+    for t in range(H * W):
+        y, xx = divmod(t, W)
+        ang = np.concatenate([scale * y * freqs, scale * xx * freqs])
+        z = (x[:, t, :, 0::2] + 1j * x[:, t, :, 1::2]) * np.exp(1j * ang)
+        out[:, t, :, 0::2], out[:, t, :, 1::2] = z.real, z.imag
+    return out
+
+
+def pin_rope_at_matches_full(M):
+    """The sampled-query form equals the whole-grid form at every sampled query, both pad modes,
+    with a base and scale other than the defaults (so both must be passed through)."""
+    rng = np.random.default_rng(37)
+    for H, W, k, s, pm in ((9, 7, 4, 2, 0), (9, 7, 4, 2, 1), (6, 10, 8, 3, 1), (5, 5, 8, 0, 0)):
+        L = H * W
+        q = rng.standard_normal((2, L, 2, 16))
+        kk = rng.standard_normal((2, L + pm, 2, 16))
+        v = rng.standard_normal((2, L + pm, 2, 16))
+        full = M.swin_attention_rope(q, kk, v, H, W, k, s, pm, 40.0, 0.6)
+        qs = np.array([(b, y, x) for b in range(2) for y in range(H) for x in range(W)
+                       if (b * 7 + y * 3 + x) % 4 == 0])
+        got = M.swin_attention_rope_at(q, kk, v, H, W, k, s, pm, qs, 40.0, 0.6)
+        want = full[qs[:, 0], qs[:, 1] * W + qs[:, 2]]
+        np.testing.assert_allclose(got, want, atol=1e-12, err_msg=str((H, W, k, s, pm)))
+
+
+def pin_rope_lse_one_hot(M):
+    """LSE of the RoPE attention read off the textbook attention of inputs rotated by this file's
+    own rotation with one-hot values (out[i, j] = P_ij); a second, global case against scipy."""
+    rng = np.random.default_rng(38)
+    theta, scale = 30.0, 0.7
+    for H, W, k, s, pm in ((5, 7, 4, 2, 0), (5, 7, 4, 2, 1), (7, 5, 8, 3, 1)):
+        L = H * W
+        d = 36                                   # >= L + 1 keys, a multiple of 4
+        q = rng.standard_normal((1, L, 1, d))
+        kk = rng.standard_normal((1, L + pm, 1, d))
+        v = np.zeros_like(kk)
+        v[0, np.arange(L + pm), 0, np.arange(L + pm)] = 1.0
+        qr, kr = _rotate_here(q, H, W, theta, scale), _rotate_here(kk, H, W, theta, scale)
+        out = SO.swin_attention_textbook(qr, kr, v, H, W, k, s, pm)       # out[0, i, 0, j] = P_ij
+        lse = M.swin_attention_rope_lse(q, kk, v, H, W, k, s, pm, theta, scale)
+        c = 1.0 / math.sqrt(d)
+        for i in range(L):
+            j = int(np.argmax(out[0, i, 0]))
+            w = 1.0
+            if j == L:
+                w = float(k * k - np.count_nonzero(out[0, i, 0, :L] > 0))
+            want = c * float(qr[0, i, 0] @ kr[0, j, 0]) + math.log(w) - math.log(out[0, i, 0, j])
+            assert abs(lse[0, 0, i] - want) < 1e-10, ((H, W, k, s, pm), i, lse[0, 0, i], want)
+    H, W, d = 4, 6, 8
+    q = rng.standard_normal((2, H * W, 3, d))
+    kk = rng.standard_normal((2, H * W, 3, d))
+    v = rng.standard_normal((2, H * W, 3, d))
+    lse = M.swin_attention_rope_lse(q, kk, v, H, W, 7, 0, 0, theta, scale)
+    qr, kr = _rotate_here(q, H, W, theta, scale), _rotate_here(kk, H, W, theta, scale)
+    z = np.einsum("bihd,bjhd->bhij", qr, kr) / math.sqrt(d)
+    np.testing.assert_allclose(lse, scipy.special.logsumexp(z, axis=-1), rtol=1e-12, atol=1e-12)
+
+
 PINS = [pin_golden, pin_complex_form, pin_norms_and_pad_row, pin_scale_zero_is_plain, pin_relative_positions,
-        pin_inverse, pin_rope_bwd_fd]
+        pin_inverse, pin_rope_bwd_fd, pin_rope_at_matches_full, pin_rope_lse_one_hot]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -183,7 +255,42 @@ def _apply_inverse_skipped_on_pad(x, H, W, theta=10000.0, scale=1.0, y0=0.0, x0=
     return out
 
 
+_orig_at = R.swin_attention_rope_at
+_orig_lse = R.swin_attention_rope_lse
+
+
+def _at_k_unrotated(q, k, v, H, W, window, shift, pad_mode, queries, theta=10000.0, scale=1.0):
+    return SO.swin_attention_at(_orig_apply(q, H, W, theta, scale), k, v, H, W, window, shift, pad_mode, queries)
+
+
+def _at_scale_dropped(q, k, v, H, W, window, shift, pad_mode, queries, theta=10000.0, scale=1.0):
+    return _orig_at(q, k, v, H, W, window, shift, pad_mode, queries, theta, 1.0)
+
+
+def _at_theta_dropped(q, k, v, H, W, window, shift, pad_mode, queries, theta=10000.0, scale=1.0):
+    return _orig_at(q, k, v, H, W, window, shift, pad_mode, queries, 10000.0, scale)
+
+
+def _lse_k_unrotated(q, k, v, H, W, window, shift, pad_mode=0, theta=10000.0, scale=1.0):
+    from oracle.backward import swin_attention_lse
+    return swin_attention_lse(_orig_apply(q, H, W, theta, scale), k, v, H, W, window, shift, pad_mode)
+
+
+def _lse_scale_dropped(q, k, v, H, W, window, shift, pad_mode=0, theta=10000.0, scale=1.0):
+    return _orig_lse(q, k, v, H, W, window, shift, pad_mode, theta, 1.0)
+
+
+def _lse_theta_dropped(q, k, v, H, W, window, shift, pad_mode=0, theta=10000.0, scale=1.0):
+    return _orig_lse(q, k, v, H, W, window, shift, pad_mode, 10000.0, scale)
+
+
 MUTANTS = {
+    "at_k_unrotated": {"swin_attention_rope_at": _at_k_unrotated},
+    "at_scale_dropped": {"swin_attention_rope_at": _at_scale_dropped},
+    "at_theta_dropped": {"swin_attention_rope_at": _at_theta_dropped},
+    "lse_k_unrotated": {"swin_attention_rope_lse": _lse_k_unrotated},
+    "lse_scale_dropped": {"swin_attention_rope_lse": _lse_scale_dropped},
+    "lse_theta_dropped": {"swin_attention_rope_lse": _lse_theta_dropped},
     "inverse_is_forward": {"apply_rope": _apply_no_inverse},
     "pad_gradient_dropped": {"apply_rope": _apply_inverse_skipped_on_pad},
     "axes_swapped": {"rope_angles": _angles_axes_swapped},
