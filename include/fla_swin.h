@@ -29,18 +29,23 @@
  * owned by the caller; the library never allocates, frees, copies or synchronises.
  * q, k and v may alias each other; out must not overlap any of them.
  *
- * Errors.  Each entry point checks its arguments in the order of the status codes below
- * (after the size checks) and returns the first failure without launching anything and
- * without touching out.  An empty problem (B, heads, Hgrid or Wgrid equal to 0) returns
- * FLA_OK at once and ignores the pointers.  Launches are asynchronous on `stream`
- * (a hipStream_t; NULL = the null stream): a fault during execution surfaces at the
- * caller's next synchronisation, not here.  The library is stateless apart from a
- * per-device architecture probe and is safe to call from several threads.
+ * Errors.  Each entry point checks its arguments in this order and returns the first
+ * failure without launching anything and without touching any output: FLA_ERR_SHAPE
+ * (n_grids, then negative sizes), FLA_ERR_NULL, FLA_ERR_ALIGN, FLA_ERR_HEAD_DIM,
+ * FLA_ERR_WINDOW, FLA_ERR_SHIFT, FLA_ERR_PAD_MODE, FLA_ERR_ROPE, FLA_ERR_TOO_LARGE,
+ * FLA_ERR_UNSUPPORTED, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS, FLA_ERR_ARCH, FLA_ERR_LAUNCH.
+ * An empty problem (B, heads, Hgrid or Wgrid equal to 0) returns FLA_OK at once and
+ * ignores the pointers.  Launches are asynchronous on `stream` (NULL = the null stream):
+ * a fault during execution surfaces at the caller's next synchronisation, not here.  The
+ * library is stateless apart from a per-device architecture probe and is safe to call
+ * from several threads.
  */
 #ifndef FLA_SWIN_H
 #define FLA_SWIN_H
 
 #include <stddef.h>
+
+#include <hip/hip_runtime_api.h>   /* hipStream_t */
 
 #ifdef __cplusplus
 extern "C" {
@@ -53,28 +58,29 @@ typedef enum {
 
 typedef enum {
     FLA_OK = 0,
-    FLA_ERR_SHAPE = 1,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8       */
-    FLA_ERR_NULL = 2,      /* a pointer is NULL on a non-empty problem                     */
-    FLA_ERR_ALIGN = 3,     /* a pointer is not 16-byte aligned                             */
+    FLA_ERR_NULL = 1,      /* a pointer is NULL on a non-empty problem (the grid list of the
+                              multi-scale entry points: always)                           */
+    FLA_ERR_ALIGN = 2,     /* a pointer is not 16-byte aligned                             */
+    FLA_ERR_SHAPE = 3,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8       */
     FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (supported: 64)                      */
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
     FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */
-    FLA_ERR_TOO_LARGE = 8, /* a tensor has 2^40 elements or more, the launch would need
+    FLA_ERR_ALIAS = 8,     /* an output (out, lse, dq, dk, dv, workspace) overlaps an input
+                              or another output                                          */
+    FLA_ERR_ARCH = 9,      /* the current device is not gfx950, or no device is present   */
+    FLA_ERR_LAUNCH = 10,   /* the HIP runtime refused the kernel launch                    */
+    FLA_ERR_TOO_LARGE = 11, /* a tensor has 2^40 elements or more, the launch would need
                               2^24 workgroups or more, the rows of one window span 2 GiB or
                               more (min(window, Hgrid) * Wgrid * heads * head_dim * element
                               bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
-    FLA_ERR_ALIAS = 9,     /* an output (out, lse, dq, dk, dv, workspace) overlaps an input
-                              or another output                                          */
-    FLA_ERR_ARCH = 10,     /* the current device is not gfx950, or no device is present   */
-    FLA_ERR_LAUNCH = 11,   /* the HIP runtime refused the kernel launch                    */
     FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE backward with a window of more than 256 tokens
                                  (min(window, H) * min(window, W) > 256), or bf16 RoPE
                                  forward with min(window, H) or min(window, W) above 32   */
     FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
                                fla_swin_attn_bwd_workspace() reports                      */
     FLA_ERR_ROPE = 14      /* RoPE entry points: rope_theta not finite and > 0, or
-                              rope_scale not finite (checked after FLA_ERR_PAD_MODE)      */
+                              rope_scale not finite                                       */
 } fla_status;
 
 /* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
@@ -82,13 +88,13 @@ typedef enum {
  * P is rounded to bf16 before P.V.  Returns an fla_status. */
 int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out,
                       int B, int heads, int Hgrid, int Wgrid, int head_dim,
-                      int window, int shift, int pad_mode, void* stream);
+                      int window, int shift, int pad_mode, hipStream_t stream);
 
 /* fp32 forward: same operation and layout with float tensors, computed entirely in
  * fp32 (used for tight-tolerance checks on small grids).  Returns an fla_status. */
 int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out,
                           int B, int heads, int Hgrid, int Wgrid, int head_dim,
-                          int window, int shift, int pad_mode, void* stream);
+                          int window, int shift, int pad_mode, hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* fla_status_string(int status);
@@ -121,12 +127,12 @@ int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim,
  * have no tokens is empty, and the size limits of FLA_ERR_TOO_LARGE apply to every grid. */
 int fla_swin_attn_ms_fwd(const void* q, const void* k, const void* v, void* out,
                          int B, int heads, int n_grids, const int* grid_hw, int head_dim,
-                         int window, int shift, int pad_mode, void* stream);
+                         int window, int shift, int pad_mode, hipStream_t stream);
 
 /* fp32 multi-scale forward: the same with float tensors, computed entirely in fp32. */
 int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, float* out,
                              int B, int heads, int n_grids, const int* grid_hw, int head_dim,
-                             int window, int shift, int pad_mode, void* stream);
+                             int window, int shift, int pad_mode, hipStream_t stream);
 
 /* Algorithmic work of one multi-scale call: fla_swin_attn_work summed over the grids, with
  * one shared pad row instead of one per grid. */
@@ -149,11 +155,11 @@ int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int
 int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out,
                            int B, int heads, int Hgrid, int Wgrid, int head_dim,
                            int window, int shift, int pad_mode, float rope_theta,
-                           float rope_scale, void* stream);
+                           float rope_scale, hipStream_t stream);
 int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, float* out,
                                int B, int heads, int Hgrid, int Wgrid, int head_dim,
                                int window, int shift, int pad_mode, float rope_theta,
-                               float rope_scale, void* stream);
+                               float rope_scale, hipStream_t stream);
 
 /* bf16 RoPE training forward: fla_swin_attn_rope_fwd, and also lse as in
  * fla_swin_attn_fwd_lse (of the rotated logits).  Errors as for fla_swin_attn_rope_fwd and
@@ -161,7 +167,7 @@ int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, f
 int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
                                int B, int heads, int Hgrid, int Wgrid, int head_dim,
                                int window, int shift, int pad_mode, float rope_theta,
-                               float rope_scale, void* stream);
+                               float rope_scale, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------------
  * Training: the forward that keeps the log-sum-exp, and the backward pass.
@@ -184,16 +190,16 @@ int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void
  * denominator is the sum of the bf16-rounded probabilities the output uses. */
 int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
                           int B, int heads, int Hgrid, int Wgrid, int head_dim,
-                          int window, int shift, int pad_mode, void* stream);
+                          int window, int shift, int pad_mode, hipStream_t stream);
 int fla_swin_attn_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
                               float* lse, int B, int heads, int Hgrid, int Wgrid, int head_dim,
-                              int window, int shift, int pad_mode, void* stream);
+                              int window, int shift, int pad_mode, hipStream_t stream);
 int fla_swin_attn_ms_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
                              int B, int heads, int n_grids, const int* grid_hw, int head_dim,
-                             int window, int shift, int pad_mode, void* stream);
+                             int window, int shift, int pad_mode, hipStream_t stream);
 int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
                                  float* lse, int B, int heads, int n_grids, const int* grid_hw,
-                                 int head_dim, int window, int shift, int pad_mode, void* stream);
+                                 int head_dim, int window, int shift, int pad_mode, hipStream_t stream);
 
 /* Workspace the backward needs, in bytes (host arithmetic only).  With nqb = the number of
  * 256-token blocks of the largest window (1 when every window has at most 256 tokens):
@@ -222,21 +228,21 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
  * grid); wider windows (min(window, H) * min(window, W) > 256 for some grid) are taken in
  * key blocks of 256, each writing its fp32 share of dq to the workspace, and a second
  * kernel sums the shares in block order and rounds dq once.  Errors: checked in the order
- * of the status codes (after the size checks), then FLA_ERR_TOO_LARGE, FLA_ERR_WORKSPACE,
- * FLA_ERR_ALIAS, FLA_ERR_ARCH; nothing is launched and no output is touched on error.
+ * stated at the top of this header (FLA_ERR_WORKSPACE after FLA_ERR_TOO_LARGE, before
+ * FLA_ERR_ALIAS); nothing is launched and no output is touched on error.
  * Asynchronous on `stream`: one kernel (two for windows over 256 tokens), and the
  * pad-gradient reduction in FLA_PAD_KVTOKEN mode. */
 int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                       const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
-                      int Wgrid, int head_dim, int window, int shift, int pad_mode, void* stream);
+                      int Wgrid, int head_dim, int window, int shift, int pad_mode, hipStream_t stream);
 
 /* fp32 backward: the same with float tensors, computed entirely in fp32, any window size. */
 int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,
                           const float* dout, const float* lse, float* dq, float* dk, float* dv,
                           void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
                           int Wgrid, int head_dim, int window, int shift, int pad_mode,
-                          void* stream);
+                          hipStream_t stream);
 
 /* Multi-scale backward (App. C): the backward of fla_swin_attn_ms_fwd; the shared pad
  * token's gradient sums over all grids. */
@@ -244,12 +250,12 @@ int fla_swin_attn_ms_bwd(const void* q, const void* k, const void* v, const void
                          const void* dout, const float* lse, void* dq, void* dk, void* dv,
                          void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
                          const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
-                         void* stream);
+                         hipStream_t stream);
 int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, const float* out,
                              const float* dout, const float* lse, float* dq, float* dk, float* dv,
                              void* workspace, size_t workspace_bytes, int B, int heads,
                              int n_grids, const int* grid_hw, int head_dim, int window, int shift,
-                             int pad_mode, void* stream);
+                             int pad_mode, hipStream_t stream);
 
 /* bf16 RoPE backward: the gradients of fla_swin_attn_rope_fwd with respect to the unrotated q, k
  * and v.  Inside, q and k are rotated as they are loaded (as in the forward) and the
@@ -264,7 +270,7 @@ int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const vo
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
                            int Wgrid, int head_dim, int window, int shift, int pad_mode,
-                           float rope_theta, float rope_scale, void* stream);
+                           float rope_theta, float rope_scale, hipStream_t stream);
 
 /* Algorithmic work of one backward call:
  *   *flops = 10 * head_dim * heads * B * pairs (pairs as in fla_swin_attn_work: the five

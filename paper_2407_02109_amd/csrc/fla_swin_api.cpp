@@ -209,7 +209,7 @@ void set_rope(fla::SwinArgs* a, const Rope& r) {
 // lse: NULL for the plain forward; the training forward passes want_lse and its buffer.
 int forward(const void* q, const void* k, const void* v, void* out, float* lse, bool want_lse, int B,
             int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
-            void* stream, int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t),
+            hipStream_t stream, int elem_bytes, hipError_t (*launch)(const fla::SwinArgs&, hipStream_t),
             const Rope* rope = nullptr) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
@@ -250,7 +250,7 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
     fla::SwinArgs a = make_args(pr, q, k, v, out, want_lse ? lse : nullptr, B, heads, n_grids, head_dim,
                                 window, shift, pad_mode, cus);
     if (rope) set_rope(&a, *rope);
-    if (launch(a, static_cast<hipStream_t>(stream)) != hipSuccess) {
+    if (launch(a, stream) != hipSuccess) {
         (void)hipGetLastError();
         return FLA_ERR_LAUNCH;
     }
@@ -274,7 +274,7 @@ int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode, boo
 int backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
              const float* lse, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes, int B,
              int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
-             void* stream, int elem_bytes, const Rope* rope = nullptr) {
+             hipStream_t stream, int elem_bytes, const Rope* rope = nullptr) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
     bool empty = false;
@@ -334,7 +334,7 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.ws = static_cast<float*>(ws);
     a.ws_dq = dq_shares ? a.ws + pad_partial_bytes(B, heads, pr.geo, pad_mode) / 4 : nullptr;
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
-    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const hipStream_t s = stream;
     hipError_t e = elem_bytes != 2 ? fla::launch_swin_bwd_f32(a, s)
                    : wide         ? fla::launch_swin_bwd_bf16_wide(a, s)
                                   : fla::launch_swin_bwd_bf16(a, s);
@@ -404,7 +404,7 @@ extern "C" {
 
 int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
                       int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
-                      void* stream) {
+                      hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
                    stream, 2, fla::launch_swin_fwd_bf16);
@@ -412,7 +412,7 @@ int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out, in
 
 int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                           int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
-                          int pad_mode, void* stream) {
+                          int pad_mode, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
                    stream, 4, fla::launch_swin_fwd_f32);
@@ -420,21 +420,21 @@ int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float*
 
 int fla_swin_attn_ms_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
                          int n_grids, const int* grid_hw, int head_dim, int window, int shift,
-                         int pad_mode, void* stream) {
+                         int pad_mode, hipStream_t stream) {
     return forward(q, k, v, out, nullptr, false, B, heads, n_grids, grid_hw, head_dim, window, shift,
                    pad_mode, stream, 2, fla::launch_swin_fwd_bf16);
 }
 
 int fla_swin_attn_ms_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                              int heads, int n_grids, const int* grid_hw, int head_dim, int window,
-                             int shift, int pad_mode, void* stream) {
+                             int shift, int pad_mode, hipStream_t stream) {
     return forward(q, k, v, out, nullptr, false, B, heads, n_grids, grid_hw, head_dim, window, shift,
                    pad_mode, stream, 4, fla::launch_swin_fwd_f32);
 }
 
 int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse, int B,
                           int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
-                          int pad_mode, void* stream) {
+                          int pad_mode, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
                    fla::launch_swin_fwd_bf16);
@@ -442,7 +442,7 @@ int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out
 
 int fla_swin_attn_fwd_lse_f32(const float* q, const float* k, const float* v, float* out, float* lse,
                               int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
-                              int shift, int pad_mode, void* stream) {
+                              int shift, int pad_mode, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 4,
                    fla::launch_swin_fwd_f32);
@@ -450,21 +450,21 @@ int fla_swin_attn_fwd_lse_f32(const float* q, const float* k, const float* v, fl
 
 int fla_swin_attn_ms_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,
                              int B, int heads, int n_grids, const int* grid_hw, int head_dim,
-                             int window, int shift, int pad_mode, void* stream) {
+                             int window, int shift, int pad_mode, hipStream_t stream) {
     return forward(q, k, v, out, lse, true, B, heads, n_grids, grid_hw, head_dim, window, shift,
                    pad_mode, stream, 2, fla::launch_swin_fwd_bf16);
 }
 
 int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v, float* out,
                                  float* lse, int B, int heads, int n_grids, const int* grid_hw,
-                                 int head_dim, int window, int shift, int pad_mode, void* stream) {
+                                 int head_dim, int window, int shift, int pad_mode, hipStream_t stream) {
     return forward(q, k, v, out, lse, true, B, heads, n_grids, grid_hw, head_dim, window, shift,
                    pad_mode, stream, 4, fla::launch_swin_fwd_f32);
 }
 
 int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out, int B, int heads,
                            int Hgrid, int Wgrid, int head_dim, int window, int shift, int pad_mode,
-                           float rope_theta, float rope_scale, void* stream) {
+                           float rope_theta, float rope_scale, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     const Rope r{rope_theta, rope_scale};
     return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
@@ -473,7 +473,7 @@ int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* ou
 
 int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, float* out, int B,
                                int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
-                               int pad_mode, float rope_theta, float rope_scale, void* stream) {
+                               int pad_mode, float rope_theta, float rope_scale, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     const Rope r{rope_theta, rope_scale};
     return forward(q, k, v, out, nullptr, false, B, heads, 1, hw, head_dim, window, shift, pad_mode,
@@ -482,7 +482,7 @@ int fla_swin_attn_rope_fwd_f32(const float* q, const float* k, const float* v, f
 
 int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse, int B,
                                int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
-                               int pad_mode, float rope_theta, float rope_scale, void* stream) {
+                               int pad_mode, float rope_theta, float rope_scale, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     const Rope r{rope_theta, rope_scale};
     return forward(q, k, v, out, lse, true, B, heads, 1, hw, head_dim, window, shift, pad_mode, stream, 2,
@@ -493,7 +493,7 @@ int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const vo
                            const float* lse, void* dq, void* dk, void* dv, void* workspace,
                            size_t workspace_bytes, int B, int heads, int Hgrid, int Wgrid, int head_dim,
                            int window, int shift, int pad_mode, float rope_theta, float rope_scale,
-                           void* stream) {
+                           hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     const Rope r{rope_theta, rope_scale};
     return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
@@ -523,7 +523,7 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
 int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
                       const float* lse, void* dq, void* dk, void* dv, void* workspace,
                       size_t workspace_bytes, int B, int heads, int Hgrid, int Wgrid, int head_dim,
-                      int window, int shift, int pad_mode, void* stream) {
+                      int window, int shift, int pad_mode, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
                     head_dim, window, shift, pad_mode, stream, 2);
@@ -532,7 +532,7 @@ int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* o
 int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,
                           const float* dout, const float* lse, float* dq, float* dk, float* dv,
                           void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
-                          int Wgrid, int head_dim, int window, int shift, int pad_mode, void* stream) {
+                          int Wgrid, int head_dim, int window, int shift, int pad_mode, hipStream_t stream) {
     const int hw[2] = {Hgrid, Wgrid};
     return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, 1, hw,
                     head_dim, window, shift, pad_mode, stream, 4);
@@ -542,7 +542,7 @@ int fla_swin_attn_ms_bwd(const void* q, const void* k, const void* v, const void
                          const void* dout, const float* lse, void* dq, void* dk, void* dv,
                          void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
                          const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
-                         void* stream) {
+                         hipStream_t stream) {
     return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, n_grids,
                     grid_hw, head_dim, window, shift, pad_mode, stream, 2);
 }
@@ -551,7 +551,7 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
                              const float* dout, const float* lse, float* dq, float* dk, float* dv,
                              void* workspace, size_t workspace_bytes, int B, int heads, int n_grids,
                              const int* grid_hw, int head_dim, int window, int shift, int pad_mode,
-                             void* stream) {
+                             hipStream_t stream) {
     return backward(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_bytes, B, heads, n_grids,
                     grid_hw, head_dim, window, shift, pad_mode, stream, 4);
 }

@@ -70,6 +70,30 @@ def test_status_strings_cover_every_code(lib):
     assert fb.fla_status_string(-1) == "unknown status"
 
 
+def test_status_values_are_the_interface_table():
+    """The numeric status values of the interface (the ten of the boundary's contract, then the
+    library's own additions after FLA_ERR_LAUNCH), and the numbers the binding exposes."""
+    want = {"FLA_OK": 0, "FLA_ERR_NULL": 1, "FLA_ERR_ALIGN": 2, "FLA_ERR_SHAPE": 3, "FLA_ERR_HEAD_DIM": 4,
+            "FLA_ERR_WINDOW": 5, "FLA_ERR_SHIFT": 6, "FLA_ERR_PAD_MODE": 7, "FLA_ERR_ALIAS": 8,
+            "FLA_ERR_ARCH": 9, "FLA_ERR_LAUNCH": 10, "FLA_ERR_TOO_LARGE": 11, "FLA_ERR_UNSUPPORTED": 12,
+            "FLA_ERR_WORKSPACE": 13, "FLA_ERR_ROPE": 14}
+    codes = _header_enum("FLA")
+    assert {k: v for k, v in codes.items() if k.startswith("FLA_ERR") or k == "FLA_OK"} == want
+    assert codes["FLA_PAD_MASK"] == 0 and codes["FLA_PAD_KVTOKEN"] == 1
+
+
+def test_stream_parameter_is_a_hip_stream():
+    """Every launching entry point takes its stream as hipStream_t (NULL = the null stream)."""
+    text = open(HEADER).read()
+    assert "void* stream" not in text
+    decls = re.findall(r"int\s+(fla_swin_attn_\w+)\(([^;]*)\);", text)
+    launching = [n for n, a in decls if "stream" in a]
+    assert len(launching) >= 14
+    for n, a in decls:
+        if "stream" in a:
+            assert re.search(r"hipStream_t\s+stream\s*$", a.strip()), n
+
+
 # fake, 256-byte aligned, non-overlapping device addresses: never dereferenced on failure
 Q, K, V, OUT = 0x10000000, 0x20000000, 0x30000000, 0x40000000
 GOOD = dict(B=1, heads=12, Hgrid=64, Wgrid=64, head_dim=64, window=16, shift=8, pad_mode=0)
@@ -116,7 +140,7 @@ def test_argument_checks(lib, fn, status, kw):
 
 def test_first_failing_check_wins(lib):
     codes = _header_enum("FLA")
-    # NULL and bad shift: NULL is reported (checks run in status-code order)
+    # NULL and bad shift: NULL is reported (the header's check order)
     assert _call(fb.fla_swin_attn_fwd, q=0, shift=99) == codes["FLA_ERR_NULL"]
     # bad head_dim and bad shift: head_dim first
     assert _call(fb.fla_swin_attn_fwd, head_dim=48, shift=99) == codes["FLA_ERR_HEAD_DIM"]
