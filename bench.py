@@ -11,6 +11,12 @@ Prints one JSON line: microseconds per layer (the headline), TFLOP/s and the fra
 the bf16 matrix-core peak, the HBM roofline of the kernel, the fp64 CPU oracle timed on
 this host as a baseline, and a "backward" object: the same layer's training forward and
 backward pass (dq, dk, dv) with their own roofline.
+
+Headline mode.  A layer whose bytes exceed the 256 MB last-level cache (MALL) is timed
+cold: before each timed call a read-only pass over a 1 GiB buffer evicts the inputs from
+L2 and the MALL (reads only, so no dirty lines are left to compete with the call's own
+traffic), and each call sits between its own pair of events.  Smaller layers fit the MALL
+and are timed warm, back to back.  Both figures are always reported.
 """
 from __future__ import annotations
 
@@ -32,6 +38,8 @@ PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 SIMDS = 256 * 4               # MI355X: 256 compute units of 4 SIMDs
 XCDS = 8                      # accelerator complex dies; rocprofv3 sums GRBM_GUI_ACTIVE over them
+MALL_BYTES = 256 << 20        # MI355X last-level (Infinity) cache
+FLUSH_BYTES = 1 << 30         # read before each cold call: 4x the MALL
 # the kernel each leg's roofline is about, and the sources its hash covers
 KERNELS = {
     "fwd": ("swin_fwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
@@ -110,12 +118,20 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
                 out.extend(csv.DictReader(f))
         return out
 
-    trace = [r for r in rows("trace/**/*kernel_trace.csv") if kname in r["Kernel_Name"]]
+    all_rows = sorted(rows("trace/**/*kernel_trace.csv"), key=lambda r: int(r["Start_Timestamp"]))
+    trace = [r for r in all_rows if kname in r["Kernel_Name"]]
     # the workload's own launches: the most common grid (the bench also times a one-token
     # launch of the same kernel, for the launch overhead)
     grids = collections.Counter(r["Grid_Size_X"] for r in trace)
     main_grid = grids.most_common(1)[0][0] if grids else None
     durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace if r["Grid_Size_X"] == main_grid]
+    # cold launches: those that directly follow the read-only cache flush (a reduction kernel)
+    cold_durs, warm_durs, prev = [], [], None
+    for r in all_rows:
+        if kname in r["Kernel_Name"] and r["Grid_Size_X"] == main_grid:
+            cold = prev is not None and "reduce_kernel" in prev["Kernel_Name"]
+            (cold_durs if cold else warm_durs).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        prev = r
     # the kernel those launches ran (swin_bwd_bf16_wide_kernel for windows of more than 256 tokens)
     found = sorted({m.group(1) for r in trace if r["Grid_Size_X"] == main_grid
                     for m in [re.search(r"(%s\w*_kernel)" % kname, r["Kernel_Name"])] if m})
@@ -165,6 +181,11 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
     if durs:
         lines += ["Kernel trace: %d dispatches, duration avg %.2f us, median %.2f us, min %.2f us, max %.2f us"
                   % (len(durs), st.mean(durs) / 1e3, st.median(durs) / 1e3, min(durs) / 1e3, max(durs) / 1e3), ""]
+    if cold_durs:
+        lines += ["Cold launches (each right after the read-only 1 GiB flush): %d, duration avg %.2f us, "
+                  "median %.2f us" % (len(cold_durs), st.mean(cold_durs) / 1e3, st.median(cold_durs) / 1e3),
+                  "Warm launches (the others): %d, duration avg %.2f us, median %.2f us"
+                  % (len(warm_durs), st.mean(warm_durs) / 1e3, st.median(warm_durs) / 1e3), ""]
     if stats:
         lines += ["| kernel | calls | total ns | average ns | percentage |", "|---|---|---|---|---|"]
         for r in stats:
@@ -192,7 +213,9 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
                        "fetch_kib": counters["FETCH_SIZE"], "write_kib": counters["WRITE_SIZE"],
                        "fetch_scale": fetch_scale, "write_scale": write_scale,
                        "mfma_flop_per_launch": mfma_flop, "mfma_busy": mfma_busy,
-                       "avg_duration_us": st.mean(durs) / 1e3 if durs else None}, f, indent=1)
+                       "avg_duration_us": st.mean(durs) / 1e3 if durs else None,
+                       "avg_cold_us": st.mean(cold_durs) / 1e3 if cold_durs else None,
+                       "avg_warm_us": st.mean(warm_durs) / 1e3 if warm_durs else None}, f, indent=1)
     print("\n".join(lines))
 
 
@@ -234,7 +257,39 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
             "kind": "oracle",
             "sample": "fp64 textbook oracle on %d of %d heads of the %s layer, median of 3, "
                       "scaled to the whole layer; host %s with %d usable cores"
-                      % (use_heads, heads, wl.name, os.uname().machine, len(os.sched_getaffinity(0)))}
+                      % (use_heads, heads, wl.name, cpu_model(), len(os.sched_getaffinity(0))),
+            "cpu_model": cpu_model(), "usable_cores": len(os.sched_getaffinity(0)),
+            "bruteforce_tiny_us": bruteforce_tiny()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return os.uname().machine
+
+
+def bruteforce_tiny() -> dict:
+    """The oracle's brute-force form (every query scans every key with the region test) on the
+    two 32x32 fp32 workloads, shift 0 and 4: median of 3 runs, microseconds per layer."""
+    import oracle
+    from paper_2407_02109_amd import synth
+    res = {}
+    for name in ("tiny_s0", "tiny_s4"):
+        wl = synth.WORKLOADS[name]
+        q, k, v = (synth.to_f64_numpy(t) for t in synth.make_inputs(wl))
+        times = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            oracle.swin_attention_bruteforce(q, k, v, wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
+            times.append(time.perf_counter() - t0)
+        res[name] = round(statistics.median(times) * 1e6, 1)
+    return res
 
 
 def device_info(torch) -> dict:
@@ -263,9 +318,11 @@ def percentiles(xs):
 
 def per_call_us(step, stream, calls: int, before=None):
     """Duration of single calls, each bracketed by its own pair of events on the stream;
-    `before` (e.g. a cache flush) runs ahead of each call, outside its events."""
+    `before` (e.g. a cache flush) runs ahead of each call, outside its events.  Without
+    `before` each call is synchronised before the next is issued; with it the calls are
+    issued without waiting (the flush ahead of each call keeps the queue ahead of the host)."""
     import torch
-    out = []
+    evs = []
     for _ in range(calls):
         if before is not None:
             before()
@@ -274,12 +331,50 @@ def per_call_us(step, stream, calls: int, before=None):
         e0.record(stream)
         step()
         e1.record(stream)
-        e1.synchronize()
-        out.append(e0.elapsed_time(e1) * 1e3)
-    return out
+        if before is None:
+            e1.synchronize()
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 for a, b in evs]
 
 
-def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
+class ReadFlush:
+    """Evicts L2 and the MALL by reading FLUSH_BYTES of other data (a sum over a 1 GiB buffer
+    on the stream): reads only, so the caches are left holding clean lines."""
+
+    def __init__(self, torch, device, stream):
+        self.buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device=device)
+        self.acc = torch.zeros((), dtype=torch.float32, device=device)
+        self.stream = stream
+        self.torch = torch
+
+    def __call__(self):
+        with self.torch.cuda.stream(self.stream):
+            self.torch.sum(self.buf, dim=0, out=self.acc)
+
+
+def stream_ceiling(torch, qd, kd, vd, out, stream, flush) -> dict:
+    """A plain streaming kernel over the layer's own bytes: torch.addcmul reading as many bytes
+    of q, k and v as the layer reads and writing out once, warm (back to back) and cold (after
+    the same read-only flush).  It is the practical HBM rate for this traffic pattern."""
+    n = out.numel()
+    a, b, c, o = qd.view(-1)[:n], kd.view(-1)[:n], vd.view(-1)[:n], out.view(-1)
+
+    def run():
+        torch.addcmul(a, b, c, out=o)
+
+    for _ in range(200):
+        run()
+    warm = per_call_us(run, stream, 200)
+    cold = per_call_us(run, stream, 100, before=flush)
+    nbytes = 4 * n * out.element_size()
+    return {"kernel": "torch.addcmul (3 reads, 1 write)", "bytes": nbytes,
+            "warm_p50_us": percentiles(warm)[1], "cold_p50_us": percentiles(cold)[1],
+            "warm_gbs": round(nbytes / (percentiles(warm)[1] * 1e3), 1),
+            "cold_gbs": round(nbytes / (percentiles(cold)[1] * 1e3), 1)}
+
+
+def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int, mode: str, flush) -> dict:
     """Training on the same layer: the forward that keeps the log-sum-exp, then the backward
     (dq, dk, dv for a seeded upstream gradient), each timed with events on the stream.  The
     roofline is that of swin_bwd_bf16_kernel, the backward's dominant kernel (windows of more
@@ -327,24 +422,37 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int) -> dict:
 
     fwd_us = mean_us(fwd, steps)
     fwd()
-    us = mean_us(bwd, steps)
+    warm_us = mean_us(bwd, steps)
     p10, p50, p90 = percentiles(per_call_us(bwd, stream, 100))
+    cold = per_call_us(bwd, stream, max(steps // 5, 50), before=flush)
+    cold_us = statistics.mean(cold)
+    c10, c50, c90 = percentiles(cold)
     assert torch.isfinite(dq[:, :64].float()).all() and torch.isfinite(dk[:, :64].float()).all()
     flops, nbytes = binding.fla_swin_attn_bwd_work(B, heads, grids, d, wl.window, wl.shift, wl.pad_mode, 2)
+    us = cold_us if mode == "cold" else warm_us
     tflops = flops / (us * 1e-6) / 1e12
-    return {"us_per_layer": round(us, 3), "steps": steps, "fwd_lse_us": round(fwd_us, 3),
+    traffic = measured_traffic(wl.name, "bwd")
+    return {"us_per_layer": round(us, 3), "mode": mode, "steps": steps, "fwd_lse_us": round(fwd_us, 3),
             "tflops": round(tflops, 2), "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "roofline": roofline(flops, nbytes, us, measured_traffic(wl.name, "bwd")),
+            "roofline": roofline(flops, nbytes, us, traffic),
+            "roofline_warm": roofline(flops, nbytes, warm_us, traffic),
+            "roofline_cold": roofline(flops, nbytes, cold_us, traffic),
             "alg_flops": flops, "alg_bytes": nbytes,
-            "timing": {"p10_us": p10, "p50_us": p50, "p90_us": p90}}
+            "timing": {"warm_mean_us": round(warm_us, 3), "warm_p10_us": p10, "warm_p50_us": p50,
+                       "warm_p90_us": p90, "cold_mean_us": round(cold_us, 3), "cold_p10_us": c10,
+                       "cold_p50_us": c50, "cold_p90_us": c90}}
 
 
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=5000,
-                    help="untimed steps first; about half a second of them lets the clocks settle")
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--mode", default="auto", choices=["auto", "cold", "warm"],
+                    help="timed mode: cold (caches flushed before each call) or warm (back to back); "
+                         "auto = cold when the layer's bytes exceed the 256 MB MALL")
+    ap.add_argument("--warmup", type=int, default=20, help="untimed steps before the timed region")
+    ap.add_argument("--settle", type=float, default=0.5,
+                    help="seconds of untimed calls before the warm-up, so that the clocks have ramped")
     ap.add_argument("--workload", default="img4096",
                     help="img1024 | img2048 | img4096 | img4096_kv | img4096_rope | ragged150x203 | "
                          "ms_img2048 (default: img4096)")
@@ -412,23 +520,53 @@ def main() -> int:
             binding.fla_swin_attn_fwd(qd, kd, vd, out, wl.B, wl.heads, wl.H, wl.W, wl.head_dim,
                                       wl.window, wl.shift, wl.pad_mode, stream)
 
-    print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    mode = args.mode if args.mode != "auto" else ("cold" if nbytes > MALL_BYTES else "warm")
+    flush = ReadFlush(torch, dev, stream)
+    # clocks: run the layer for about half a second before the counted warm-up, so that the
+    # engine clock has ramped whatever --warmup is (with a few calls only it has not)
+    print("[bench] settling clocks, then warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    settle0 = time.perf_counter()
+    settle_calls = 0
+    while time.perf_counter() - settle0 < args.settle:
+        for _ in range(100):
+            step()
+        settle_calls += 100
+        torch.cuda.synchronize()
+    settle_s = time.perf_counter() - settle0
     for _ in range(args.warmup):
         step()
+    for _ in range(20):
+        flush()
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
+
+    def warm_mean(n):
+        """Mean of n back-to-back calls between one pair of events."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            step()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    # the timed region: exactly `steps` calls of the headline mode
+    print("[bench] timing %d %s steps" % (args.steps, mode), file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
+    if mode == "cold":
+        cold = per_call_us(step, stream, args.steps, before=flush)
+        us = statistics.mean(cold)
+    else:
+        us = warm_mean(args.steps)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    gpu_ms = ev0.elapsed_time(ev1)
-    us = gpu_ms * 1e3 / args.steps
+    # the other mode, outside the timed region
+    if mode == "cold":
+        warm_us = warm_mean(max(args.steps, 1000))
+    else:
+        cold = per_call_us(step, stream, 100, before=flush)
+        warm_us = us
+    cold_us = statistics.mean(cold)
     tflops = flops / (us * 1e-6) / 1e12
     assert torch.isfinite(out[:, :64].float()).all()
 
@@ -449,32 +587,37 @@ def main() -> int:
         "config": {"workload": wl.name, "B": wl.B, "heads": wl.heads,
                    "grid": [list(g) for g in wl.grid_list] if wl.grids else [wl.H, wl.W],
                    "head_dim": wl.head_dim, "window": wl.window, "shift": wl.shift,
-                   "pad_mode": wl.pad_mode, "parallelism": "none (1 GPU)"},
+                   "pad_mode": wl.pad_mode, "parallelism": "none (1 GPU)", "timing": mode},
         "tflops": round(tflops, 2),
         "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
         "roofline": roofline(flops, nbytes, us, traffic),
+        "roofline_warm": roofline(flops, nbytes, warm_us, traffic),
+        "roofline_cold": roofline(flops, nbytes, cold_us, traffic),
         "alg_flops": flops,
         "alg_bytes": nbytes,
     }
-    # distribution of single warm calls, cold calls (L2 and the 256 MB MALL flushed by a
-    # 1 GiB write before each), and the cost of a launch on a one-token problem
+    # distributions of single warm and cold calls, a streaming kernel over the same bytes
+    # (the practical HBM ceiling), and the cost of a launch on a one-token problem
     p10, p50, p90 = percentiles(per_call_us(step, stream, 200))
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-    c10, c50, c90 = percentiles(per_call_us(step, stream, 50, before=lambda: flush.random_(0, 255)))
-    del flush
+    c10, c50, c90 = percentiles(cold)
     tq = torch.zeros(1, 1, 1, wl.head_dim, dtype=torch.bfloat16, device=dev)
     tout = torch.empty_like(tq)
     tiny = lambda: binding.fla_swin_attn_fwd(tq, tq, tq, tout, 1, 1, 1, 1, wl.head_dim, wl.window, 0,
                                              0, stream)
     l10, l50, l90 = percentiles(per_call_us(tiny, stream, 200))
-    torch.cuda.synchronize()
-    rec["timing"] = {"warm_mean_us": round(us, 3), "warm_p10_us": p10, "warm_p50_us": p50, "warm_p90_us": p90,
-                     "cold_p10_us": c10, "cold_p50_us": c50, "cold_p90_us": c90,
-                     "launch_one_token_p50_us": l50}
+    rec["timing"] = {"mode": mode, "warm_mean_us": round(warm_us, 3), "warm_p10_us": p10, "warm_p50_us": p50,
+                     "warm_p90_us": p90, "cold_mean_us": round(cold_us, 3), "cold_p10_us": c10,
+                     "cold_p50_us": c50, "cold_p90_us": c90, "cold_calls": len(cold),
+                     "launch_one_token_p50_us": l50,
+                     "flush": "read-only sum over %d MiB before each cold call" % (FLUSH_BYTES >> 20),
+                     "settle_s": round(settle_s, 3), "settle_calls": settle_calls}
+    rec["stream_ceiling"] = stream_ceiling(torch, qd, kd, vd, out, stream, flush)
     rec["device"] = device_info(torch)
     if not args.no_backward:
         print("[bench] backward", file=sys.stderr, flush=True)
-        rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps)
+        rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps, mode, flush)
+    del flush
+    torch.cuda.synchronize()
     if args.copy_calibration:
         copy_calibration()
     if not args.no_cpu_baseline:
