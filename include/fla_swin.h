@@ -33,7 +33,8 @@
  * failure without launching anything and without touching any output: FLA_ERR_SHAPE
  * (n_grids, then negative sizes), FLA_ERR_NULL, FLA_ERR_ALIGN, FLA_ERR_HEAD_DIM,
  * FLA_ERR_WINDOW, FLA_ERR_SHIFT, FLA_ERR_PAD_MODE, FLA_ERR_ROPE, FLA_ERR_TOO_LARGE,
- * FLA_ERR_UNSUPPORTED, FLA_ERR_WORKSPACE, FLA_ERR_ALIAS, FLA_ERR_ARCH, FLA_ERR_LAUNCH.
+ * FLA_ERR_UNSUPPORTED, FLA_ERR_WORKSPACE (or FLA_ERR_SCRATCH), FLA_ERR_ALIAS, FLA_ERR_ARCH,
+ * FLA_ERR_LAUNCH.
  * An empty problem (B, heads, Hgrid or Wgrid equal to 0) returns FLA_OK at once and
  * ignores the pointers.  Launches are asynchronous on `stream` (NULL = the null stream):
  * a fault during execution surfaces at the caller's next synchronisation, not here.  The
@@ -79,8 +80,10 @@ typedef enum {
                                  forward with min(window, H) or min(window, W) above 32   */
     FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
                                fla_swin_attn_bwd_workspace() reports                      */
-    FLA_ERR_ROPE = 14      /* RoPE entry points: rope_theta not finite and > 0, or
+    FLA_ERR_ROPE = 14,     /* RoPE entry points: rope_theta not finite and > 0, or
                               rope_scale not finite                                       */
+    FLA_ERR_SCRATCH = 15   /* allocation-free backward: the problem needs more workspace than
+                              the library's static scratch holds (FLA_SCRATCH_BYTES)      */
 } fla_status;
 
 /* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
@@ -236,6 +239,24 @@ int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* o
                       const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
                       int Wgrid, int head_dim, int window, int shift, int pad_mode, hipStream_t stream);
+
+/* Allocation-free bf16 backward, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): fla_swin_attn_bwd
+ * with the same kernels and results, whose workspace is instead a static device array of
+ * FLA_SCRATCH_BYTES inside the library.  The library and its callers allocate nothing for it:
+ * each device holds its own copy from the moment the library is loaded on it until the process
+ * ends; its device address is looked up once per device, on this entry point's first call there.
+ * No part of it needs clearing between calls (every workgroup writes its whole share before it
+ * is read).  All calls on one device share that device's array: calls that may run at the same
+ * time on one device (on different streams, or from several host threads without ordering)
+ * race on it and must be serialised by the caller.  Arguments, layout, results and errors as
+ * for fla_swin_attn_bwd, with FLA_ERR_SCRATCH (in place of FLA_ERR_WORKSPACE) when
+ * fla_swin_attn_bwd_workspace() exceeds FLA_SCRATCH_BYTES. */
+#define FLA_SCRATCH_BYTES (16u << 20)
+int fla_swin_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* out,
+                              const void* dout, const float* lse, void* dq, void* dk, void* dv, int B,
+                              int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                              int pad_mode, hipStream_t stream);
 
 /* fp32 backward: the same with float tensors, computed entirely in fp32, any window size. */
 int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,

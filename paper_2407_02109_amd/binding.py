@@ -62,6 +62,8 @@ def _declare(lib):
                        ("fla_swin_attn_ms_bwd", ms_bwd_args), ("fla_swin_attn_ms_bwd_f32", ms_bwd_args)):
         getattr(lib, name).argtypes = args
         getattr(lib, name).restype = I
+    lib.fla_swin_attn_bwd_noalloc.argtypes = [P] * 9 + [I, I, I, I, I, I, I, I, P]
+    lib.fla_swin_attn_bwd_noalloc.restype = I
     lib.fla_swin_attn_bwd_workspace.argtypes = [I, I, I, IP, I, I, I, ctypes.POINTER(Z)]
     lib.fla_swin_attn_bwd_workspace.restype = I
     lib.fla_swin_attn_bwd_work.argtypes = [I, I, I, IP, I, I, I, I, I, D, D]
@@ -280,6 +282,18 @@ def fla_swin_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, workspace, workspace_
     rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
             _ptr(workspace), int(workspace_bytes), B, heads, Hgrid, Wgrid, head_dim, window, shift,
             pad_mode, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_swin_attn_bwd_noalloc(q, k, v, out, dout, lse, dq, dk, dv, B, heads, Hgrid, Wgrid, head_dim, window,
+                              shift, pad_mode=FLA_PAD_MASK, stream=None, check=True) -> int:
+    """Allocation-free bf16 backward: the library's static device scratch is the workspace."""
+    lib = load_library()
+    rc = lib.fla_swin_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq),
+                                       _ptr(dk), _ptr(dv), B, heads, Hgrid, Wgrid, head_dim, window, shift,
+                                       pad_mode, _stream(stream))
     if check:
         _check(rc)
     return rc

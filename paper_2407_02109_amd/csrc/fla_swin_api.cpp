@@ -10,6 +10,8 @@
 
 #include "fla_swin_internal.h"
 
+static_assert(fla::kScratchBytes == FLA_SCRATCH_BYTES, "static scratch size of the header and the kernels");
+
 namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;
@@ -271,10 +273,12 @@ int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode, boo
     return n;
 }
 
+// static_scratch: the workspace is the library's static device scratch (ws and ws_bytes are
+// ignored), for the allocation-free entry point.
 int backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
              const float* lse, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes, int B,
              int heads, int n_grids, const int* hw, int head_dim, int window, int shift, int pad_mode,
-             hipStream_t stream, int elem_bytes, const Rope* rope = nullptr) {
+             hipStream_t stream, int elem_bytes, const Rope* rope = nullptr, bool static_scratch = false) {
     if (n_grids < 1 || n_grids > fla::kMaxGrids) return FLA_ERR_SHAPE;
     if (!hw) return FLA_ERR_NULL;
     bool empty = false;
@@ -284,6 +288,7 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     for (const void* p : {q, k, v, out, dout, static_cast<const void*>(lse), static_cast<const void*>(dq),
                           static_cast<const void*>(dk), static_cast<const void*>(dv)})
         if (!aligned16(p)) return FLA_ERR_ALIGN;
+    if (static_scratch) ws = nullptr;
     if (ws && !aligned16(ws)) return FLA_ERR_ALIGN;
     st = check_scalars(head_dim, window, shift, pad_mode);
     if (st != FLA_OK) return st;
@@ -297,7 +302,11 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     if (rope && (elem_bytes != 2 || wide)) return FLA_ERR_UNSUPPORTED;
     const bool dq_shares = elem_bytes == 2 && wide;
     const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode, dq_shares);
-    if (need > 0 && (!ws || ws_bytes < uint64_t(need))) return FLA_ERR_WORKSPACE;
+    if (static_scratch) {
+        if (need > fla::kScratchBytes) return FLA_ERR_SCRATCH;
+    } else if (need > 0 && (!ws || ws_bytes < uint64_t(need))) {
+        return FLA_ERR_WORKSPACE;
+    }
 
     const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
     const int64_t kv_bytes = int64_t(B) * pr.kv_rows * pr.tok * elem_bytes;
@@ -308,7 +317,9 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     };
     const Range inputs[] = {{q, q_bytes}, {k, kv_bytes}, {v, kv_bytes}, {out, q_bytes}, {dout, q_bytes},
                             {lse, lse_bytes}};
-    const Range outputs[] = {{dq, q_bytes}, {dk, kv_bytes}, {dv, kv_bytes}, {ws, need}};
+    // (the static scratch cannot overlap a caller's buffer: only its device address, which
+    // the library keeps to itself, reaches it)
+    const Range outputs[] = {{dq, q_bytes}, {dk, kv_bytes}, {dv, kv_bytes}, {ws, static_scratch ? 0 : need}};
     for (int i = 0; i < 4; ++i) {
         if (outputs[i].n == 0) continue;
         for (const Range& r : inputs)
@@ -321,6 +332,10 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     int cus = 0;
     st = check_arch(&cus);
     if (st != FLA_OK) return st;
+    if (static_scratch && need > 0 && fla::scratch_address(&ws) != hipSuccess) {
+        (void)hipGetLastError();
+        return FLA_ERR_LAUNCH;
+    }
 
     fla::SwinBwdArgs a;
     a.f = make_args(pr, q, k, v, nullptr, nullptr, B, heads, n_grids, head_dim, window, shift, pad_mode, cus);
@@ -529,6 +544,15 @@ int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* o
                     head_dim, window, shift, pad_mode, stream, 2);
 }
 
+int fla_swin_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* out,
+                              const void* dout, const float* lse, void* dq, void* dk, void* dv, int B,
+                              int heads, int Hgrid, int Wgrid, int head_dim, int window, int shift,
+                              int pad_mode, hipStream_t stream) {
+    const int hw[2] = {Hgrid, Wgrid};
+    return backward(q, k, v, out, dout, lse, dq, dk, dv, nullptr, 0, B, heads, 1, hw, head_dim, window,
+                    shift, pad_mode, stream, 2, nullptr, true);
+}
+
 int fla_swin_attn_bwd_f32(const float* q, const float* k, const float* v, const float* out,
                           const float* dout, const float* lse, float* dq, float* dk, float* dv,
                           void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
@@ -573,6 +597,7 @@ const char* fla_status_string(int status) {
         case FLA_ERR_UNSUPPORTED: return "window too large for this bf16 entry point (RoPE backward: 256 tokens; RoPE forward: 32 x 32)";
         case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
         case FLA_ERR_ROPE: return "rope_theta must be finite and > 0, rope_scale finite";
+        case FLA_ERR_SCRATCH: return "problem needs more workspace than the 16 MiB static scratch of the allocation-free backward";
         default: return "unknown status";
     }
 }

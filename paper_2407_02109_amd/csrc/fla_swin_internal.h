@@ -112,6 +112,11 @@ hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
 // bf16, windows of more than kBwdMaxTokens tokens: key-block kernel, then the dq reduction
 hipError_t launch_swin_bwd_bf16_wide(const SwinBwdArgs& a, hipStream_t stream);
 hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
+
+// Static device scratch of the allocation-free backward: its size, and its device address
+// on the current device (taken with hipGetSymbolAddress on the first call per device).
+constexpr int64_t kScratchBytes = int64_t(16) << 20;
+hipError_t scratch_address(void** ptr);
 // sums the partials of ws into row L of dk and dv (elem_bytes 2: bf16, 4: fp32)
 hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
 

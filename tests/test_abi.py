@@ -42,7 +42,7 @@ def test_header_declares_the_entry_points():
         "fla_swin_attn_ms_fwd_lse_f32", "fla_swin_attn_bwd_workspace", "fla_swin_attn_bwd",
         "fla_swin_attn_bwd_f32", "fla_swin_attn_ms_bwd", "fla_swin_attn_ms_bwd_f32",
         "fla_swin_attn_bwd_work", "fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32",
-        "fla_swin_attn_rope_fwd_lse", "fla_swin_attn_rope_bwd"])
+        "fla_swin_attn_rope_fwd_lse", "fla_swin_attn_rope_bwd", "fla_swin_attn_bwd_noalloc"])
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -76,7 +76,7 @@ def test_status_values_are_the_interface_table():
     want = {"FLA_OK": 0, "FLA_ERR_NULL": 1, "FLA_ERR_ALIGN": 2, "FLA_ERR_SHAPE": 3, "FLA_ERR_HEAD_DIM": 4,
             "FLA_ERR_WINDOW": 5, "FLA_ERR_SHIFT": 6, "FLA_ERR_PAD_MODE": 7, "FLA_ERR_ALIAS": 8,
             "FLA_ERR_ARCH": 9, "FLA_ERR_LAUNCH": 10, "FLA_ERR_TOO_LARGE": 11, "FLA_ERR_UNSUPPORTED": 12,
-            "FLA_ERR_WORKSPACE": 13, "FLA_ERR_ROPE": 14}
+            "FLA_ERR_WORKSPACE": 13, "FLA_ERR_ROPE": 14, "FLA_ERR_SCRATCH": 15}
     codes = _header_enum("FLA")
     assert {k: v for k, v in codes.items() if k.startswith("FLA_ERR") or k == "FLA_OK"} == want
     assert codes["FLA_PAD_MASK"] == 0 and codes["FLA_PAD_KVTOKEN"] == 1
@@ -392,9 +392,58 @@ def test_training_entry_points_without_device_report_arch(lib):
     assert _call_bwd(pad_mode=1) == codes["FLA_ERR_ARCH"]
 
 
+def _call_noalloc(**kw):
+    a = dict(GOOD)
+    a.update({k: v for k, v in kw.items() if k in GOOD})
+    p = dict(q=Q, k=K, v=V, out=OUT, dout=DOUT, lse=LSE, dq=DQ, dk=DK, dv=DV)
+    p.update({k: v for k, v in kw.items() if k in p})
+    return fb.fla_swin_attn_bwd_noalloc(p["q"], p["k"], p["v"], p["out"], p["dout"], p["lse"], p["dq"], p["dk"],
+                                        p["dv"], a["B"], a["heads"], a["Hgrid"], a["Wgrid"], a["head_dim"],
+                                        a["window"], a["shift"], a["pad_mode"], 0, check=False)
+
+
+NOALLOC_CASES = [
+    ("FLA_ERR_SHAPE", dict(B=-1)), ("FLA_ERR_NULL", dict(dout=0)), ("FLA_ERR_ALIGN", dict(dk=DK + 2)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=32)), ("FLA_ERR_SHIFT", dict(shift=16)),
+    ("FLA_ERR_PAD_MODE", dict(pad_mode=2)), ("FLA_ERR_TOO_LARGE", dict(Hgrid=1 << 20, Wgrid=1 << 20)),
+    # workspace beyond the static scratch: pad partials of 40 batch entries (40 * 25 * 12 * 512 B
+    # = 5.9 MiB fits; 160 entries do not), and the dq shares of 12 heads of window-32 windows
+    ("FLA_ERR_SCRATCH", dict(B=160, pad_mode=1)), ("FLA_ERR_SCRATCH", dict(window=32, shift=16)),
+    ("FLA_ERR_ALIAS", dict(dq=Q)), ("FLA_ERR_ALIAS", dict(dv=DK + 64)),
+]
+
+
+@pytest.mark.parametrize("status,kw", NOALLOC_CASES, ids=["%s-%d" % (c[0], i) for i, c in enumerate(NOALLOC_CASES)])
+def test_noalloc_argument_checks(lib, status, kw):
+    """The allocation-free backward checks its arguments like the backward, and turns a
+    workspace need beyond the static scratch into FLA_ERR_SCRATCH before touching a device."""
+    assert _call_noalloc(**kw) == _header_enum("FLA")[status]
+
+
+def test_noalloc_scratch_limit_matches_workspace_sizes(lib):
+    """FLA_ERR_SCRATCH exactly when fla_swin_attn_bwd_workspace() exceeds FLA_SCRATCH_BYTES."""
+    m = re.search(r"#define FLA_SCRATCH_BYTES \((\d+)u << (\d+)\)", open(HEADER).read())
+    cap = int(m.group(1)) << int(m.group(2))
+    assert cap == 16 << 20
+    code = _header_enum("FLA")["FLA_ERR_SCRATCH"]
+    for B, heads, window, shift, pm in ((1, 12, 16, 8, 1), (100, 12, 16, 8, 1), (110, 12, 16, 8, 1),
+                                        (1, 1, 32, 16, 0), (1, 2, 32, 16, 0), (1, 1, 32, 16, 1)):
+        need = fb.fla_swin_attn_bwd_workspace(B, heads, [(64, 64)], window, shift, pm)
+        st = _call_noalloc(B=B, heads=heads, window=window, shift=shift, pad_mode=pm)
+        assert (st == code) == (need > cap), (B, heads, window, need, st)
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_noalloc_without_device_reports_arch(lib):
+    codes = _header_enum("FLA")
+    assert _call_noalloc() == codes["FLA_ERR_ARCH"] and _call_noalloc(pad_mode=1) == codes["FLA_ERR_ARCH"]
+    assert _call_noalloc(heads=1, window=32, shift=16) == codes["FLA_ERR_ARCH"]
+
+
 def test_empty_training_calls_are_ok(lib):
     assert _call_lse(B=0, lse=0, q=0) == 0
     assert _call_bwd(heads=0, dq=0, ws=0, ws_bytes=0) == 0
+    assert _call_noalloc(B=0, dq=0) == 0
 
 
 @pytest.mark.parametrize("grids,k,s,pm", [
