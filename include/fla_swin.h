@@ -72,12 +72,11 @@ typedef enum {
     FLA_ERR_ARCH = 9,      /* the current device is not gfx950, or no device is present   */
     FLA_ERR_LAUNCH = 10,   /* the HIP runtime refused the kernel launch                    */
     FLA_ERR_TOO_LARGE = 11, /* a tensor has 2^40 elements or more, the launch would need
-                              2^24 workgroups or more, the rows of one window span 2 GiB or
+                              2^23 workgroups or more, the rows of one window span 2 GiB or
                               more (min(window, Hgrid) * Wgrid * heads * head_dim * element
                               bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
-    FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE backward with a window of more than 256 tokens
-                                 (min(window, H) * min(window, W) > 256), or bf16 RoPE
-                                 forward with min(window, H) or min(window, W) above 32   */
+    FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE forward or backward with min(window, H) or
+                                 min(window, W) above 32                                  */
     FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
                                fla_swin_attn_bwd_workspace() reports                      */
     FLA_ERR_ROPE = 14,     /* RoPE entry points: rope_theta not finite and > 0, or
@@ -204,16 +203,12 @@ int fla_swin_attn_ms_fwd_lse_f32(const float* q, const float* k, const float* v,
                                  float* lse, int B, int heads, int n_grids, const int* grid_hw,
                                  int head_dim, int window, int shift, int pad_mode, hipStream_t stream);
 
-/* Workspace the backward needs, in bytes (host arithmetic only).  With nqb = the number of
- * 256-token blocks of the largest window (1 when every window has at most 256 tokens):
- *   - FLA_PAD_KVTOKEN mode: 512 bytes per (batch entry, head, window, block), each block's
- *     share of the pad token's gradient;
- *   - nqb > 1 (the bf16 kernels; the fp32 ones need only the part above): nqb * 256 * 64 * 4
- *     bytes per (batch entry, head, window, key block), each key block's fp32 share of dq.
- * So 0 in FLA_PAD_MASK mode for windows of up to 256 tokens.  The largest amount is that of
- * the bf16 entry points; the fp32 ones accept it.  Single-grid callers pass n_grids = 1 and
- * grid_hw = {Hgrid, Wgrid}.  Argument errors as for the forward; bytes must be non-NULL
- * (FLA_ERR_NULL). */
+/* Workspace the backward needs, in bytes (host arithmetic only): in FLA_PAD_KVTOKEN mode 512
+ * bytes per (batch entry, head, window, block), each block's share of the pad token's
+ * gradient, where the blocks are the 128-token pieces of the largest window (nbb =
+ * ceil(max window tokens / 128)); 0 in FLA_PAD_MASK mode.  The fp32 entry points need at most
+ * as much.  Single-grid callers pass n_grids = 1 and grid_hw = {Hgrid, Wgrid}.  Argument
+ * errors as for the forward; bytes must be non-NULL (FLA_ERR_NULL). */
 int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_hw, int window,
                                 int shift, int pad_mode, size_t* bytes);
 
@@ -227,14 +222,13 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
  * S = Q.K^T, dP = dO.V^T, dV = P^T.dO, dK = dS^T.Q and dQ = dS.K run on bf16 matrix cores
  * with fp32 accumulation (P and dS rounded to bf16 before their products); outputs are
  * rounded to bf16 (RNE).  The result does not depend on scheduling (fixed summation
- * order).  One workgroup holds a window of up to 256 tokens (window <= 16 covers every
- * grid); wider windows (min(window, H) * min(window, W) > 256 for some grid) are taken in
- * key blocks of 256, each writing its fp32 share of dq to the workspace, and a second
- * kernel sums the shares in block order and rounds dq once.  Errors: checked in the order
+ * order).  Any window size: one workgroup per 128-token block of a window computes dK and dV
+ * of its keys over all the window's queries, another dQ of its queries over all the keys.
+ * Errors: checked in the order
  * stated at the top of this header (FLA_ERR_WORKSPACE after FLA_ERR_TOO_LARGE, before
  * FLA_ERR_ALIAS); nothing is launched and no output is touched on error.
- * Asynchronous on `stream`: one kernel (two for windows over 256 tokens), and the
- * pad-gradient reduction in FLA_PAD_KVTOKEN mode. */
+ * Asynchronous on `stream`: one kernel, and the pad-gradient reduction in FLA_PAD_KVTOKEN
+ * mode. */
 int fla_swin_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                       const void* dout, const float* lse, void* dq, void* dk, void* dv,
                       void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,
@@ -284,9 +278,9 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
  * rotation (dq = R^T dq', dk = R^T dk'); dv is unchanged, and the pad token, which is never
  * rotated, gets its gradient as in fla_swin_attn_bwd.  out and lse are those of
  * fla_swin_attn_rope_fwd_lse.  Arguments and errors as for fla_swin_attn_bwd, plus
- * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE) and FLA_ERR_UNSUPPORTED for windows of
- * more than 256 tokens (checked after FLA_ERR_TOO_LARGE): only the kernel that holds a
- * whole window has the rotation. */
+ * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE) and FLA_ERR_UNSUPPORTED (checked after
+ * FLA_ERR_TOO_LARGE) for windows of more than 32 rows or columns, the limit of the bf16 RoPE
+ * forward whose out and lse it takes. */
 int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,

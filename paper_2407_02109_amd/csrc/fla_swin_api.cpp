@@ -15,12 +15,12 @@ static_assert(fla::kScratchBytes == FLA_SCRATCH_BYTES, "static scratch size of t
 namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;
-constexpr int64_t kMaxGroups = (int64_t(1) << 24) - 1;   // grid.x * 256 threads < 2^32
+constexpr int64_t kMaxGroups = (int64_t(1) << 23) - 1;   // grid.x * 512 threads < 2^32
 
 // Windows of a grid list: the canvas has `origin` virtual tokens in front of each axis;
 // window i of an axis covers canvas [i*window, (i+1)*window) = grid [i*window - origin, ...).
 struct Geometry {
-    int origin, nqb, n_windows;
+    int origin, nqb, nbb, n_windows;   // nbb: bf16 backward blocks of kBwdBlock tokens
     int64_t L;                   // tokens per batch entry
     int64_t n_groups;
     fla::GridDesc grid[fla::kMaxGrids];
@@ -28,6 +28,19 @@ struct Geometry {
 
 int64_t windows_along(int64_t len, int window, int origin) {
     return len > 0 ? (len + origin + window - 1) / window : 0;
+}
+
+// Largest extent of a window along an axis of `len` tokens: the first window (clipped by the
+// origin), the last one (clipped by the end) and, when there are three or more, a full one.
+int64_t max_extent(int64_t len, int window, int origin) {
+    const int64_t n = windows_along(len, window, origin);
+    if (n == 0) return 0;
+    const int64_t first = len < window - origin ? len : window - origin;
+    const int64_t start_last = (n - 1) * window - origin;
+    const int64_t last = len - (start_last > 0 ? start_last : 0);
+    int64_t m = first > last ? first : last;
+    if (n >= 3 && window > m) m = window;
+    return m;
 }
 
 // Fills `g` for n grids of (hw[2i], hw[2i+1]) tokens; false if a count overflows int.
@@ -45,7 +58,7 @@ bool geometry(int B, int heads, int n, const int* hw, int window, int shift, Geo
         d.win_begin = (int)wins;
         d.tok_off = L;
         d.div_nwx = fla::FastDiv::make((unsigned)(nwx > 0 ? nwx : 1));
-        const int64_t rows = window < H ? window : H, cols = window < W ? window : W;
+        const int64_t rows = max_extent(H, window, g->origin), cols = max_extent(W, window, g->origin);
         if (rows * cols > nmax) nmax = rows * cols;
         wins += nwy * nwx;
         L += int64_t(H) * W;
@@ -54,6 +67,7 @@ bool geometry(int B, int heads, int n, const int* hw, int window, int shift, Geo
     g->n_windows = (int)wins;
     g->L = L;
     g->nqb = (int)((nmax + fla::kQueryBlock - 1) / fla::kQueryBlock);
+    g->nbb = (int)((nmax + fla::kBwdBlock - 1) / fla::kBwdBlock);
     g->n_groups = int64_t(B) * heads * wins * g->nqb;
     return true;
 }
@@ -260,17 +274,11 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
 }
 
 // Workspace bytes of a backward call: one pad-gradient partial per (b, head, window, block)
-// in KV-token mode; for the bf16 kernels on windows of more than 256 tokens (dq_shares)
-// also each key block's fp32 share of the window's dq.  Assumes the geometry is valid.
-int64_t pad_partial_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
+// in KV-token mode, with the bf16 kernel's blocks of kBwdBlock tokens (at least as many as
+// the fp32 kernels' blocks).  Assumes the geometry is valid.
+int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode) {
     if (pad_mode != FLA_PAD_KVTOKEN) return 0;
-    return int64_t(B) * heads * geo.n_windows * geo.nqb * fla::kPadPartial * 4;
-}
-int64_t workspace_bytes(int B, int heads, const Geometry& geo, int pad_mode, bool dq_shares) {
-    int64_t n = pad_partial_bytes(B, heads, geo, pad_mode);
-    if (dq_shares)
-        n += int64_t(B) * heads * geo.n_windows * geo.nqb * geo.nqb * fla::kQueryBlock * fla::kHeadDim * 4;
-    return n;
+    return int64_t(B) * heads * geo.n_windows * geo.nbb * fla::kPadPartial * 4;
 }
 
 // static_scratch: the workspace is the library's static device scratch (ws and ws_bytes are
@@ -296,12 +304,17 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     Problem pr;
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
-    // windows of more than kBwdMaxTokens = kQueryBlock tokens take several key blocks; the
-    // RoPE backward exists only for the bf16 kernel that holds a whole window
-    const bool wide = pr.geo.nqb > 1;
-    if (rope && (elem_bytes != 2 || wide)) return FLA_ERR_UNSUPPORTED;
-    const bool dq_shares = elem_bytes == 2 && wide;
-    const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode, dq_shares);
+    // the bf16 launch: both roles of every block of every (batch entry, window, head)
+    const int64_t units = int64_t(B) * heads * pr.geo.n_windows;
+    if (elem_bytes == 2 && fla::bwd_bf16_groups(units, pr.geo.nbb) > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    // RoPE training is bf16 only, with the RoPE forward's window limit
+    if (rope && elem_bytes != 2) return FLA_ERR_UNSUPPORTED;
+    if (rope)
+        for (int i = 0; i < n_grids; ++i)
+            if ((window < hw[2 * i] ? window : hw[2 * i]) > fla::kRopeMaxSide ||
+                (window < hw[2 * i + 1] ? window : hw[2 * i + 1]) > fla::kRopeMaxSide)
+                return FLA_ERR_UNSUPPORTED;
+    const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
     if (static_scratch) {
         if (need > fla::kScratchBytes) return FLA_ERR_SCRATCH;
     } else if (need > 0 && (!ws || ws_bytes < uint64_t(need))) {
@@ -347,12 +360,13 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.dk = dk;
     a.dv = dv;
     a.ws = static_cast<float*>(ws);
-    a.ws_dq = dq_shares ? a.ws + pad_partial_bytes(B, heads, pr.geo, pad_mode) / 4 : nullptr;
+    a.pad_blocks = elem_bytes == 2 ? pr.geo.nbb : pr.geo.nqb;
+    a.nbb = pr.geo.nbb;
+    a.div_2nbb = fla::FastDiv::make(2u * (unsigned)pr.geo.nbb);
+    a.n_units = units;
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
     const hipStream_t s = stream;
-    hipError_t e = elem_bytes != 2 ? fla::launch_swin_bwd_f32(a, s)
-                   : wide         ? fla::launch_swin_bwd_bf16_wide(a, s)
-                                  : fla::launch_swin_bwd_bf16(a, s);
+    hipError_t e = elem_bytes != 2 ? fla::launch_swin_bwd_f32(a, s) : fla::launch_swin_bwd_bf16(a, s);
     if (e == hipSuccess && pad_mode == FLA_PAD_KVTOKEN) e = fla::launch_swin_bwd_pad_reduce(a, elem_bytes, s);
     if (e != hipSuccess) {
         (void)hipGetLastError();
@@ -531,7 +545,7 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
     Problem pr;
     st = check_limits(B, heads, n_grids, grid_hw, fla::kHeadDim, window, shift, pad_mode, 2, &pr);
     if (st != FLA_OK) return st;
-    *bytes = (size_t)workspace_bytes(B, heads, pr.geo, pad_mode, pr.geo.nqb > 1);
+    *bytes = (size_t)workspace_bytes(B, heads, pr.geo, pad_mode);
     return FLA_OK;
 }
 
@@ -590,11 +604,11 @@ const char* fla_status_string(int status) {
         case FLA_ERR_WINDOW: return "window must be >= 1";
         case FLA_ERR_SHIFT: return "shift must satisfy 0 <= shift < window";
         case FLA_ERR_PAD_MODE: return "pad_mode must be FLA_PAD_MASK (0) or FLA_PAD_KVTOKEN (1)";
-        case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements, 2^24 workgroups or a 2 GiB window span)";
+        case FLA_ERR_TOO_LARGE: return "problem too large (2^40 elements, 2^23 workgroups or a 2 GiB window span)";
         case FLA_ERR_ALIAS: return "an output overlaps an input or another output";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";
-        case FLA_ERR_UNSUPPORTED: return "window too large for this bf16 entry point (RoPE backward: 256 tokens; RoPE forward: 32 x 32)";
+        case FLA_ERR_UNSUPPORTED: return "window too large for the bf16 RoPE entry points (32 x 32), or RoPE training in fp32";
         case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
         case FLA_ERR_ROPE: return "rope_theta must be finite and > 0, rope_scale finite";
         case FLA_ERR_SCRATCH: return "problem needs more workspace than the 16 MiB static scratch of the allocation-free backward";

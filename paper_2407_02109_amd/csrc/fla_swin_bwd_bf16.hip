@@ -5,69 +5,74 @@
 // and D_i = <dO_i, O_i>:
 //   P = exp(c Q K^T - LSE),  dP = dO V^T,  dS = P o (dP - D)
 //   dV = P^T dO,  dK = c dS^T Q,  dQ = c dS K
-// P is recomputed, never stored.  A window of window <= 16 has at most 256 tokens, so one
-// workgroup takes a whole (batch entry, window, head) and no gradient leaves it half done.
-// Wider windows take swin_bwd_bf16_wide_kernel (further down): the same steps per key
-// block of 256, with the queries streamed in chunks and dq summed over the key blocks by
-// a second kernel.
+// P is recomputed, never stored.
 //
-// Per workgroup (512 threads = 8 waves):
-//   1. Q and dO rows of the window -> LDS (row-major, 144-byte rows); LSE and D per query
-//      -> LDS (D from the dO and O rows as they arrive).  Wave w owns keys [32w, 32w + 32):
-//      its K and V rows stay in registers as MFMA operands, and K also as K^T, obtained
-//      once through LDS with the gfx950 transposing read (ds_read_b64_tr_b16).
-//   2. Steps t = 0 .. nt-1 (nt = ceil(n / 32) query tiles = key tiles): wave w works on
-//      query tile (w + t) mod nt, so at every step each tile belongs to exactly one wave.
-//        S = Q K_w^T and dP = dO V_w^T      (v_mfma_f32_32x32x16_bf16, fp32 accumulation;
-//                                             each lane holds one key and 16 queries)
-//        P = exp2(S c log2(e) - LSE log2(e)), dS = P (dP - D) in fp32, rounded to bf16
-//        dV_w^T += dO^T P,  dK_w^T += Q^T dS  (dO^T and Q^T come straight from the LDS
-//                                             rows by transposing reads)
-//        dQ^T += K_w^T dS^T                   (dS goes through a per-wave LDS scratch to
-//                                             put queries on the lanes)
-//      The matrix cores do the bookkeeping adds as well: keys past the window's end get -inf
-//      through the C operand of S (so P = 0), -D enters as the C operand of dP, and the tile's
-//      fp32 dQ^T accumulator in LDS is read into the C operand of the dQ^T product and
-//      written back (stored at step 0).  Since no two waves share a tile within a step, one
-//      barrier per step orders the updates and the sum order is fixed.
-//   3. Epilogue: scale, round to bf16 (RNE), stage each wave's 32 rows of dK, dV and dQ in
-//      LDS and store whole 128-byte rows at their own tokens.
+// One launch, two kinds of workgroup (256 threads = 4 waves) per (batch entry, window,
+// block of 128 tokens, head):
+//   * key role: owns 128 keys of the window.  Wave w keeps the K and V rows of keys
+//     32w .. 32w + 31 in registers (MFMA B operands) and accumulates their dK^T and dV^T
+//     in registers, while the window's queries stream through LDS in chunks of 128 (Q and
+//     dO rows, -D and LSE log2(e) per query).  Per 32-query tile:
+//        S = Q K_w^T, dP - D = dO V_w^T - D        (C operand -D)
+//        P = exp2(S c log2(e) - LSE log2(e)), dS = P (dP - D), both rounded to bf16
+//        dV_w^T += dO^T P, dK_w^T += Q^T dS       (dO^T, Q^T by the transposing LDS read)
+//   * query role: owns 128 queries.  Wave w keeps the Q and dO rows of queries 32w .. + 31
+//     in registers (B operands), their LSE and D in one register each (a lane holds one
+//     query), and accumulates their dQ^T in registers, while the window's keys stream
+//     through LDS in chunks of 128 (K and V rows).  Per 32-key tile:
+//        S^T = K Q_w^T, dP^T - D = V dO_w^T - D
+//        dS^T = P^T o (dP^T - D) in fp32, rounded to bf16
+//        dQ_w^T += K^T dS^T                        (K^T by the transposing LDS read)
+// No accumulator is shared between waves, so the tile loops run without barriers, and a
+// workgroup needs 39 KB of LDS and at most 168 VGPRs: three workgroups (three waves per
+// SIMD) share a compute unit, and one's loads run under the others' products.  All the
+// workgroups of one (batch entry, window, head) -- both roles of every block -- get ids
+// that are equal mod 8, which the dispatcher sends to one XCD one after the other, so the
+// window's rows come from HBM once and the other readers find them in that XCD's L2.
 //
-// RoPE (Sec. 3.1; the training form of the forward's prologue fusion): q and K rows are
-// rotated as they are loaded, and dq, dk are rotated back (the transpose) before rounding;
-// the pad token is never rotated.
+// Keys past the window's end are zero rows in LDS (query role): their dS multiplies a zero
+// K row, and the one partial key tile of a chunk clears their P as well, so no infinity can
+// reach the products.  Rows past a window's end are never stored.
+//
+// RoPE (Sec. 3.1; the training form of the forward's prologue fusion): q and k are rotated
+// as they are loaded, and dq, dk are rotated back (the transpose) before rounding; the pad
+// token is never rotated.
 //
 // KV-only padding (Sec. 3.4, App. B): the pad token is one more key of weight n_pad per
-// query.  Its terms are rank one per query, so they are done during staging: its dS joins
-// dQ in the epilogue, and the workgroup's share of the pad token's own gradient goes to
-// the workspace, which a small kernel sums over the windows in a fixed order.
+// query.  Its terms are rank one per query: the query role adds dS_p k_p to dQ, and key
+// block 0's key role sums the pad token's own gradient over the window's queries (P_p and
+// dS_p per query in LDS, then one column sum per channel) into the workspace, which a small
+// kernel sums over the windows in a fixed order.
 #include "fla_swin_device.h"
 
 namespace fla {
 namespace {
 
 constexpr int D = kHeadDim;            // 64 channels
-constexpr int THREADS = 512;
-constexpr int NW = 8;                  // waves
-constexpr int TL = 32;                 // keys per wave = queries per tile
-constexpr int NMAX = kBwdMaxTokens;    // 256 = NW * TL
-constexpr int RS = D + 8;              // bf16 stride of Q / dO / staging rows (144 B)
-constexpr int SS = TL + 4;             // bf16 stride of the dS^T scratch rows (72 B)
+constexpr int THREADS = 256;
+constexpr int NW = 4;                  // waves
+constexpr int TL = 32;                 // keys (key role) or queries (query role) per wave
+constexpr int NMAX = kBwdBlock;        // 128 = NW * TL tokens per block and per chunk
+constexpr int RPP = THREADS / 8;       // rows staged per pass, 8 threads per 128-byte row
+constexpr int RS = D + 8;              // bf16 stride of staged rows (144 B)
+static_assert(NW * TL == NMAX && NMAX % RPP == 0, "block geometry");
 constexpr float kLog2e = 1.4426950408889634f;
 
-// LDS carve-up, bytes
-constexpr int OFF_Q = 0;                               // Q rows       [256][RS] bf16
-constexpr int OFF_DO = OFF_Q + NMAX * RS * 2;          // dO rows      [256][RS] bf16
-constexpr int OFF_DQ = OFF_DO + NMAX * RS * 2;         // dQ^T accumulators, [tile][8][64] float4
-constexpr int OFF_LSE = OFF_DQ + NMAX * D * 4;         // LSE * log2(e) [256] fp32
-constexpr int OFF_DD = OFF_LSE + NMAX * 4;             // D            [256] fp32
-constexpr int OFF_DSP = OFF_DD + NMAX * 4;             // pad-token dS [256] fp32
-constexpr int OFF_KP = OFF_DSP + NMAX * 4;             // pad-token key row [64] fp32
-constexpr int OFF_DST = OFF_KP + D * 4;                // dS^T scratch [wave][32][SS] bf16
-constexpr int LDS_BYTES = OFF_DST + NW * TL * SS * 2;
-static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
-static_assert(NW * TL * RS * 2 <= NMAX * D * 4, "K staging fits in the dQ area");
-static_assert(NW * kPadPartial * 4 <= NW * TL * SS * 2, "pad partials fit in the dS^T scratch");
+// LDS carve-up, bytes.  Key role: A = Q rows, B = dO rows of the query chunk, L and ND per
+// query; pad token: its k and v rows (PADKV), PP and DSP (its P and dS per query of the
+// chunk) and PADW (two half sums per channel of its gradient).  Query role: A = K rows, B = V rows of the key chunk,
+// the pad token's key row in PADW; A stages the dQ rows at the end.
+constexpr int OFF_A = 0;                              // [128][RS] bf16
+constexpr int OFF_B = OFF_A + NMAX * RS * 2;          // [128][RS] bf16
+constexpr int OFF_L = OFF_B + NMAX * RS * 2;          // LSE * log2(e) [128] fp32
+constexpr int OFF_ND = OFF_L + NMAX * 4;              // -D [128] fp32
+constexpr int OFF_PP = OFF_ND + NMAX * 4;             // [128] fp32
+constexpr int OFF_DSP = OFF_PP + NMAX * 4;            // [128] fp32
+constexpr int OFF_PADW = OFF_DSP + NMAX * 4;          // [2][128] fp32
+constexpr int OFF_PADKV = OFF_PADW + 2 * kPadPartial * 4;   // pad token's k then v row, [128] bf16
+constexpr int LDS_BYTES = OFF_PADKV + kPadPartial * 2;
+static_assert(3 * LDS_BYTES <= 160 * 1024, "three workgroups per compute unit");
+static_assert(THREADS == 2 * kPadPartial, "two threads per pad-gradient channel");
 
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
@@ -76,7 +81,9 @@ typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 // rows row0 + 4 * (l >> 5) + {0..3} and row0 + 8 + 4 * (l >> 5) + {0..3} of a row-major
 // bf16 array with row stride `stride`.  Within each 16-lane group, ds_read_b64_tr_b16 has
 // lane i name a 4-element piece (row i / 4, elements 4 * (i % 4) .. + 3) of a 4 x 16 block
-// and returns to lane i the block's column i.
+// and returns to lane i the block's column i.  The row order matches the rows a lane holds
+// in the accumulator of a 32 x 32 product, so that accumulator, rounded, is the other
+// operand of a product summed over those rows.
 __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* base, int stride, int row0, int col0, int lane) {
     const int e = (lane & 15) >> 2, q = lane & 3, g1 = (lane >> 4) & 1, h = lane >> 5;
     const uint16_t* p = base + (row0 + 4 * h + e) * stride + col0 + 16 * g1 + 4 * q;
@@ -94,6 +101,12 @@ __device__ __forceinline__ float dot8(const uint4& x, const uint4& y) {
     return s;
 }
 
+__device__ __forceinline__ float dot8(const bf16x8& a, const bf16x8& b, float s) {
+    for (int e = 0; e < 8; e += 2)
+        s = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{a[e], a[e + 1]}, bf16x2{b[e], b[e + 1]}, s, false);
+    return s;
+}
+
 // sum over the 8 lanes l, l ^ 1, ..., l ^ 7
 __device__ __forceinline__ float sum8(float x) {
     x += __shfl_xor(x, 1);
@@ -102,33 +115,17 @@ __device__ __forceinline__ float sum8(float x) {
     return x;
 }
 
-// One step of a wave: the query tile whose rows start at q0 (Q, dO rows, -D and LSE*log2(e)
-// in LDS) against the wave's 32 keys (kreg, vreg, kt in registers).  dK^T and dV^T add up in
-// registers; the tile's fp32 dQ^T accumulator in LDS (acc, lane-major, 8 float4 per lane)
-// is read (read_acc; else taken as zero), advanced by this step's product and written back.
-__device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dOs, const float* Ds, const float* Ls,
-                                          float4* acc, uint16_t* dst, const bf16x8 (&kreg)[4],
-                                          const bf16x8 (&vreg)[4], const bf16x8 (&kt)[2][2],
-                                          const floatx16& s_init, floatx16 (&dkT)[2], floatx16 (&dvT)[2], int q0,
-                                          bool read_acc, float c2, int lane) {
+// Key role, one tile: the 32 queries whose rows start at q0 (Q, dO rows, -D and LSE*log2(e)
+// in LDS) against the wave's 32 keys (kreg, vreg).  dK^T and dV^T add up in registers.
+__device__ __forceinline__ void key_tile(const uint16_t* Qs, const uint16_t* dOs, const float* ND, const float* Ls,
+                                         const bf16x8 (&kreg)[4], const bf16x8 (&vreg)[4], floatx16 (&dkT)[2],
+                                         floatx16 (&dvT)[2], int q0, float c2, int lane) {
     const int li = lane & 31, h = lane >> 5;
-    // the tile's dQ^T accumulator (written by earlier steps) becomes the C operand of
-    // this step's dQ^T product; fetched first so that the read is long done by then
-    floatx16 dq[2];
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        const float4 y = read_acc ? acc[g * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-        const int dh = g >> 2, i = g & 3;
-        dq[dh][4 * i] = y.x;
-        dq[dh][4 * i + 1] = y.y;
-        dq[dh][4 * i + 2] = y.z;
-        dq[dh][4 * i + 3] = y.w;
-    }
-    // dP - D in one go: the MFMA's C operand holds -D of each entry's query
-    floatx16 sacc = s_init, pacc;
+    // dP - D in one go: the C operand holds -D of each entry's query
+    floatx16 sacc = {}, pacc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const float4 d4 = *reinterpret_cast<const float4*>(Ds + q0 + 8 * i + 4 * h);
+        const float4 d4 = *reinterpret_cast<const float4*>(ND + q0 + 8 * i + 4 * h);
         pacc[4 * i] = d4.x;
         pacc[4 * i + 1] = d4.y;
         pacc[4 * i + 2] = d4.z;
@@ -138,10 +135,10 @@ __device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dO
     const uint16_t* grow = dOs + (q0 + li) * RS + 8 * h;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s),
-                                                      kreg[s], sacc, 0, 0, 0);
-        pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s),
-                                                      vreg[s], pacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(qrow + 16 * s), kreg[s],
+                                                      sacc, 0, 0, 0);
+        pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(grow + 16 * s), vreg[s],
+                                                      pacc, 0, 0, 0);
     }
     // entry r: query q0 + 8 (r / 4) + 4 h + r % 4, the wave's key li
     bf16x8 pb[2], sb[2];
@@ -153,12 +150,10 @@ __device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dO
         for (int j = 0; j < 4; ++j) {
             const int r = 4 * i + j;
             const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -lv[j]));
-            const float ds = p * pacc[r];
             pb[i >> 1][4 * (i & 1) + j] = (__bf16)p;
-            sb[i >> 1][4 * (i & 1) + j] = (__bf16)ds;
+            sb[i >> 1][4 * (i & 1) + j] = (__bf16)(p * pacc[r]);
         }
     }
-    // dV^T += dO^T P, dK^T += Q^T dS
 #pragma unroll
     for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
@@ -168,243 +163,252 @@ __device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dO
             dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
             dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
         }
-    // dS^T -> scratch (row = key li, 4 consecutive queries per write)
+}
+
+// Query role, one tile: the 32 keys whose rows start at k0 (K, V rows in LDS) against the
+// wave's 32 queries (qreg, greg; one query per lane column with its -D and LSE*log2(e)).
+// dQ^T adds up in registers.  MASKED: keys k0 + j with j >= nvalid get P = 0.
+template <bool MASKED>
+__device__ __forceinline__ void query_tile(const uint16_t* Ks, const uint16_t* Vs, const bf16x8 (&qreg)[4],
+                                           const bf16x8 (&greg)[4], float nd, float l2, floatx16 (&dqT)[2],
+                                           int k0, int nvalid, float c2, int lane) {
+    const int li = lane & 31, h = lane >> 5;
+    floatx16 sacc = {}, pacc;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
-            bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
-                   sb[i >> 1][4 * (i & 1) + 3]};
-    asm volatile("" ::: "memory");   // the scratch reads below follow these writes
-    // dQ^T += K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
+    for (int r = 0; r < 16; ++r) pacc[r] = nd;
+    const uint16_t* krow = Ks + (k0 + li) * RS + 8 * h;
+    const uint16_t* vrow = Vs + (k0 + li) * RS + 8 * h;
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-        const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
+    for (int s = 0; s < 4; ++s) {
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * s), qreg[s],
+                                                      sacc, 0, 0, 0);
+        pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(vrow + 16 * s), greg[s],
+                                                      pacc, 0, 0, 0);
+    }
+    // entry r: key k0 + 8 (r / 4) + 4 h + r % 4, the lane's query li
+    bf16x8 sb[2];
 #pragma unroll
-        for (int dh = 0; dh < 2; ++dh)
-            dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
+    for (int r = 0; r < 16; ++r) {
+        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[r], c2, -l2));
+        if (MASKED && 8 * (r >> 2) + 4 * h + (r & 3) >= nvalid) p = 0.f;
+        sb[r >> 3][r & 7] = (__bf16)(p * pacc[r]);
     }
 #pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        const int dh = g >> 2, i = g & 3;
-        acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh)
+            dqT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_operand(Ks, RS, k0 + 16 * s2, 32 * dh, lane), sb[s2],
+                                                             dqT[dh], 0, 0, 0);
+}
+
+// What both roles know about their block.
+struct Block {
+    int b, win, blk, head;
+    WindowRect wr;
+    int n;                      // tokens of the window
+    long long n_pad;            // virtual key slots of its canvas square (KV-token mode)
+    WindowAddr addr;
+    __amdgpu_buffer_rsrc_t qr, orr, dor, kr, vr, lr;
+};
+
+// (row, col) grid coordinates of window-local index t
+__device__ __forceinline__ void coords(const Block& k, int t, float& y, float& x) {
+    const unsigned r = __umulhi((unsigned)t, k.addr.magic) + ((unsigned)t & k.addr.one_mask);
+    y = (float)(k.wr.y0 + (int)r);
+    x = (float)(k.wr.x0 + (int)((unsigned)t - r * k.addr.cols));
+}
+
+// Key role: a query chunk's rows (rows r0 + RPP u of the 8-thread row groups, zero past the
+// chunk's nq rows) -> LDS: Q and dO rows, -D and LSE log2(e) per query.  Every load is issued
+// before the first LDS write.  With RoPE each thread then rotates its own pieces of the Q rows
+// in place (its LDS writes and reads stay in order), once the loaded registers are free.
+template <bool ROPE>
+__device__ __forceinline__ void key_stage(const SwinArgs& a, const Block& k, unsigned char* smem, int qbase, int nq) {
+    uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_A);
+    uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_B);
+    float* Ls = reinterpret_cast<float*>(smem + OFF_L);
+    float* ND = reinterpret_cast<float*>(smem + OFF_ND);
+    const int part = threadIdx.x & 7, r0 = threadIdx.x >> 3;
+    constexpr int NU = NMAX / RPP;
+    uint4 qv[NU], gv[NU], ov[NU];
+    float lse_raw[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+        const int r = r0 + RPP * u;
+        const unsigned off = r < nq ? k.addr(qbase + r) + 16 * part : kOutside;
+        qv[u] = bload16(k.qr, off);
+        gv[u] = bload16(k.dor, off);
+        ov[u] = bload16(k.orr, off);
+        lse_raw[u] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(
+                       k.lr, r < nq ? 4 * k.addr.token(qbase + r, (unsigned)k.wr.W) : kOutside, 0, 0));
+    }
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+        const int r = r0 + RPP * u;
+        *reinterpret_cast<uint4*>(Qs + r * RS + 8 * part) = qv[u];
+        *reinterpret_cast<uint4*>(dOs + r * RS + 8 * part) = gv[u];
+        const float dd = sum8(dot8(gv[u], ov[u]));
+        if (part == 0) {
+            ND[r] = -dd;
+            Ls[r] = lse_raw[u] * kLog2e;
+        }
+    }
+    if constexpr (ROPE) {
+#pragma unroll 1
+        for (int u = 0; u < NU; ++u) {
+            const int r = r0 + RPP * u;
+            float y, x;
+            coords(k, min(qbase + r, k.n - 1), y, x);
+            uint4* piece = reinterpret_cast<uint4*>(Qs + r * RS + 8 * part);
+            *piece = __builtin_bit_cast(uint4, rope_rotate_bf16x8(__builtin_bit_cast(bf16x8, *piece),
+                                                                  (part < 4 ? y : x) * a.rope_scale,
+                                                                  a.rope_rev + 4 * (part & 3)));
+        }
     }
 }
 
-template <bool MULTI, bool KVPAD, bool ROPE>
-__global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) {
-    const SwinArgs& a = ba.f;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
-    uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_Q);
-    uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_DO);
-    float4* DQ = reinterpret_cast<float4*>(smem + OFF_DQ);
-    float* Ls = reinterpret_cast<float*>(smem + OFF_LSE);
-    float* Ds = reinterpret_cast<float*>(smem + OFF_DD);
+// Key role, KV-token mode, after a chunk is staged: the pad token's P and dS per query, two
+// threads per row (32 channels each) from the staged Q and dO rows.
+__device__ __forceinline__ void key_pad_terms(const SwinArgs& a, unsigned char* smem, int nq, float log2_npad) {
+    const uint16_t* Qs = reinterpret_cast<const uint16_t*>(smem + OFF_A);
+    const uint16_t* dOs = reinterpret_cast<const uint16_t*>(smem + OFF_B);
+    const float* Ls = reinterpret_cast<const float*>(smem + OFF_L);
+    const float* ND = reinterpret_cast<const float*>(smem + OFF_ND);
+    float* PP = reinterpret_cast<float*>(smem + OFF_PP);
     float* DSP = reinterpret_cast<float*>(smem + OFF_DSP);
-    float* KP = reinterpret_cast<float*>(smem + OFF_KP);
-    uint16_t* DST = reinterpret_cast<uint16_t*>(smem + OFF_DST);
+    const uint16_t* PADKV = reinterpret_cast<const uint16_t*>(smem + OFF_PADKV);
+    static_assert(THREADS == 2 * NMAX, "two threads per staged row");
+    const int r = threadIdx.x >> 1, half = threadIdx.x & 1;
+    float zp = 0.f, dp = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = 32 * half + 8 * j;
+        zp = dot8(*reinterpret_cast<const bf16x8*>(Qs + r * RS + c), *reinterpret_cast<const bf16x8*>(PADKV + c), zp);
+        dp = dot8(*reinterpret_cast<const bf16x8*>(dOs + r * RS + c), *reinterpret_cast<const bf16x8*>(PADKV + D + c),
+                  dp);
+    }
+    zp += __shfl_xor(zp, 1);
+    dp += __shfl_xor(dp, 1);
+    // P = n_pad exp(c <q, k_pad> - LSE), dS = P (<dO, v_pad> - D)
+    const float p = r < nq ? __builtin_amdgcn_exp2f(__builtin_fmaf(zp, a.scale_log2, log2_npad - Ls[r])) : 0.f;
+    if (half == 0) {
+        PP[r] = p;
+        DSP[r] = p * (dp + ND[r]);
+    }
+}
 
-    // ---- workgroup -> (b, window, head), heads fastest
-    const unsigned id0 = blockIdx.x;
-    const unsigned id1 = a.div_heads.div(id0);
-    const int head = (int)(id0 - id1 * (unsigned)a.heads);
-    const unsigned id2 = a.div_nwin.div(id1);
-    const int win = (int)(id1 - id2 * (unsigned)a.n_windows);
-    const int b = (int)id2;
-
-    const WindowRect wr = window_rect<MULTI>(a, win);
-    const int n = wr.rows * wr.cols;          // 1 .. 256
-    const int nt = (n + TL - 1) / TL;
-    const long long n_pad = (long long)a.window * a.window - n;
-    const bool has_pad = KVPAD && n_pad > 0;
-
-    // ---- buffer resources at the window's first token, head `head`
-    const long long win_elems = wr.tok0 * a.tok_stride + head * D;
-    const long long q_base = (long long)b * a.q_batch_stride + win_elems;
-    const long long kv_base = (long long)b * a.kv_batch_stride + win_elems;
-    const long long q_bytes = ((long long)a.B * a.q_batch_stride - q_base) * 2;
-    const long long kv_bytes = ((long long)a.B * a.kv_batch_stride - kv_base) * 2;
-    const __amdgpu_buffer_rsrc_t qr = make_rsrc(static_cast<const uint16_t*>(a.q) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t orr = make_rsrc(static_cast<const uint16_t*>(ba.out) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t dor = make_rsrc(static_cast<const uint16_t*>(ba.dout) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t dqr = make_rsrc(static_cast<uint16_t*>(ba.dq) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t kr = make_rsrc(static_cast<const uint16_t*>(a.k) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t vr = make_rsrc(static_cast<const uint16_t*>(a.v) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t dkr = make_rsrc(static_cast<uint16_t*>(ba.dk) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t dvr = make_rsrc(static_cast<uint16_t*>(ba.dv) + kv_base, kv_bytes);
-    const long long lse_base = ((long long)b * a.heads + head) * a.L + wr.tok0;
-    const long long lse_total = (long long)a.B * a.heads * a.L;
-    const __amdgpu_buffer_rsrc_t lr = make_rsrc(ba.lse + lse_base, (lse_total - lse_base) * 4);
-
-    WindowAddr addr;
-    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
+template <bool KVPAD, bool ROPE>
+__device__ __forceinline__ void key_role(const SwinBwdArgs& ba, const Block& k, unsigned char* smem) {
+    const SwinArgs& a = ba.f;
+    uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_A);
+    uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_B);
+    float* Ls = reinterpret_cast<float*>(smem + OFF_L);
+    float* ND = reinterpret_cast<float*>(smem + OFF_ND);
+    float* PP = reinterpret_cast<float*>(smem + OFF_PP);
+    float* DSP = reinterpret_cast<float*>(smem + OFF_DSP);
+    float* PADW = reinterpret_cast<float*>(smem + OFF_PADW);
+    const int tid = threadIdx.x, lane = tid & 63, li = lane & 31, h = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int li = lane & 31;
-    const int h = lane >> 5;
+    const long long e = (((long long)k.b * a.heads + k.head) * a.n_windows + k.win) * ba.nbb + k.blk;
+    const int key0 = NMAX * k.blk;
+    if (key0 >= k.n) {   // the window has fewer blocks; its pad partial is still read
+        if (KVPAD && tid < kPadPartial) ba.ws[e * kPadPartial + tid] = 0.f;
+        return;
+    }
+    const int nkeys = min(NMAX, k.n - key0);
+    const int nkt = (nkeys + TL - 1) / TL;
+    const bool pad_here = KVPAD && k.n_pad > 0 && k.blk == 0;
 
-    // ---- 1. loads.  K_w and V_w rows: lane holds row 32 * wave + li, channels 16 s + 8 h .. + 7
-    //         (the B operand of S = Q K^T and dP = dO V^T).
+    // K_w and V_w rows: lane holds key key0 + 32 wave + li, channels 16 s + 8 h .. + 7
     const int key = TL * wave + li;
-    const bool key_ok = key < n;
-    const unsigned krow = key_ok ? addr(key) : kOutside;
+    const unsigned krow = key < nkeys ? k.addr(key0 + key) : kOutside;
     bf16x8 kreg[4], vreg[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        kreg[s] = __builtin_bit_cast(bf16x8, bload16(kr, krow + 32 * s + 16 * h));
-        vreg[s] = __builtin_bit_cast(bf16x8, bload16(vr, krow + 32 * s + 16 * h));
+        kreg[s] = __builtin_bit_cast(bf16x8, bload16(k.kr, krow + 32 * s + 16 * h));
+        vreg[s] = __builtin_bit_cast(bf16x8, bload16(k.vr, krow + 32 * s + 16 * h));
     }
-    // Q, dO, O: 8 threads per 128-byte row, rows r0 + 64 u
-    const int part = tid & 7;
-    const int r0 = tid >> 3;
-    uint4 qv[4], gv[4], ov[4];
-    float lse_raw[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int r = r0 + 64 * u;
-        const unsigned off = r < n ? addr(r) + 16 * part : kOutside;
-        qv[u] = bload16(qr, off);
-        gv[u] = bload16(dor, off);
-        ov[u] = bload16(orr, off);
-        lse_raw[u] = __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(lr, r < n ? 4 * addr.token(r, (unsigned)wr.W) : kOutside, 0, 0));
-    }
-    uint4 kp8 = {0u, 0u, 0u, 0u}, vp8 = {0u, 0u, 0u, 0u};
-    if (has_pad) {
-        const long long pad_elems = (long long)b * a.kv_batch_stride + a.L * a.tok_stride + head * D;
-        const __amdgpu_buffer_rsrc_t kpr = make_rsrc(static_cast<const uint16_t*>(a.k) + pad_elems, D * 2);
-        const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, D * 2);
-        kp8 = bload16(kpr, 16 * part);
-        vp8 = bload16(vpr, 16 * part);
-    }
-
-    // (row, col) grid coordinates of window-local index t
-    auto coords = [&](int t, float& y, float& x) {
-        const unsigned r = __umulhi((unsigned)t, addr.magic) + ((unsigned)t & addr.one_mask);
-        y = (float)(wr.y0 + (int)r);
-        x = (float)(wr.x0 + (int)((unsigned)t - r * addr.cols));
-    };
     if constexpr (ROPE) {
-        // RoPE on the loaded q rows (channels 8 part .. + 7: the row half for part < 4) and on
-        // the wave's K rows (channels 16 s + 8 h .. + 7); the pad token is not rotated
         float y, x;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            coords(min(r0 + 64 * u, n - 1), y, x);
-            qv[u] = __builtin_bit_cast(uint4, rope_rotate_bf16x8(__builtin_bit_cast(bf16x8, qv[u]),
-                                                                 (part < 4 ? y : x) * a.rope_scale,
-                                                                 a.rope_rev + 4 * (part & 3)));
-        }
-        coords(min(key, n - 1), y, x);
+        coords(k, min(key0 + key, k.n - 1), y, x);
 #pragma unroll
         for (int s = 0; s < 4; ++s)
             kreg[s] = rope_rotate_bf16x8(kreg[s], (s < 2 ? y : x) * a.rope_scale, a.rope_rev + 8 * (s & 1) + 4 * h);
     }
+    // pad token's key and value rows: loaded with the first chunk, kept in LDS (PADKV)
+    const int part = tid & 7;
+    uint4 padrow = {0u, 0u, 0u, 0u};
+    if (pad_here && tid < 16) {
+        const long long pad_elems = (long long)k.b * a.kv_batch_stride + a.L * a.tok_stride + k.head * D;
+        const __amdgpu_buffer_rsrc_t pr = make_rsrc(static_cast<const uint16_t*>(tid < 8 ? a.k : a.v) + pad_elems, D * 2);
+        padrow = bload16(pr, 16 * part);
+    }
+    float pad_sum = 0.f;   // thread (half, channel): its half of the chunk rows, over the chunks
+    const float c2 = a.scale_log2;
+    const float log2_npad = pad_here ? log2f((float)k.n_pad) : 0.f;
+    floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
 
-    // ---- LDS: rows, LSE, D; the wave's K rows into its staging area (in the dQ space)
-    float pk[8], pv[8];   // this thread's share of the pad token's gradient (8 channels)
-    for (int e = 0; e < 8; ++e) pk[e] = pv[e] = 0.f;
+    const int nqc = (k.n + NMAX - 1) / NMAX;
+    for (int qc = 0; qc < nqc; ++qc) {
+        const int qbase = NMAX * qc;
+        const int nq = min(NMAX, k.n - qbase);
+        const int nqt = (nq + TL - 1) / TL;
+        if (qc > 0) __syncthreads();   // every wave is done with the previous chunk's rows
+        // ---- the chunk's Q, dO rows -> LDS, -D and LSE log2(e) per query
+        key_stage<ROPE>(a, k, smem, qbase, nq);
+        if (pad_here && qc == 0 && tid < 16)
+            *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(smem + OFF_PADKV) + 8 * tid) = padrow;
+        __syncthreads();
+        if (pad_here) {
+            key_pad_terms(a, smem, nq, log2_npad);
+            __syncthreads();
+            // the pad token's gradient over this chunk's rows: thread (half, c) sums channel c of
+            // dS_p q (c < 64) or P_p dO (c >= 64) over rows half * 64 .. + 63, in row order
+            // (four interleaved partial sums, added in a fixed order: rows past nq have P = dS = 0)
+            const int c = tid & (kPadPartial - 1), half = tid / kPadPartial;
+            const float* w = c < D ? DSP : PP;
+            const uint16_t* col = (c < D ? Qs : dOs) + (c & (D - 1));
+            float acc4[4] = {0.f, 0.f, 0.f, 0.f};
+            const int r_begin = NMAX / 2 * half;
+#pragma unroll 4
+            for (int i = 0; i < NMAX / 2; i += 4)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int r = r0 + 64 * u;
-        *reinterpret_cast<uint4*>(Qs + r * RS + 8 * part) = qv[u];
-        *reinterpret_cast<uint4*>(dOs + r * RS + 8 * part) = gv[u];
-        const float dd = sum8(dot8(gv[u], ov[u]));
-        const float lse2 = lse_raw[u] * kLog2e;
-        if (part == 0) {
-            Ds[r] = -dd;   // stored negated: it is the C operand of dP - D
-            Ls[r] = lse2;
+                for (int j = 0; j < 4; ++j) {
+                    const int r = r_begin + i + j;
+                    acc4[j] = __builtin_fmaf(w[r], __uint_as_float((unsigned)col[r * RS] << 16), acc4[j]);
+                }
+            pad_sum += (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
         }
-        if (has_pad) {
-            // pad token as key: P = n_pad exp(c <q, k_pad> - LSE), dS = P (<dO, v_pad> - D)
-            const float zp = sum8(dot8(qv[u], kp8));
-            const float dp = sum8(dot8(gv[u], vp8));
-            const float p = r < n ? __builtin_amdgcn_exp2f(__builtin_fmaf(zp, a.scale_log2, log2f((float)n_pad) - lse2)) : 0.f;
-            const float ds = p * (dp - dd);
-            if (part == 0) DSP[r] = ds;
-            const bf16x8 q8 = __builtin_bit_cast(bf16x8, qv[u]), g8 = __builtin_bit_cast(bf16x8, gv[u]);
-            for (int e = 0; e < 8; ++e) {
-                pk[e] = __builtin_fmaf(ds, (float)q8[e], pk[e]);
-                pv[e] = __builtin_fmaf(p, (float)g8[e], pv[e]);
+        // ---- tiles: the wave's keys against each query tile of the chunk (starting at a
+        //      different tile per wave, to spread the LDS reads)
+        if (wave < nkt) {
+            int T = wave < nqt ? wave : wave % nqt;
+            for (int t = 0; t < nqt; ++t) {
+                key_tile(Qs, dOs, ND, Ls, kreg, vreg, dkT, dvT, TL * T, c2, lane);
+                T = T + 1 == nqt ? 0 : T + 1;
             }
         }
     }
-    if (has_pad) {
-        if (tid < 8) {
-            const bf16x8 k8 = __builtin_bit_cast(bf16x8, kp8);
-            for (int e = 0; e < 8; ++e) KP[8 * part + e] = (float)k8[e];
-        }
-        // sum over the 8 row groups of the wave (lanes part, part + 8, ...), then per wave to LDS
-        float* wsum = reinterpret_cast<float*>(DST) + wave * kPadPartial;
-        for (int e = 0; e < 8; ++e) {
-            float x = pk[e], y = pv[e];
-            x += __shfl_xor(x, 8);
-            x += __shfl_xor(x, 16);
-            x += __shfl_xor(x, 32);
-            y += __shfl_xor(y, 8);
-            y += __shfl_xor(y, 16);
-            y += __shfl_xor(y, 32);
-            if (lane < 8) {
-                wsum[8 * part + e] = x;
-                wsum[D + 8 * part + e] = y;
-            }
-        }
-    }
-    uint16_t* kstage = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * TL * RS;
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-        *reinterpret_cast<bf16x8*>(kstage + li * RS + 16 * s + 8 * h) = kreg[s];
-    __syncthreads();
+    if (pad_here) PADW[tid] = pad_sum;
+    __syncthreads();   // the rows are free for staging; the pad sums are complete
 
-    // K_w^T (A operand of dQ^T = K^T dS^T): lane row = channel 32 dh + li, keys along k
-    bf16x8 kt[2][2];
-#pragma unroll
-    for (int dh = 0; dh < 2; ++dh)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) kt[dh][s2] = tr_operand(kstage, RS, 16 * s2, 32 * dh, lane);
     if (KVPAD && tid < kPadPartial) {
-        // every workgroup writes its share (zero without virtual slots), so the reduction
-        // reads a dense array
-        float acc = 0.f;
-        if (has_pad) {
-            const float* wsum = reinterpret_cast<const float*>(DST);
-            for (int w = 0; w < NW; ++w) acc += wsum[w * kPadPartial + tid];
-        }
-        const long long e = ((long long)b * a.heads + head) * a.n_windows + win;
+        // every block writes its share (zero without virtual slots or past block 0), so the
+        // reduction reads a dense array
+        const float acc = pad_here ? PADW[tid] + PADW[kPadPartial + tid] : 0.f;
         ba.ws[e * kPadPartial + tid] = tid < D ? acc * ba.scale : acc;
     }
-    __syncthreads();
 
-    // ---- 2. steps
-    floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
-    uint16_t* dst = DST + wave * TL * SS;
-    const float c2 = a.scale_log2;
-    // C operand of S = Q K^T: 0, or -inf for a key past the window's last (its P is then 0)
-    floatx16 s_init;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s_init[r] = key_ok ? 0.f : -INFINITY;
-    for (int t = 0; t < nt; ++t) {
-        if (wave < nt) {
-            const int T = wave + t < nt ? wave + t : wave + t - nt;
-            wave_step(Qs, dOs, Ds, Ls, DQ + T * 8 * 64 + lane, dst, kreg, vreg, kt, s_init, dkT, dvT, TL * T, t > 0,
-                      c2, lane);
-        }
-        __syncthreads();
-    }
-
-    // ---- 3. epilogue: each wave stages its 32 key rows of dK and dV (in the Q and dO rows)
-    //         and its query tile of dQ (in that tile's accumulator space), then stores whole
-    //         128-byte rows, 8 lanes per row.
-    if (wave < nt) {
+    // ---- dK, dV of the wave's keys: stage its 32 rows in the Q and dO rows, store whole
+    //      128-byte rows, 8 lanes per row
+    if (wave < nkt) {
         const float sc = ba.scale;
-        uint16_t* krow_s = Qs + (TL * wave + li) * RS;
-        uint16_t* vrow_s = dOs + (TL * wave + li) * RS;
         if constexpr (ROPE) {
             // dk = R^T dk': this lane's key, channels 32 dh + 8 i + 4 h + {0..3} = pairs
             // 4 i + 2 h + {0, 1} of half dh
             float y, x;
-            coords(min(key, n - 1), y, x);
+            coords(k, min(key0 + key, k.n - 1), y, x);
 #pragma unroll
             for (int dh = 0; dh < 2; ++dh)
 #pragma unroll
@@ -417,286 +421,6 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_kernel(SwinBwdArgs ba) 
                         dkT[dh][4 * i + 2 * pr + 1] = p1;
                     }
         }
-#pragma unroll
-        for (int dh = 0; dh < 2; ++dh)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                bf16x4 k4, v4;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    k4[j] = (__bf16)(dkT[dh][4 * i + j] * sc);
-                    v4[j] = (__bf16)dvT[dh][4 * i + j];
-                }
-                *reinterpret_cast<bf16x4*>(krow_s + 32 * dh + 8 * i + 4 * h) = k4;
-                *reinterpret_cast<bf16x4*>(vrow_s + 32 * dh + 8 * i + 4 * h) = v4;
-            }
-        // dQ: this wave's tile is tile `wave`; read all of it before staging rows over it
-        const float4* acc = DQ + wave * 8 * 64 + lane;
-        float4 x[8];
-#pragma unroll
-        for (int g = 0; g < 8; ++g) x[g] = acc[g * 64];
-        asm volatile("" ::: "memory");
-        const int qi = TL * wave + li;
-        const float dsp = has_pad ? DSP[qi] : 0.f;
-        uint16_t* qrow_s = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * 8 * 64 * 8 + li * RS;
-        [[maybe_unused]] float qy = 0.f, qx = 0.f;
-        if constexpr (ROPE) coords(min(qi, n - 1), qy, qx);
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            const int ch = 32 * (g >> 2) + 8 * (g & 3) + 4 * h;
-            float v4[4] = {x[g].x, x[g].y, x[g].z, x[g].w};
-            bf16x4 o4;
-            if (has_pad)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) v4[j] = __builtin_fmaf(dsp, KP[ch + j], v4[j]);
-            if constexpr (ROPE) {
-                // dq = R^T dq': pairs (ch % 32) / 2 + {0, 1} of half ch / 32
-                const float pos = (ch < 32 ? qy : qx) * a.rope_scale;
-                rope_unrotate_pair(v4[0], v4[1], pos, a.rope_rev[(ch & 31) / 2]);
-                rope_unrotate_pair(v4[2], v4[3], pos, a.rope_rev[(ch & 31) / 2 + 1]);
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(v4[j] * sc);
-            *reinterpret_cast<bf16x4*>(qrow_s + ch) = o4;
-        }
-        asm volatile("" ::: "memory");   // staged rows are read back by other lanes
-        const uint16_t* qbase_s = reinterpret_cast<const uint16_t*>(smem + OFF_DQ) + wave * 8 * 64 * 8;
-        const int sp = lane & 7;
-#pragma unroll
-        for (int it = 0; it < TL / 8; ++it) {
-            const int rl = 8 * it + (lane >> 3);
-            const int tok = TL * wave + rl;
-            const unsigned off = tok < n ? addr(tok) + 16 * sp : kOutside;
-            const uint4 kx = *reinterpret_cast<const uint4*>(Qs + tok * RS + 8 * sp);
-            const uint4 vx = *reinterpret_cast<const uint4*>(dOs + tok * RS + 8 * sp);
-            const uint4 qx = *reinterpret_cast<const uint4*>(qbase_s + rl * RS + 8 * sp);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, kx), dkr, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, vx), dvr, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, qx), dqr, off, 0, 0);
-        }
-    }
-}
-
-// ---- windows of more than 256 tokens (window > 16 on grids that hold such a window)
-//
-// One workgroup per (batch entry, window, key block of 256 tokens, head).  The block's keys
-// stay with the waves as above (32 per wave, dK and dV accumulated in registers over the
-// whole window), and the window's queries stream through LDS in chunks of 256 with the same
-// step rotation, over max(query tiles, key tiles) steps so that the two counts may differ.
-// dQ of a chunk then holds only this key block's share: it goes, unscaled, to the workspace
-// as fp32, and swin_bwd_dq_reduce_kernel sums the key blocks' shares in block order,
-// scales by c and rounds once.  In KV-token mode key block 0 also takes the pad token's
-// per-query terms (its dS k_pad joins that block's dQ share).
-constexpr int OFF_PP = LDS_BYTES;                       // pad-token P  [256] fp32
-constexpr int WIDE_LDS_BYTES = OFF_PP + NMAX * 4;
-static_assert(WIDE_LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
-
-template <bool MULTI, bool KVPAD>
-__global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs ba) {
-    const SwinArgs& a = ba.f;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[WIDE_LDS_BYTES];
-    uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_Q);
-    uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_DO);
-    float4* DQ = reinterpret_cast<float4*>(smem + OFF_DQ);
-    float* Ls = reinterpret_cast<float*>(smem + OFF_LSE);
-    float* Ds = reinterpret_cast<float*>(smem + OFF_DD);
-    float* DSP = reinterpret_cast<float*>(smem + OFF_DSP);
-    float* KP = reinterpret_cast<float*>(smem + OFF_KP);
-    uint16_t* DST = reinterpret_cast<uint16_t*>(smem + OFF_DST);
-    float* PP = reinterpret_cast<float*>(smem + OFF_PP);
-
-    // ---- workgroup -> (b, window, key block, head), heads fastest
-    const unsigned id0 = blockIdx.x;
-    const unsigned id1 = a.div_heads.div(id0);
-    const int head = (int)(id0 - id1 * (unsigned)a.heads);
-    const unsigned id2 = a.div_nqb.div(id1);
-    const int kb = (int)(id1 - id2 * (unsigned)a.nqb);
-    const unsigned id3 = a.div_nwin.div(id2);
-    const int win = (int)(id2 - id3 * (unsigned)a.n_windows);
-    const int b = (int)id3;
-
-    const WindowRect wr = window_rect<MULTI>(a, win);
-    const int n = wr.rows * wr.cols;
-    const long long n_pad = (long long)a.window * a.window - n;
-    const int tid = threadIdx.x;
-    // this block's entries: pad-gradient partial and dQ share
-    const long long e = (((long long)b * a.heads + head) * a.n_windows + win) * a.nqb + kb;
-    const int key0 = NMAX * kb;
-    if (key0 >= n) {   // the window has fewer key blocks; its pad partial is still read
-        if (KVPAD && tid < kPadPartial) ba.ws[e * kPadPartial + tid] = 0.f;
-        return;
-    }
-    const int nkeys = min(NMAX, n - key0);
-    const int nkt = (nkeys + TL - 1) / TL;
-    const bool pad_here = KVPAD && n_pad > 0 && kb == 0;
-
-    const long long win_elems = wr.tok0 * a.tok_stride + head * D;
-    const long long q_base = (long long)b * a.q_batch_stride + win_elems;
-    const long long kv_base = (long long)b * a.kv_batch_stride + win_elems;
-    const long long q_bytes = ((long long)a.B * a.q_batch_stride - q_base) * 2;
-    const long long kv_bytes = ((long long)a.B * a.kv_batch_stride - kv_base) * 2;
-    const __amdgpu_buffer_rsrc_t qr = make_rsrc(static_cast<const uint16_t*>(a.q) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t orr = make_rsrc(static_cast<const uint16_t*>(ba.out) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t dor = make_rsrc(static_cast<const uint16_t*>(ba.dout) + q_base, q_bytes);
-    const __amdgpu_buffer_rsrc_t kr = make_rsrc(static_cast<const uint16_t*>(a.k) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t vr = make_rsrc(static_cast<const uint16_t*>(a.v) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t dkr = make_rsrc(static_cast<uint16_t*>(ba.dk) + kv_base, kv_bytes);
-    const __amdgpu_buffer_rsrc_t dvr = make_rsrc(static_cast<uint16_t*>(ba.dv) + kv_base, kv_bytes);
-    const long long lse_base = ((long long)b * a.heads + head) * a.L + wr.tok0;
-    const long long lse_total = (long long)a.B * a.heads * a.L;
-    const __amdgpu_buffer_rsrc_t lr = make_rsrc(ba.lse + lse_base, (lse_total - lse_base) * 4);
-
-    WindowAddr addr;
-    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
-
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int li = lane & 31;
-    const int h = lane >> 5;
-
-    // ---- K_w and V_w rows (B operands), lane: key key0 + 32 wave + li
-    const int key = TL * wave + li;
-    const bool key_ok = key < nkeys;
-    const unsigned krow = key_ok ? addr(key0 + key) : kOutside;
-    bf16x8 kreg[4], vreg[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        kreg[s] = __builtin_bit_cast(bf16x8, bload16(kr, krow + 32 * s + 16 * h));
-        vreg[s] = __builtin_bit_cast(bf16x8, bload16(vr, krow + 32 * s + 16 * h));
-    }
-    const int part = tid & 7;
-    const int r0 = tid >> 3;
-    // pad row (key block 0 in KV-token mode), read again per chunk so that it does not stay
-    // in registers through the steps
-    const long long pad_elems = (long long)b * a.kv_batch_stride + a.L * a.tok_stride + head * D;
-    const __amdgpu_buffer_rsrc_t kpr = make_rsrc(static_cast<const uint16_t*>(a.k) + pad_elems, pad_here ? D * 2 : 0);
-    const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, pad_here ? D * 2 : 0);
-    // K_w^T (A operand of dQ^T = K^T dS^T) through the staging rows in the dQ space
-    uint16_t* kstage = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * TL * RS;
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-        *reinterpret_cast<bf16x8*>(kstage + li * RS + 16 * s + 8 * h) = kreg[s];
-    if (pad_here && tid < 8) {
-        const bf16x8 k8 = __builtin_bit_cast(bf16x8, bload16(kpr, 16 * part));
-        for (int j = 0; j < 8; ++j) KP[8 * part + j] = (float)k8[j];
-    }
-    __syncthreads();
-    bf16x8 kt[2][2];
-#pragma unroll
-    for (int dh = 0; dh < 2; ++dh)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) kt[dh][s2] = tr_operand(kstage, RS, 16 * s2, 32 * dh, lane);
-    __syncthreads();   // the staging rows are the accumulators of the first chunk
-
-    // key block 0, KV-token mode: thread c < 64 sums channel c of the pad token's dk, thread
-    // 64 + c channel c of its dv, over the chunks
-    float pad_acc = 0.f;
-    floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
-    uint16_t* dst = DST + wave * TL * SS;
-    const float c2 = a.scale_log2;
-    // C operand of S = Q K^T: 0, or -inf for a key past the block's last (its P is then 0)
-    floatx16 s_init;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s_init[r] = key_ok ? 0.f : -INFINITY;
-    float* wsq = ba.ws_dq + e * ((long long)a.nqb * kQueryBlock * D);   // [query of the window][64]
-
-    const int nqc = (n + NMAX - 1) / NMAX;
-    for (int qc = 0; qc < nqc; ++qc) {
-        const int qbase = NMAX * qc;
-        const int nq = min(NMAX, n - qbase);
-        const int nqt = (nq + TL - 1) / TL;
-        // ---- the chunk's Q, dO, O rows (zero past its end) and LSE; zero accumulators
-        uint4 qv[4], gv[4], ov[4], kp8 = {0u, 0u, 0u, 0u}, vp8 = {0u, 0u, 0u, 0u};
-        if (pad_here) {
-            kp8 = bload16(kpr, 16 * part);
-            vp8 = bload16(vpr, 16 * part);
-        }
-        float lse_raw[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = r0 + 64 * u;
-            const unsigned off = r < nq ? addr(qbase + r) + 16 * part : kOutside;
-            qv[u] = bload16(qr, off);
-            gv[u] = bload16(dor, off);
-            ov[u] = bload16(orr, off);
-            lse_raw[u] = __builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(
-                           lr, r < nq ? 4 * addr.token(qbase + r, (unsigned)wr.W) : kOutside, 0, 0));
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) DQ[tid + THREADS * i] = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int r = r0 + 64 * u;
-            *reinterpret_cast<uint4*>(Qs + r * RS + 8 * part) = qv[u];
-            *reinterpret_cast<uint4*>(dOs + r * RS + 8 * part) = gv[u];
-            const float dd = sum8(dot8(gv[u], ov[u]));
-            const float lse2 = lse_raw[u] * kLog2e;
-            if (part == 0) {
-                Ds[r] = -dd;
-                Ls[r] = lse2;
-            }
-            if (pad_here) {
-                const float zp = sum8(dot8(qv[u], kp8));
-                const float dp = sum8(dot8(gv[u], vp8));
-                const float p = r < nq ? __builtin_amdgcn_exp2f(__builtin_fmaf(zp, c2, log2f((float)n_pad) - lse2))
-                                       : 0.f;
-                if (part == 0) {
-                    DSP[r] = p * (dp - dd);
-                    PP[r] = p;
-                }
-            }
-        }
-        __syncthreads();
-
-        // ---- steps: wave w takes query tile (w + t) mod M; with w < nkt <= M no two waves
-        //      share a tile within a step, and each wave meets every tile once
-        const int M = nqt > nkt ? nqt : nkt;
-        for (int t = 0; t < M; ++t) {
-            const int T = wave + t < M ? wave + t : wave + t - M;
-            if (wave < nkt && T < nqt)
-                wave_step(Qs, dOs, Ds, Ls, DQ + T * 8 * 64 + lane, dst, kreg, vreg, kt, s_init, dkT, dvT, TL * T,
-                          true, c2, lane);
-            __syncthreads();
-        }
-
-        // ---- this key block's dQ share of the chunk -> workspace, 16 lanes per 256-byte row;
-        //      accumulator entry (tile T, g, lane) holds query 32 T + (lane & 31), channels
-        //      32 (g >> 2) + 8 (g & 3) + 4 (lane >> 5) + {0..3}
-#pragma unroll
-        for (int it = 0; it < NMAX / 32; ++it) {
-            const int row = 32 * it + (tid >> 4);
-            const int ch = 4 * (tid & 15);
-            if (row < nq) {
-                float4 x = DQ[(row >> 5) * 8 * 64 + (4 * (ch >> 5) + ((ch & 31) >> 3)) * 64 + (row & 31) +
-                              32 * ((ch >> 2) & 1)];
-                if (pad_here) {
-                    const float d = DSP[row];
-                    x.x = __builtin_fmaf(d, KP[ch], x.x);
-                    x.y = __builtin_fmaf(d, KP[ch + 1], x.y);
-                    x.z = __builtin_fmaf(d, KP[ch + 2], x.z);
-                    x.w = __builtin_fmaf(d, KP[ch + 3], x.w);
-                }
-                *reinterpret_cast<float4*>(wsq + (long long)(qbase + row) * D + ch) = x;
-            }
-        }
-        // pad token's gradient over the chunk's queries (rows past the chunk have dS = P = 0):
-        // dk_pad += sum dS_p q, dv_pad += sum P_p dO, in row order
-        if (pad_here && tid < kPadPartial) {
-            const float* w = tid < D ? DSP : PP;
-            const uint16_t* col = (tid < D ? Qs : dOs) + (tid & (D - 1));
-            for (int r = 0; r < nq; ++r)
-                pad_acc = __builtin_fmaf(w[r], __uint_as_float((unsigned)col[r * RS] << 16), pad_acc);
-        }
-        __syncthreads();   // the next chunk overwrites rows, D, LSE, pad terms and accumulators
-    }
-
-    // ---- pad-gradient partial: key block 0's sums, zero from the others
-    if (KVPAD && tid < kPadPartial) ba.ws[e * kPadPartial + tid] = tid < D ? pad_acc * ba.scale : pad_acc;
-
-    // ---- dK, dV of the block's keys: stage each wave's 32 rows, store whole 128-byte rows
-    if (wave < nkt) {
-        const float sc = ba.scale;
         uint16_t* krow_s = Qs + (TL * wave + li) * RS;
         uint16_t* vrow_s = dOs + (TL * wave + li) * RS;
 #pragma unroll
@@ -712,12 +436,16 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs
                 *reinterpret_cast<bf16x4*>(krow_s + 32 * dh + 8 * i + 4 * h) = k4;
                 *reinterpret_cast<bf16x4*>(vrow_s + 32 * dh + 8 * i + 4 * h) = v4;
             }
-        asm volatile("" ::: "memory");   // staged rows are read back by other lanes
+        asm volatile("" ::: "memory");   // staged rows are read back by other lanes of the wave
+        const long long kv_base = (long long)k.b * a.kv_batch_stride + k.wr.tok0 * a.tok_stride + k.head * D;
+        const long long kv_bytes = ((long long)a.B * a.kv_batch_stride - kv_base) * 2;
+        const __amdgpu_buffer_rsrc_t dkr = make_rsrc(static_cast<uint16_t*>(ba.dk) + kv_base, kv_bytes);
+        const __amdgpu_buffer_rsrc_t dvr = make_rsrc(static_cast<uint16_t*>(ba.dv) + kv_base, kv_bytes);
         const int sp = lane & 7;
 #pragma unroll
         for (int it = 0; it < TL / 8; ++it) {
             const int rl = TL * wave + 8 * it + (lane >> 3);
-            const unsigned off = rl < nkeys ? addr(key0 + rl) + 16 * sp : kOutside;
+            const unsigned off = rl < nkeys ? k.addr(key0 + rl) + 16 * sp : kOutside;
             const uint4 kx = *reinterpret_cast<const uint4*>(Qs + rl * RS + 8 * sp);
             const uint4 vx = *reinterpret_cast<const uint4*>(dOs + rl * RS + 8 * sp);
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, kx), dkr, off, 0, 0);
@@ -726,57 +454,212 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_wide_kernel(SwinBwdArgs
     }
 }
 
-// dq of windows of more than 256 tokens: one workgroup per (batch entry, window, query block
-// of 256, head) sums the key blocks' fp32 shares of its queries in block order, scales by c,
-// rounds to bf16 once and stores whole rows (8 threads per 128-byte row).
-template <bool MULTI>
-__global__ __launch_bounds__(THREADS) void swin_bwd_dq_reduce_kernel(SwinBwdArgs ba) {
+template <bool KVPAD, bool ROPE>
+__device__ __forceinline__ void query_role(const SwinBwdArgs& ba, const Block& k, unsigned char* smem) {
     const SwinArgs& a = ba.f;
-    const unsigned id0 = blockIdx.x;
-    const unsigned id1 = a.div_heads.div(id0);
-    const int head = (int)(id0 - id1 * (unsigned)a.heads);
-    const unsigned id2 = a.div_nqb.div(id1);
-    const int qb = (int)(id1 - id2 * (unsigned)a.nqb);
-    const unsigned id3 = a.div_nwin.div(id2);
-    const int win = (int)(id2 - id3 * (unsigned)a.n_windows);
-    const int b = (int)id3;
-    const WindowRect wr = window_rect<MULTI>(a, win);
-    const int n = wr.rows * wr.cols;
-    const int q0 = NMAX * qb;
-    if (q0 >= n) return;
-    const int nq = min(NMAX, n - q0);
-    const int nkb = (n + NMAX - 1) / NMAX;
-    const long long q_base = (long long)b * a.q_batch_stride + wr.tok0 * a.tok_stride + head * D;
-    const __amdgpu_buffer_rsrc_t dqr =
-        make_rsrc(static_cast<uint16_t*>(ba.dq) + q_base, ((long long)a.B * a.q_batch_stride - q_base) * 2);
-    WindowAddr addr;
-    addr.init(wr.cols, (unsigned)((long long)wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
-    const long long blk = (long long)a.nqb * kQueryBlock * D;
-    const float* src0 = ba.ws_dq + ((((long long)b * a.heads + head) * a.n_windows + win) * a.nqb) * blk;
-    const int part = threadIdx.x & 7;
+    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + OFF_A);
+    uint16_t* Vs = reinterpret_cast<uint16_t*>(smem + OFF_B);
+    float* KP = reinterpret_cast<float*>(smem + OFF_PADW);
+    const int tid = threadIdx.x, lane = tid & 63, li = lane & 31, h = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int q0 = NMAX * k.blk;
+    if (q0 >= k.n) return;
+    const int nq = min(NMAX, k.n - q0);
+    const bool has_pad = KVPAD && k.n_pad > 0;
+
+    // Q_w and dO_w (B operands): lane holds query q0 + 32 wave + li, channels 16 s + 8 h .. + 7;
+    // O only for D = <dO, O>, and the query's LSE.  The first key chunk's loads go out with
+    // them; each later chunk's are issued before the tiles of the one before (kv, vv).
+    const int qi = TL * wave + li;
+    const bool q_ok = qi < nq;
+    const unsigned qrow = q_ok ? k.addr(q0 + qi) : kOutside;
+    const int part = tid & 7, r0 = tid >> 3;
+    const int nkc = (k.n + NMAX - 1) / NMAX;
+    uint4 kv[NMAX / RPP], vv[NMAX / RPP];
+    auto load_chunk = [&](int kbase) {
+        const int nk = min(NMAX, k.n - kbase);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int r = (threadIdx.x >> 3) + 64 * u;
-        if (r >= nq) break;
-        const float* src = src0 + (long long)(q0 + r) * D + 8 * part;
-        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-        for (int k = 0; k < nkb; ++k) {
-            const float4 y0 = *reinterpret_cast<const float4*>(src + k * blk);
-            const float4 y1 = *reinterpret_cast<const float4*>(src + k * blk + 4);
-            x0.x += y0.x;
-            x0.y += y0.y;
-            x0.z += y0.z;
-            x0.w += y0.w;
-            x1.x += y1.x;
-            x1.y += y1.y;
-            x1.z += y1.z;
-            x1.w += y1.w;
+        for (int u = 0; u < NMAX / RPP; ++u) {
+            const int r = r0 + RPP * u;
+            const unsigned off = r < nk ? k.addr(kbase + r) + 16 * part : kOutside;
+            kv[u] = bload16(k.kr, off);
+            vv[u] = bload16(k.vr, off);
         }
-        const float c = ba.scale;
-        const bf16x8 o = {(__bf16)(x0.x * c), (__bf16)(x0.y * c), (__bf16)(x0.z * c), (__bf16)(x0.w * c),
-                          (__bf16)(x1.x * c), (__bf16)(x1.y * c), (__bf16)(x1.z * c), (__bf16)(x1.w * c)};
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), dqr, addr(q0 + r) + 16 * part, 0, 0);
+    };
+    bf16x8 qreg[4], greg[4];
+    uint4 oreg[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        qreg[s] = __builtin_bit_cast(bf16x8, bload16(k.qr, qrow + 32 * s + 16 * h));
+        greg[s] = __builtin_bit_cast(bf16x8, bload16(k.dor, qrow + 32 * s + 16 * h));
+        oreg[s] = bload16(k.orr, qrow + 32 * s + 16 * h);
     }
+    load_chunk(0);
+    float dd = 0.f;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) dd = dot8(greg[s], __builtin_bit_cast(bf16x8, oreg[s]), dd);
+    const float l2 = __builtin_bit_cast(
+                         float, __builtin_amdgcn_raw_buffer_load_b32(
+                                    k.lr, q_ok ? 4 * k.addr.token(q0 + qi, (unsigned)k.wr.W) : kOutside, 0, 0)) *
+                     kLog2e;
+    dd = xhalf_sum(dd);
+    const float c2 = a.scale_log2;
+    [[maybe_unused]] float qy = 0.f, qx = 0.f;
+    if constexpr (ROPE) {
+        coords(k, min(q0 + qi, k.n - 1), qy, qx);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+            qreg[s] = rope_rotate_bf16x8(qreg[s], (s < 2 ? qy : qx) * a.rope_scale, a.rope_rev + 8 * (s & 1) + 4 * h);
+    }
+    // pad token as key: dS_p = n_pad exp(c <q, k_pad> - LSE) (<dO, v_pad> - D); dq gets dS_p k_pad
+    float dsp = 0.f;
+    if (has_pad) {
+        const long long pad_elems = (long long)k.b * a.kv_batch_stride + a.L * a.tok_stride + k.head * D;
+        const __amdgpu_buffer_rsrc_t kpr = make_rsrc(static_cast<const uint16_t*>(a.k) + pad_elems, D * 2);
+        const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, D * 2);
+        float zp = 0.f, dp = 0.f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            zp = dot8(qreg[s], __builtin_bit_cast(bf16x8, bload16(kpr, 32 * s + 16 * h)), zp);
+            dp = dot8(greg[s], __builtin_bit_cast(bf16x8, bload16(vpr, 32 * s + 16 * h)), dp);
+        }
+        zp = xhalf_sum(zp);
+        dp = xhalf_sum(dp);
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(zp, c2, log2f((float)k.n_pad) - l2));
+        dsp = p * (dp - dd);
+        if (tid < 8) {
+            const bf16x8 k8 = __builtin_bit_cast(bf16x8, bload16(kpr, 16 * tid));
+            for (int j = 0; j < 8; ++j) KP[8 * tid + j] = (float)k8[j];
+        }
+    }
+    const float nd = -dd;
+
+    floatx16 dqT[2] = {floatx16{}, floatx16{}};
+    for (int kc = 0; kc < nkc; ++kc) {
+        const int kbase = NMAX * kc;
+        const int nk = min(NMAX, k.n - kbase);
+        const int nkt = (nk + TL - 1) / TL;
+        // ---- the chunk's K, V rows (zero past its end) -> LDS, 8 threads per row
+        if (kc > 0) __syncthreads();   // every wave is done with the previous chunk's rows
+#pragma unroll
+        for (int u = 0; u < NMAX / RPP; ++u) {
+            const int r = r0 + RPP * u;
+            if constexpr (ROPE) {
+                float y, x;
+                coords(k, min(kbase + r, k.n - 1), y, x);
+                kv[u] = __builtin_bit_cast(uint4, rope_rotate_bf16x8(__builtin_bit_cast(bf16x8, kv[u]),
+                                                                     (part < 4 ? y : x) * a.rope_scale,
+                                                                     a.rope_rev + 4 * (part & 3)));
+            }
+            *reinterpret_cast<uint4*>(Ks + r * RS + 8 * part) = kv[u];
+            *reinterpret_cast<uint4*>(Vs + r * RS + 8 * part) = vv[u];
+        }
+        if (kc + 1 < nkc) load_chunk(kbase + NMAX);   // in flight during this chunk's tiles
+        __syncthreads();
+        // ---- tiles: the wave's queries against each key tile of the chunk; only a partial
+        //      last tile masks its missing keys
+        if (TL * wave < nq) {
+            const int full = nk / TL;
+            int T = wave < full ? wave : (full > 0 ? wave % full : 0);
+            for (int t = 0; t < full; ++t) {
+                query_tile<false>(Ks, Vs, qreg, greg, nd, l2, dqT, TL * T, TL, c2, lane);
+                T = T + 1 == full ? 0 : T + 1;
+            }
+            if (full < nkt) query_tile<true>(Ks, Vs, qreg, greg, nd, l2, dqT, TL * full, nk - TL * full, c2, lane);
+        }
+    }
+    __syncthreads();   // the K rows are free for staging
+
+    // ---- dQ of the wave's queries: + dS_p k_pad, rotate back, scale, round; stage the 32 rows
+    //      in the K rows and store whole 128-byte rows, 8 lanes per row.  dqT[dh] entry r:
+    //      channel 32 dh + 8 (r / 4) + 4 h + r % 4 of the lane's query.
+    if (TL * wave < nq) {
+        const float sc = ba.scale;
+        uint16_t* row_s = Ks + (TL * wave + li) * RS;
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int ch = 32 * dh + 8 * i + 4 * h;
+                float v4[4] = {dqT[dh][4 * i], dqT[dh][4 * i + 1], dqT[dh][4 * i + 2], dqT[dh][4 * i + 3]};
+                if (has_pad)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v4[j] = __builtin_fmaf(dsp, KP[ch + j], v4[j]);
+                if constexpr (ROPE) {
+                    // dq = R^T dq': pairs (ch % 32) / 2 + {0, 1} of half dh
+                    const float pos = (dh == 0 ? qy : qx) * a.rope_scale;
+                    rope_unrotate_pair(v4[0], v4[1], pos, a.rope_rev[4 * i + 2 * h]);
+                    rope_unrotate_pair(v4[2], v4[3], pos, a.rope_rev[4 * i + 2 * h + 1]);
+                }
+                bf16x4 o4;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(v4[j] * sc);
+                *reinterpret_cast<bf16x4*>(row_s + ch) = o4;
+            }
+        asm volatile("" ::: "memory");   // staged rows are read back by other lanes of the wave
+        const long long q_base = (long long)k.b * a.q_batch_stride + k.wr.tok0 * a.tok_stride + k.head * D;
+        const __amdgpu_buffer_rsrc_t dqr =
+            make_rsrc(static_cast<uint16_t*>(ba.dq) + q_base, ((long long)a.B * a.q_batch_stride - q_base) * 2);
+        const int sp = lane & 7;
+#pragma unroll
+        for (int it = 0; it < TL / 8; ++it) {
+            const int rl = TL * wave + 8 * it + (lane >> 3);
+            const unsigned off = rl < nq ? k.addr(q0 + rl) + 16 * sp : kOutside;
+            const uint4 qx4 = *reinterpret_cast<const uint4*>(Ks + rl * RS + 8 * sp);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, qx4), dqr, off, 0, 0);
+        }
+    }
+}
+
+// Workgroup id -> (unit, role, block), unit = (batch entry, window, head): the 2 nbb
+// workgroups of unit u (both roles of each of its nbb blocks) get ids
+// 8 (2 nbb (u / 8) + j) + u % 8, j = 2 block + role, all on XCD u % 8 and dispatched
+// one after the other there.  Units are numbered heads fastest, then windows, then batch
+// entries.
+template <bool MULTI, bool KVPAD, bool ROPE>
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(3, 3)))
+void swin_bwd_bf16_kernel(SwinBwdArgs ba) {
+    const SwinArgs& a = ba.f;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+    const unsigned id = blockIdx.x;
+    const unsigned rest = id >> 3;
+    const unsigned g = ba.div_2nbb.div(rest);
+    const unsigned j = rest - g * (2u * (unsigned)ba.nbb);
+    const unsigned unit = (g << 3) + (id & 7u);
+    if (unit >= (unsigned)ba.n_units) return;
+    const bool query = j & 1u;
+
+    Block k;
+    k.blk = (int)(j >> 1);
+    const unsigned i2 = a.div_heads.div(unit);
+    k.head = (int)(unit - i2 * (unsigned)a.heads);
+    const unsigned i3 = a.div_nwin.div(i2);
+    k.win = (int)(i2 - i3 * (unsigned)a.n_windows);
+    k.b = (int)i3;
+    k.wr = window_rect<MULTI>(a, k.win);
+    k.n = k.wr.rows * k.wr.cols;
+    k.n_pad = (long long)a.window * a.window - k.n;
+
+    // buffer resources at the window's first token, head `head`
+    const long long win_elems = k.wr.tok0 * a.tok_stride + k.head * D;
+    const long long q_base = (long long)k.b * a.q_batch_stride + win_elems;
+    const long long kv_base = (long long)k.b * a.kv_batch_stride + win_elems;
+    const long long q_bytes = ((long long)a.B * a.q_batch_stride - q_base) * 2;
+    const long long kv_bytes = ((long long)a.B * a.kv_batch_stride - kv_base) * 2;
+    k.qr = make_rsrc(static_cast<const uint16_t*>(a.q) + q_base, q_bytes);
+    k.orr = make_rsrc(static_cast<const uint16_t*>(ba.out) + q_base, q_bytes);
+    k.dor = make_rsrc(static_cast<const uint16_t*>(ba.dout) + q_base, q_bytes);
+    k.kr = make_rsrc(static_cast<const uint16_t*>(a.k) + kv_base, kv_bytes);
+    k.vr = make_rsrc(static_cast<const uint16_t*>(a.v) + kv_base, kv_bytes);
+    const long long lse_base = ((long long)k.b * a.heads + k.head) * a.L + k.wr.tok0;
+    const long long lse_total = (long long)a.B * a.heads * a.L;
+    k.lr = make_rsrc(ba.lse + lse_base, (lse_total - lse_base) * 4);
+    k.addr.init(k.wr.cols, (unsigned)((long long)k.wr.W * a.tok_stride * 2), (unsigned)(a.tok_stride * 2));
+
+    if (query)
+        query_role<KVPAD, ROPE>(ba, k, smem);
+    else
+        key_role<KVPAD, ROPE>(ba, k, smem);
 }
 
 }  // namespace
@@ -794,24 +677,7 @@ hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream) {
                          : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<true, false, false>))
                    : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, true, false>)
                          : reinterpret_cast<const void*>(&swin_bwd_bf16_kernel<false, false, false>));
-    const long long groups = (long long)a.f.B * a.f.heads * a.f.n_windows;
-    return hipLaunchKernel(fn, dim3((unsigned)groups), dim3(THREADS), params, 0, stream);
-}
-
-hipError_t launch_swin_bwd_bf16_wide(const SwinBwdArgs& a, hipStream_t stream) {
-    SwinBwdArgs args = a;
-    void* params[] = {&args};
-    const bool multi = a.f.n_grids > 1, kv = a.f.pad_mode == 1;
-    const void* fn = multi ? (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<true, true>)
-                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<true, false>))
-                           : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<false, true>)
-                                 : reinterpret_cast<const void*>(&swin_bwd_bf16_wide_kernel<false, false>));
-    const dim3 grid((unsigned)a.f.n_groups);
-    hipError_t e = hipLaunchKernel(fn, grid, dim3(THREADS), params, 0, stream);
-    if (e != hipSuccess) return e;
-    const void* red = multi ? reinterpret_cast<const void*>(&swin_bwd_dq_reduce_kernel<true>)
-                            : reinterpret_cast<const void*>(&swin_bwd_dq_reduce_kernel<false>);
-    return hipLaunchKernel(red, grid, dim3(THREADS), params, 0, stream);
+    return hipLaunchKernel(fn, dim3((unsigned)bwd_bf16_groups(a.n_units, a.nbb)), dim3(THREADS), params, 0, stream);
 }
 
 }  // namespace fla

@@ -280,7 +280,7 @@ __global__ __launch_bounds__(kRedSlices * kPadPartial) void swin_bwd_pad_reduce_
     const int bh = blockIdx.x;
     const int col = threadIdx.x % kPadPartial;
     const int slice = threadIdx.x / kPadPartial;
-    const long long nent = (long long)a.n_windows * a.nqb;
+    const long long nent = (long long)a.n_windows * ba.pad_blocks;
     const float* src = ba.ws + (long long)bh * nent * kPadPartial + col;
     float acc = 0.f;
     for (long long e0 = slice; e0 < nent; e0 += (long long)kRedBatch * kRedSlices) {

@@ -83,18 +83,17 @@ struct SwinArgs {
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
-constexpr int kBwdMaxTokens = 256;   // window tokens one bf16 backward workgroup holds (window <= 16)
+constexpr int kBwdBlock = 128;    // tokens of one bf16 backward block (and of one streamed chunk)
 constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: dk then dv
 constexpr int kRopeMaxSide = 32;   // bf16 RoPE forward: window rows and columns it takes
 
 // Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
 // out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,
-// window, block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * nqb
+// window, block) in KV-token mode: ws[((b * heads + head) * n_windows + win) * pad_blocks
 // + blk][0:64] = dk part, [64:128] = dv part.  Every block writes its entry (zero when its
-// window has no virtual slots), and the pad reduce kernel sums them.  ws_dq (bf16 windows
-// of more than 256 tokens only) holds each key block's fp32 share of dq, unscaled:
-// ws_dq[(((b * heads + head) * n_windows + win) * nqb + kb) * nqb * 256 * 64 + t * 64 + ch]
-// for window-local query t.
+// window has no virtual slots), and the pad reduce kernel sums them.  The bf16 kernel's
+// blocks are kBwdBlock tokens (pad_blocks = nbb), the fp32 kernels' kQueryBlock tokens
+// (pad_blocks = f.nqb).
 struct SwinBwdArgs {
     SwinArgs f;
     const void* out;
@@ -104,13 +103,20 @@ struct SwinBwdArgs {
     void* dk;
     void* dv;
     float* ws;
-    float* ws_dq;
+    int pad_blocks;             // blocks per window in the layout of ws
+    int nbb;                    // bf16: kBwdBlock-token blocks of the largest window
+    FastDiv div_2nbb;           // bf16 workgroup decode: division by 2 * nbb
+    int64_t n_units;            // bf16: B * heads * windows
     float scale;                // 1 / sqrt(head_dim)
 };
 
+// Workgroups of one bf16 backward launch: both roles of every block of every unit, in
+// groups of 8 units (one per XCD).
+__host__ __device__ inline int64_t bwd_bf16_groups(int64_t n_units, int nbb) {
+    return 16 * (int64_t)nbb * ((n_units + 7) / 8);
+}
+
 hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
-// bf16, windows of more than kBwdMaxTokens tokens: key-block kernel, then the dq reduction
-hipError_t launch_swin_bwd_bf16_wide(const SwinBwdArgs& a, hipStream_t stream);
 hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
 
 // Static device scratch of the allocation-free backward: its size, and its device address

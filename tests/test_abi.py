@@ -7,6 +7,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 import oracle as O
@@ -353,35 +354,35 @@ def test_bwd_argument_checks(lib, f32, status, kw):
 
 def test_bwd_wide_windows_supported_except_rope(lib):
     codes = _header_enum("FLA")
-    # 17 x 17 = 289 tokens per window: over the bf16 matrix-core kernel's 256, served by the
-    # fp32-arithmetic kernels in both storage types; only the RoPE backward refuses it
+    # 17 x 17 = 289 tokens per window: three 128-token blocks of the bf16 kernel; the fp32
+    # kernels take it as well
     assert _call_bwd(window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
     assert _call_bwd(f32=True, window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_rope_bwd(window=17, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
-    # a 32-wide window on a 4-row grid holds 128 tokens: fine for RoPE too
-    assert _call_rope_bwd(Hgrid=4, window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    # the RoPE backward follows the bf16 RoPE forward's 32 x 32 window limit
+    assert _call_rope_bwd(window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_rope_bwd(window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_rope_bwd(window=33, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_rope_bwd(Hgrid=4, window=64, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_rope_bwd(Hgrid=4, Wgrid=32, window=64, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
 
 
 def test_bwd_mask_mode_needs_no_workspace(lib):
     codes = _header_enum("FLA")
-    st = _call_bwd(ws=0, ws_bytes=0)
-    assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"])
-    # windows of more than 256 tokens: the bf16 kernels keep each key block's dq share there
-    # (the fp32 kernels do not)
-    assert _call_bwd(ws=0, ws_bytes=0, window=17, shift=0) == codes["FLA_ERR_WORKSPACE"]
-    assert _call_bwd(ws_bytes=16, window=17, shift=0) == codes["FLA_ERR_WORKSPACE"]
-    st = _call_bwd(f32=True, ws=0, ws_bytes=0, window=17, shift=0)
-    assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"])
+    for kw in (dict(), dict(window=17, shift=0), dict(window=32, shift=16)):
+        for f32 in (False, True):
+            st = _call_bwd(f32=f32, ws=0, ws_bytes=0, **kw)
+            assert st not in (codes["FLA_ERR_WORKSPACE"], codes["FLA_ERR_NULL"]), (kw, f32)
+    assert _call_bwd(ws=0, ws_bytes=0, pad_mode=1) == codes["FLA_ERR_WORKSPACE"]
 
 
 def test_bwd_workspace_size_examples(lib):
-    # 64 x 64 grid, 12 heads: window 16 shift 8 in KV-token mode: 25 windows x 12 heads of one
-    # 512-byte pad partial; window 32 shift 16 in mask mode: 9 windows (nqb = 4 query blocks of
-    # 256) x 12 heads x 4 key blocks x 4 x 256 queries x 64 channels x 4 bytes
-    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 16, 8, 1) == 25 * 12 * 512
+    # 64 x 64 grid, 12 heads, KV-token mode: window 16 shift 8 has 25 windows of up to 256
+    # tokens (2 blocks of 128), window 32 shift 16 has 9 windows of up to 1024 (8 blocks), each
+    # block with one 512-byte pad partial per head; MASK mode needs none
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 16, 8, 1) == 25 * 2 * 12 * 512
     assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 16, 8, 0) == 0
-    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 0) == 9 * 12 * 4 * 4 * 256 * 64 * 4
-    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 1) == 9 * 12 * 4 * (512 + 4 * 256 * 64 * 4)
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 0) == 0
+    assert fb.fla_swin_attn_bwd_workspace(1, 12, [(64, 64)], 32, 16, 1) == 9 * 8 * 12 * 512
 
 
 @pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
@@ -406,9 +407,10 @@ NOALLOC_CASES = [
     ("FLA_ERR_SHAPE", dict(B=-1)), ("FLA_ERR_NULL", dict(dout=0)), ("FLA_ERR_ALIGN", dict(dk=DK + 2)),
     ("FLA_ERR_HEAD_DIM", dict(head_dim=32)), ("FLA_ERR_SHIFT", dict(shift=16)),
     ("FLA_ERR_PAD_MODE", dict(pad_mode=2)), ("FLA_ERR_TOO_LARGE", dict(Hgrid=1 << 20, Wgrid=1 << 20)),
-    # workspace beyond the static scratch: pad partials of 40 batch entries (40 * 25 * 12 * 512 B
-    # = 5.9 MiB fits; 160 entries do not), and the dq shares of 12 heads of window-32 windows
-    ("FLA_ERR_SCRATCH", dict(B=160, pad_mode=1)), ("FLA_ERR_SCRATCH", dict(window=32, shift=16)),
+    # workspace beyond the static scratch: pad partials of 25 windows x 2 blocks x 12 heads
+    # (300 KiB per batch entry: 40 entries fit, 160 do not), and of window-32 windows
+    # (9 windows x 8 blocks x 12 heads, 432 KiB per entry)
+    ("FLA_ERR_SCRATCH", dict(B=160, pad_mode=1)), ("FLA_ERR_SCRATCH", dict(B=64, window=32, shift=16, pad_mode=1)),
     ("FLA_ERR_ALIAS", dict(dq=Q)), ("FLA_ERR_ALIAS", dict(dv=DK + 64)),
 ]
 
@@ -426,8 +428,8 @@ def test_noalloc_scratch_limit_matches_workspace_sizes(lib):
     cap = int(m.group(1)) << int(m.group(2))
     assert cap == 16 << 20
     code = _header_enum("FLA")["FLA_ERR_SCRATCH"]
-    for B, heads, window, shift, pm in ((1, 12, 16, 8, 1), (100, 12, 16, 8, 1), (110, 12, 16, 8, 1),
-                                        (1, 1, 32, 16, 0), (1, 2, 32, 16, 0), (1, 1, 32, 16, 1)):
+    for B, heads, window, shift, pm in ((1, 12, 16, 8, 1), (54, 12, 16, 8, 1), (55, 12, 16, 8, 1),
+                                        (1, 12, 32, 16, 0), (37, 12, 32, 16, 1), (38, 12, 32, 16, 1)):
         need = fb.fla_swin_attn_bwd_workspace(B, heads, [(64, 64)], window, shift, pm)
         st = _call_noalloc(B=B, heads=heads, window=window, shift=shift, pad_mode=pm)
         assert (st == code) == (need > cap), (B, heads, window, need, st)
@@ -450,15 +452,27 @@ def test_empty_training_calls_are_ok(lib):
     ([(256, 256)], 16, 8, 1), ([(64, 64)], 16, 8, 0), ([(150, 203)], 16, 8, 1),
     ([(128, 128), (32, 32)], 16, 8, 1), ([(40, 24)], 20, 10, 1), ([(3, 3)], 1, 0, 1)])
 def test_bwd_workspace_size(lib, grids, k, s, pm):
+    """KV-token mode: one pad-gradient partial (128 floats) per (batch entry, head, window,
+    block of 128 tokens of the largest window); nothing in MASK mode."""
     B, heads = 2, 3
     n_win = sum(len(O.window_sizes(h, w, k, s)) for h, w in grids)
-    nqb = max(-(-max(sz for h, w in grids for sz in O.window_sizes(h, w, k, s)) // 256), 1)
-    # pad partials (KV-token mode), then, for windows of more than 256 tokens, every key
-    # block's fp32 dq share of its window's queries
-    shares = B * heads * n_win * nqb * nqb * 256 * 64 * 4 if nqb > 1 else 0
-    want = (B * heads * n_win * nqb * 128 * 4 if pm == 1 else 0) + shares
+    nbb = max(-(-max(sz for h, w in grids for sz in O.window_sizes(h, w, k, s)) // 128), 1)
+    want = B * heads * n_win * nbb * 128 * 4 if pm == 1 else 0
     assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, pm) == want
-    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, 0) == shares
+    assert fb.fla_swin_attn_bwd_workspace(B, heads, grids, k, s, 0) == 0
+
+
+def test_bwd_block_count_is_that_of_the_largest_window(lib):
+    """The workspace counts blocks of the largest window exactly (first, last or a full window
+    along each axis), for grids smaller and larger than the window and every shift."""
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        k = int(rng.integers(1, 40))
+        s = int(rng.integers(0, k))
+        H, W = int(rng.integers(1, 90)), int(rng.integers(1, 90))
+        sizes = O.window_sizes(H, W, k, s)
+        want = len(sizes) * -(-max(sizes) // 128) * 128 * 4
+        assert fb.fla_swin_attn_bwd_workspace(1, 1, [(H, W)], k, s, 1) == want, (H, W, k, s)
 
 
 def test_bwd_workspace_errors(lib):

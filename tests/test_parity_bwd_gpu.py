@@ -135,8 +135,9 @@ def test_lse_and_backward(shape, dtype, pm):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", WIDE, ids=lambda s: "x".join(map(str, s)))
 def test_backward_wide_windows(shape, dtype, pm):
-    """Windows of more than 256 tokens take the three fp32-arithmetic kernels in both storage
-    types (bf16 operands widened exactly, one rounding of each gradient element)."""
+    """Windows of more than 256 tokens: bf16 in 128-token blocks that each stream the whole
+    window's other side through LDS in 128-token chunks (the last ones partial); fp32 in the
+    three fp32 kernels."""
     B, heads, H, W, k, s = shape
     _say("bwd wide %s %s pad_mode=%d" % (shape, dtype, pm))
     f32 = dtype == "f32"
@@ -156,7 +157,7 @@ def test_backward_wide_windows(shape, dtype, pm):
 @pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
 def test_bf16_backward_wide_windows_multi_scale(pm):
     """A grid list whose first grid has windows of more than 256 tokens and whose second has
-    small ones: one launch of the key-block kernel and the dq reduction over both."""
+    small ones, in one launch."""
     grids = ((40, 37), (9, 9))
     wl = _wl(1, 2, 40, 37, 20, 10, "bf16", pm, 31 + pm, grids=grids)
     _say("bwd wide multi-scale %s pad_mode=%d" % (grids, pm))
@@ -170,19 +171,22 @@ def test_bf16_backward_wide_windows_multi_scale(pm):
         _check_grad(name, got, ref, False)
 
 
-def test_bf16_rope_backward_rejects_windows_over_256_tokens():
+def test_bf16_rope_backward_window_limit():
+    """The RoPE backward takes the windows the bf16 RoPE forward takes (at most 32 rows and
+    columns) and refuses wider ones without touching its outputs."""
     B, heads, H, W = 1, 1, 40, 24
     wl = _wl(B, heads, H, W, 20, 10, "bf16", 0, 1)
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
     z = torch.zeros_like(q)
     lse = torch.zeros((B, heads, H * W), dtype=torch.float32, device="cuda")
-    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
-                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, 1e4, 1.0, 0,
+    dq = torch.full_like(q, float("nan"))
+    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, dq, torch.empty_like(kk),
+                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 40, 0, 0, 1e4, 1.0, 0,
                                    check=False)
-    assert rc == 12   # FLA_ERR_UNSUPPORTED
-    # a 16-wide window on a grid only 16 tokens tall but wide is fine
-    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, torch.empty_like(q), torch.empty_like(kk),
-                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 16, 0, 0, 1e4, 1.0, 0,
+    torch.cuda.synchronize()
+    assert rc == 12 and torch.isnan(dq.float()).all()   # FLA_ERR_UNSUPPORTED
+    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, dq, torch.empty_like(kk),
+                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, 1e4, 1.0, 0,
                                    check=False)
     torch.cuda.synchronize()
     assert rc == 0
@@ -205,10 +209,10 @@ def test_multiscale_backward(dtype, pm):
         _check_grad(name, got, r, dtype == "f32")
 
 
-@pytest.mark.parametrize("k,s,pm", [(16, 8, 1), (20, 10, 1), (20, 10, 0)])
+@pytest.mark.parametrize("k,s,pm", [(16, 8, 1), (20, 10, 1), (32, 16, 1)])
 def test_workspace_contents_are_ignored(k, s, pm):
-    """Every workspace element a call reads was written by that call (pad partials; dq shares
-    of windows over 256 tokens), and the result is the same bits run to run."""
+    """Every workspace element a call reads (the pad partials) was written by that call, and
+    the result is the same bits run to run."""
     wl = _wl(1, 2, 37, 29, k, s, "bf16", pm, 5)
     _say("bwd workspace k=%d s=%d pad_mode=%d" % (k, s, pm))
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))

@@ -101,7 +101,8 @@ def test_full_size_rope_sampled():
 
 
 # ---- RoPE training: forward with log-sum-exp, backward (gradients of the unrotated q, k, v)
-BWD_SHAPES = [(2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 300, 16, 15)]
+BWD_SHAPES = [(2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 300, 16, 15),
+              (1, 2, 40, 37, 20, 10), (1, 1, 40, 40, 32, 16)]   # the last two: windows over 256 tokens
 
 
 def _check_grad(name, got, ref, f32, bulk=True):

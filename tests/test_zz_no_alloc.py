@@ -52,8 +52,8 @@ def _noalloc(wl, q, kk, v, dout, out, lse):
 # pairs of (B, heads, H, W, window, shift, pad_mode): the second call of a pair is smaller
 PAIRS = [
     ((1, 12, 64, 64, 16, 8, 1), (2, 2, 20, 13, 8, 3, 1)),      # pad partials in the scratch
-    ((1, 1, 64, 64, 32, 16, 1), (1, 1, 24, 40, 32, 16, 1)),    # wide windows: dq shares too
-    ((1, 1, 48, 64, 32, 16, 0), (2, 1, 30, 20, 16, 8, 0)),     # dq shares, then no scratch at all
+    ((1, 2, 64, 64, 32, 16, 1), (1, 1, 24, 40, 32, 16, 1)),    # windows of several blocks
+    ((1, 1, 48, 64, 32, 16, 0), (2, 1, 30, 20, 16, 8, 0)),     # MASK mode: no scratch at all
 ]
 
 
@@ -89,12 +89,17 @@ def test_noalloc_against_the_oracle():
 
 
 def test_noalloc_rejects_problems_beyond_the_scratch():
-    """A problem whose workspace exceeds the static scratch is refused, and no output is touched."""
-    wl = synth.Workload("noalloc", 1, 12, 64, 64, 64, 32, 16, "bf16", seed=1)
-    q = torch.zeros(1, 64 * 64, 12, 64, dtype=torch.bfloat16, device="cuda")
-    lse = torch.zeros(1, 12, 64 * 64, dtype=torch.float32, device="cuda")
-    dq, dk, dv = (torch.full_like(q, float("nan")) for _ in range(3))
-    rc = fb.fla_swin_attn_bwd_noalloc(q, q, q, q, q, lse, dq, dk, dv, 1, 12, 64, 64, 64, 32, 16, 0, check=False)
+    """A problem whose workspace exceeds the static scratch is refused, and no output is touched:
+    window 1 on a 128 x 128 grid in KV-token mode has one 512-byte pad partial per token and
+    head, 24 MiB for 3 heads."""
+    H = W = 128
+    q = torch.zeros(1, H * W, 3, 64, dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros(1, H * W + 1, 3, 64, dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros(1, 3, H * W, dtype=torch.float32, device="cuda")
+    dq = torch.full_like(q, float("nan"))
+    dk, dv = torch.full_like(kv, float("nan")), torch.full_like(kv, float("nan"))
+    assert fb.fla_swin_attn_bwd_workspace(1, 3, [(H, W)], 1, 0, 1) == 24 << 20
+    rc = fb.fla_swin_attn_bwd_noalloc(q, kv, kv, q, q, lse, dq, dk, dv, 1, 3, H, W, 64, 1, 0, 1, check=False)
     torch.cuda.synchronize()
     assert rc == 15, fb.fla_status_string(rc)
     assert all(torch.isnan(t.float()).all() for t in (dq, dk, dv))
