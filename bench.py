@@ -45,7 +45,8 @@ KERNELS = {
     "fwd": ("swin_fwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bf16.hip",
                               "paper_2407_02109_amd/csrc/fla_swin_internal.h",
                               "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
-    "bwd": ("swin_bwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bwd_bf16.hip",
+    "bwd": ("swin_bwd_bf16", ["paper_2407_02109_amd/csrc/fla_swin_bwd_bf16_window.hip",
+                              "paper_2407_02109_amd/csrc/fla_swin_bwd_bf16_blocks.hip",
                               "paper_2407_02109_amd/csrc/fla_swin_internal.h",
                               "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
 }
@@ -132,7 +133,7 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
             cold = prev is not None and "reduce_kernel" in prev["Kernel_Name"]
             (cold_durs if cold else warm_durs).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
         prev = r
-    # the kernel those launches ran (swin_bwd_bf16_wide_kernel for windows of more than 256 tokens)
+    # the kernel those launches ran (swin_bwd_bf16_block_kernel for windows of more than 256 tokens)
     found = sorted({m.group(1) for r in trace if r["Grid_Size_X"] == main_grid
                     for m in [re.search(r"(%s\w*_kernel)" % kname, r["Kernel_Name"])] if m})
     title = ", ".join(found) or kname + "_kernel"
@@ -377,8 +378,8 @@ def stream_ceiling(torch, qd, kd, vd, out, stream, flush) -> dict:
 def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int, mode: str, flush) -> dict:
     """Training on the same layer: the forward that keeps the log-sum-exp, then the backward
     (dq, dk, dv for a seeded upstream gradient), each timed with events on the stream.  The
-    roofline is that of swin_bwd_bf16_kernel, the backward's dominant kernel (windows of more
-    than 256 tokens: swin_bwd_bf16_wide_kernel and the dq reduction)."""
+    roofline is that of the backward's kernel: swin_bwd_bf16_window_kernel, or for windows of
+    more than 256 tokens swin_bwd_bf16_block_kernel."""
     import torch
     grids = list(wl.grid_list)
     B, L, heads, d = qd.shape

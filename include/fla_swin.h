@@ -222,8 +222,9 @@ int fla_swin_attn_bwd_workspace(int B, int heads, int n_grids, const int* grid_h
  * S = Q.K^T, dP = dO.V^T, dV = P^T.dO, dK = dS^T.Q and dQ = dS.K run on bf16 matrix cores
  * with fp32 accumulation (P and dS rounded to bf16 before their products); outputs are
  * rounded to bf16 (RNE).  The result does not depend on scheduling (fixed summation
- * order).  Any window size: one workgroup per 128-token block of a window computes dK and dV
- * of its keys over all the window's queries, another dQ of its queries over all the keys.
+ * order).  Any window size: windows of up to 256 tokens are taken whole by one workgroup;
+ * wider ones in 128-token blocks, one workgroup per block computing dK and dV of its keys
+ * over all the window's queries and another dQ of its queries over all the keys.
  * Errors: checked in the order
  * stated at the top of this header (FLA_ERR_WORKSPACE after FLA_ERR_TOO_LARGE, before
  * FLA_ERR_ALIAS); nothing is launched and no output is touched on error.

@@ -360,13 +360,17 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.dk = dk;
     a.dv = dv;
     a.ws = static_cast<float*>(ws);
-    a.pad_blocks = elem_bytes == 2 ? pr.geo.nbb : pr.geo.nqb;
+    // bf16: windows of up to 256 tokens (one 256-query block) take the one-window kernel
+    const bool window_kernel = elem_bytes == 2 && pr.geo.nqb == 1;
+    a.pad_blocks = elem_bytes != 2 ? pr.geo.nqb : window_kernel ? 1 : pr.geo.nbb;
     a.nbb = pr.geo.nbb;
     a.div_2nbb = fla::FastDiv::make(2u * (unsigned)pr.geo.nbb);
     a.n_units = units;
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
     const hipStream_t s = stream;
-    hipError_t e = elem_bytes != 2 ? fla::launch_swin_bwd_f32(a, s) : fla::launch_swin_bwd_bf16(a, s);
+    hipError_t e = elem_bytes != 2   ? fla::launch_swin_bwd_f32(a, s)
+                   : window_kernel   ? fla::launch_swin_bwd_bf16_window(a, s)
+                                     : fla::launch_swin_bwd_bf16_blocks(a, s);
     if (e == hipSuccess && pad_mode == FLA_PAD_KVTOKEN) e = fla::launch_swin_bwd_pad_reduce(a, elem_bytes, s);
     if (e != hipSuccess) {
         (void)hipGetLastError();

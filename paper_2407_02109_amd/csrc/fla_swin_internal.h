@@ -116,7 +116,11 @@ __host__ __device__ inline int64_t bwd_bf16_groups(int64_t n_units, int nbb) {
     return 16 * (int64_t)nbb * ((n_units + 7) / 8);
 }
 
-hipError_t launch_swin_bwd_bf16(const SwinBwdArgs& a, hipStream_t stream);
+// bf16: one workgroup per window for launches whose windows all hold at most 256 tokens
+// (pad_blocks = 1); key-role and query-role workgroups per kBwdBlock-token block otherwise
+// (pad_blocks = nbb)
+hipError_t launch_swin_bwd_bf16_window(const SwinBwdArgs& a, hipStream_t stream);
+hipError_t launch_swin_bwd_bf16_blocks(const SwinBwdArgs& a, hipStream_t stream);
 hipError_t launch_swin_bwd_f32(const SwinBwdArgs& a, hipStream_t stream);
 
 // Static device scratch of the allocation-free backward: its size, and its device address

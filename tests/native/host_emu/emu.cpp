@@ -49,6 +49,7 @@ hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, s
 
 namespace fla {
 hipError_t launch_swin_fwd_bf16(const SwinArgs&, hipStream_t) { return 1; }
-hipError_t launch_swin_bwd_bf16(const SwinBwdArgs&, hipStream_t) { return 1; }
+hipError_t launch_swin_bwd_bf16_window(const SwinBwdArgs&, hipStream_t) { return 1; }
+hipError_t launch_swin_bwd_bf16_blocks(const SwinBwdArgs&, hipStream_t) { return 1; }
 hipError_t scratch_address(void**) { return 1; }
 }  // namespace fla
