@@ -149,6 +149,9 @@ int check_limits(int B, int heads, int n_grids, const int* hw, int head_dim, int
     if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
     if (!geometry(B, heads, n_grids, hw, window, shift, &pr->geo)) return FLA_ERR_TOO_LARGE;
     if (pr->geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    // the bf16 forward with several query blocks per window launches them in groups of 8 units
+    const int64_t units = int64_t(B) * heads * pr->geo.n_windows;
+    if (pr->geo.nqb > 1 && 8 * int64_t(pr->geo.nqb) * ((units + 7) / 8) > kMaxGroups) return FLA_ERR_TOO_LARGE;
     // the kernels address a window with 32-bit byte offsets from its first token, and
     // split a window-local index into (row, col) with a 32-bit multiply-high
     for (int i = 0; i < n_grids; ++i) {
@@ -189,6 +192,8 @@ fla::SwinArgs make_args(const Problem& pr, const void* q, const void* k, const v
     a.kv_batch_stride = pr.kv_rows * pr.tok;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)head_dim));
     a.n_groups = geo.n_groups;
+    a.n_units = int64_t(B) * heads * geo.n_windows;
+    a.xcd_group = geo.nqb > 1 ? 1 : 0;
     a.n_cus = cus;
     a.n_grids = n_grids;
     a.n_windows = geo.n_windows;

@@ -150,12 +150,28 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
     //      workgroups of one window read adjacent 128-byte pieces of the same token rows.
-    //      The divisions are multiply-high by constants the host prepared.
-    const unsigned id0 = blockIdx.x;
-    const unsigned id1 = a.div_heads.div(id0);
-    const int head = (int)(id0 - id1 * (unsigned)a.heads);
-    const unsigned id2 = a.div_nqb.div(id1);
-    const int qblk = (int)(id1 - id2 * (unsigned)a.nqb);
+    //      With several query blocks per window (xcd_group), the blocks of one unit (b,
+    //      window, head) get ids 8 (nqb (u / 8) + blk) + u % 8: the dispatcher deals ids to the
+    //      8 XCDs in turn, so they run on one XCD one after the other and the window's K and V
+    //      rows come from HBM once, then from that XCD's L2.  The divisions are multiply-high
+    //      by constants the host prepared.
+    const unsigned id = blockIdx.x;
+    unsigned id1, id2;   // id1: (b, window, query block) (raster) or (b, window) (grouped); id2: (b, window)
+    int head, qblk;
+    if (a.xcd_group) {
+        const unsigned rest = id >> 3;
+        const unsigned g = a.div_nqb.div(rest);
+        qblk = (int)(rest - g * (unsigned)a.nqb);
+        const unsigned unit = (g << 3) + (id & 7u);
+        if (unit >= (unsigned)a.n_units) return;
+        id2 = a.div_heads.div(unit);
+        head = (int)(unit - id2 * (unsigned)a.heads);
+    } else {
+        id1 = a.div_heads.div(id);
+        head = (int)(id - id1 * (unsigned)a.heads);
+        id2 = a.div_nqb.div(id1);
+        qblk = (int)(id1 - id2 * (unsigned)a.nqb);
+    }
     const int nwin = a.n_windows;
     const unsigned id3 = a.div_nwin.div(id2);
     const int win = (int)(id2 - id3 * (unsigned)nwin);
@@ -391,8 +407,7 @@ hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream) {
                                              : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, true>))
                             : (a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, false>)
                                              : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, false>));
-    return hipLaunchKernel(fn,
-                           dim3((unsigned)a.n_groups), dim3(THREADS), params, 0, stream);
+    return hipLaunchKernel(fn, dim3((unsigned)fwd_bf16_groups(a)), dim3(THREADS), params, 0, stream);
 }
 
 }  // namespace fla

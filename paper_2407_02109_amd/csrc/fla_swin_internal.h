@@ -64,6 +64,8 @@ struct SwinArgs {
     int64_t kv_batch_stride;    // same for k / v (L or L + 1 rows)
     float scale_log2;           // log2(e) / sqrt(head_dim): logits go straight to exp2
     int64_t n_groups;           // workgroups: B * heads * windows * query blocks
+    int64_t n_units;            // B * heads * windows
+    int xcd_group;              // forward: the query blocks of a unit share an XCD (nqb > 1)
     int n_cus;                  // compute units of the device
     int n_grids, n_windows;     // grids, and windows over all grids
     GridDesc grid[kMaxGrids];
@@ -79,6 +81,12 @@ struct SwinArgs {
     double rope_freq[kHeadDim / 4];
 };
 
+
+// Workgroups of a bf16 forward launch: n_groups in raster order, or with xcd_group the nqb
+// query blocks of each unit on one XCD, in groups of 8 units.
+__host__ __device__ inline int64_t fwd_bf16_groups(const SwinArgs& a) {
+    return a.xcd_group ? 8 * (int64_t)a.nqb * ((a.n_units + 7) / 8) : a.n_groups;
+}
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
