@@ -130,7 +130,9 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
     cold_durs, warm_durs, prev = [], [], None
     for r in all_rows:
         if kname in r["Kernel_Name"] and r["Grid_Size_X"] == main_grid:
-            cold = prev is not None and "reduce_kernel" in prev["Kernel_Name"]
+            # the flush is torch's reduction (at::native); the library's own pad-gradient
+            # reduction kernel is not a flush
+            cold = prev is not None and "reduce_kernel" in prev["Kernel_Name"] and "at::native" in prev["Kernel_Name"]
             (cold_durs if cold else warm_durs).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
         prev = r
     # the kernel those launches ran (swin_bwd_bf16_block_kernel for windows of more than 256 tokens)
@@ -464,6 +466,7 @@ def main() -> int:
     ap.add_argument("--summarize", metavar="PROF_DIR",
                     help="summarise rocprofv3 CSV output into profiles/ and exit (no GPU needed)")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize")
+    ap.add_argument("--summary-dir", default="", help="where --summarize writes (default: profiles/)")
     ap.add_argument("--leg", default="fwd", choices=["fwd", "bwd"],
                     help="kernel --summarize is about: the forward or the backward")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward leg")
@@ -471,7 +474,7 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.summarize:
-        summarize(args.summarize, args.workload, args.command, args.leg)
+        summarize(args.summarize, args.workload, args.command, args.leg, args.summary_dir)
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
