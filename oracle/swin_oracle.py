@@ -279,31 +279,44 @@ def swin_attention_canvas(q, k, v, H, W, window, shift, pad_mode=PAD_MASK):
 # (iii) FLA form: index mapping, lengths, block-diagonal attention, inverse mapping
 # ----------------------------------------------------------------------------------------
 def _canvas_coords(H, W, k, s):
-    """Window-major canvas coordinates; virtual tokens marked -1.
+    """The k*k slots of every canvas window, from the definitions of App. A.
 
-    Row i of the result lists the raster indices (y*W + x) of window i's k*k slots in
-    row-major order (Eq. nonshift on the extended domain, Sec. 3.3)."""
-    o, Hc, Wc = _canvas_geometry(H, W, k, s)
-    ys = np.arange(Hc) - o
-    xs = np.arange(Wc) - o
-    yy, xx = np.meshgrid(ys, xs, indexing="ij")
-    real = (yy >= 0) & (yy < H) & (xx >= 0) & (xx < W)
-    coords = np.where(real, yy * W + xx, -1)
-    coords = coords.reshape(Hc // k, k, Wc // k, k).transpose(0, 2, 1, 3)
-    return coords.reshape(-1, k * k)
+    The canvas is the grid with o = (k - s) mod k virtual tokens in front of each axis and
+    as many behind as make it a multiple of k (Sec. 3.3); its unshifted k x k windows are
+    taken in raster order of the windows.  Window (wy, wx) covers grid rows
+    wy*k - o .. wy*k - o + k - 1 and grid columns wx*k - o .. wx*k - o + k - 1; its slot
+    (a, b), numbered row-major inside the window (Eq. nonshift on the extended domain),
+    holds grid token (y, x) = (wy*k - o + a, wx*k - o + b), whose raster index is y*W + x,
+    or is virtual (-1) when (y, x) lies outside the grid.  Returns [windows, k*k]."""
+    o = (k - s) % k
+    nwy = -(-(H + o) // k)
+    nwx = -(-(W + o) // k)
+    out = np.full((nwy * nwx, k * k), -1, dtype=np.int64)
+    for wy in range(nwy):
+        for wx in range(nwx):
+            for a in range(k):
+                y = wy * k - o + a
+                for b in range(k):
+                    x = wx * k - o + b
+                    if 0 <= y < H and 0 <= x < W:
+                        out[wy * nwx + wx, a * k + b] = y * W + x
+    return out
 
 
 def fla_shift_window_indices(H, W, k, s):
     """Shift-window index mapping of App. A (Eq. finalswin, Eq. finalswinlengths).
 
-    Returns ``(indices, lengths, inv)``: ``x[indices]`` puts the tokens of each window next
-    to each other, ``lengths[i]`` is the number of real tokens of window i, and
+    Returns ``(indices, lengths, inv)``: ``indices`` lists the real tokens of window 0, then
+    of window 1, ..., each window's in its own row-major order, so ``x[indices]`` puts the
+    tokens of each window next to each other; ``lengths[i]`` is the number of real tokens of
+    window i; ``inv`` is the inverse permutation (``inv[indices[j]] = j``), so
     ``x[indices][inv] == x``."""
-    coords = _canvas_coords(H, W, k, s)
-    lengths = (coords >= 0).sum(axis=1)
-    flat = coords.reshape(-1)
-    indices = flat[flat >= 0]
-    inv = np.argsort(indices, kind="stable")
+    slots = _canvas_coords(H, W, k, s)
+    per_window = [row[row >= 0] for row in slots]
+    indices = np.concatenate(per_window)
+    lengths = np.array([len(t) for t in per_window], dtype=np.int64)
+    inv = np.empty(H * W, dtype=np.int64)
+    inv[indices] = np.arange(len(indices), dtype=np.int64)
     return indices, lengths, inv
 
 
