@@ -53,7 +53,23 @@ def _canvas_origin_is_shift(H, W, k, s):
     return o, -(-(H + o) // k) * k, -(-(W + o) // k) * k
 
 
+_orig_slots = M._canvas_coords
+
+
+def _slots_origin_is_shift(H, W, k, s):
+    # the index-list form's canvas with s virtual tokens in front instead of k - s
+    return _orig_slots(H, W, k, (k - s) % k)
+
+
+def _slots_column_major(H, W, k, s):
+    # slots numbered column-major inside each window
+    out = _orig_slots(H, W, k, s)
+    return out.reshape(-1, k, k).transpose(0, 2, 1).reshape(-1, k * k)
+
+
 MUTANTS = {
+    "index_list_origin_is_shift": {"_canvas_coords": _slots_origin_is_shift},
+    "index_list_slots_column_major": {"_canvas_coords": _slots_column_major},
     "roll_sign_flipped": {"_cyclic_shift": lambda x, s, axes: np.roll(x, (s, s), axis=axes),
                           "_cyclic_unshift": lambda x, s, axes: np.roll(x, (-s, -s), axis=axes)},
     "shift_back_missing": {"_cyclic_unshift": lambda x, s, axes: x},
