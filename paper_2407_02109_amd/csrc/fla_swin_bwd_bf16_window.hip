@@ -11,10 +11,10 @@
 // fla_swin_bwd_bf16_blocks.hip.
 //
 // Per workgroup (512 threads = 8 waves):
-//   1. Q and dO rows of the window -> LDS (row-major, 144-byte rows); LSE and D per query
+//   1. Q, dO and K rows of the window -> LDS (row-major, 144-byte rows); LSE and D per query
 //      -> LDS (D from the dO and O rows as they arrive).  Wave w owns keys [32w, 32w + 32):
-//      its K and V rows stay in registers as MFMA operands, and K also as K^T, obtained
-//      once through LDS with the gfx950 transposing read (ds_read_b64_tr_b16).
+//      its K and V rows also stay in registers as MFMA operands.  Wave w owns query tile w
+//      as well: it keeps that tile's dQ^T accumulator in registers.
 //   2. Steps t = 0 .. nt-1 (nt = ceil(n / 32) query tiles = key tiles): wave w works on
 //      query tile (w + t) mod nt, so at every step each tile belongs to exactly one wave.
 //        S = Q K_w^T and dP = dO V_w^T      (v_mfma_f32_32x32x16_bf16, fp32 accumulation;
@@ -22,13 +22,14 @@
 //        P = exp2(S c log2(e) - LSE log2(e)), dS = P (dP - D) in fp32, rounded to bf16
 //        dV_w^T += dO^T P,  dK_w^T += Q^T dS  (dO^T and Q^T come straight from the LDS
 //                                             rows by transposing reads)
-//        dQ^T += K_w^T dS^T                   (dS goes through a per-wave LDS scratch to
-//                                             put queries on the lanes)
+//      and hands its dS^T tile over through LDS (two buffers, by step parity).  In step t + 1
+//      the owner of that query tile adds its share, dQ^T += K^T dS^T, with K^T read from the
+//      K rows by the gfx950 transposing read (ds_read_b64_tr_b16).  A hand-off moves 8 KB
+//      per step and wave (bf16 dS^T written and read, K^T read), where passing an fp32 dQ^T
+//      accumulator between waves would move 16 KB: the steps are bound by LDS traffic.
 //      The matrix cores do the bookkeeping adds as well: keys past the window's end get -inf
-//      through the C operand of S (so P = 0), -D enters as the C operand of dP, and the tile's
-//      fp32 dQ^T accumulator in LDS is read into the C operand of the dQ^T product and
-//      written back (stored at step 0).  Since no two waves share a tile within a step, one
-//      barrier per step orders the updates and the sum order is fixed.
+//      through the C operand of S (so P = 0), and -D enters as the C operand of dP.  One
+//      barrier per step orders the hand-offs; every dQ^T sums its key tiles in step order.
 //   3. Epilogue: scale, round to bf16 (RNE), stage each wave's 32 rows of dK, dV and dQ in
 //      LDS and store whole 128-byte rows at their own tokens.
 //
@@ -51,22 +52,21 @@ constexpr int NW = 8;                  // waves
 constexpr int TL = 32;                 // keys per wave = queries per tile
 constexpr int NMAX = 256;              // tokens of the largest window = NW * TL
 constexpr int RS = D + 8;              // bf16 stride of Q / dO / staging rows (144 B)
-constexpr int SS = TL + 4;             // bf16 stride of the dS^T scratch rows (72 B)
+constexpr int SS = TL + 4;             // bf16 stride of the dS^T hand-off rows (72 B)
 constexpr float kLog2e = 1.4426950408889634f;
 
 // LDS carve-up, bytes
 constexpr int OFF_Q = 0;                               // Q rows       [256][RS] bf16
 constexpr int OFF_DO = OFF_Q + NMAX * RS * 2;          // dO rows      [256][RS] bf16
-constexpr int OFF_DQ = OFF_DO + NMAX * RS * 2;         // dQ^T accumulators, [tile][8][64] float4
-constexpr int OFF_LSE = OFF_DQ + NMAX * D * 4;         // LSE * log2(e) [256] fp32
+constexpr int OFF_K = OFF_DO + NMAX * RS * 2;          // K rows       [256][RS] bf16
+constexpr int OFF_LSE = OFF_K + NMAX * RS * 2;         // LSE * log2(e) [256] fp32
 constexpr int OFF_DD = OFF_LSE + NMAX * 4;             // D            [256] fp32
 constexpr int OFF_DSP = OFF_DD + NMAX * 4;             // pad-token dS [256] fp32
 constexpr int OFF_KP = OFF_DSP + NMAX * 4;             // pad-token key row [64] fp32
-constexpr int OFF_DST = OFF_KP + D * 4;                // dS^T scratch [wave][32][SS] bf16
-constexpr int LDS_BYTES = OFF_DST + NW * TL * SS * 2;
+constexpr int OFF_DST = OFF_KP + D * 4;                // dS^T hand-off [2][wave][32][SS] bf16
+constexpr int LDS_BYTES = OFF_DST + 2 * NW * TL * SS * 2;
 static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
-static_assert(NW * TL * RS * 2 <= NMAX * D * 4, "K staging fits in the dQ area");
-static_assert(NW * kPadPartial * 4 <= NW * TL * SS * 2, "pad partials fit in the dS^T scratch");
+static_assert(NW * kPadPartial * 4 <= NW * TL * SS * 2, "pad partials fit in the dS^T hand-off area");
 
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
@@ -102,27 +102,14 @@ __device__ __forceinline__ float sum8(float x) {
 }
 
 // One step of a wave: the query tile whose rows start at q0 (Q, dO rows, -D and LSE*log2(e)
-// in LDS) against the wave's 32 keys (kreg, vreg, kt in registers).  dK^T and dV^T add up in
-// registers; the tile's fp32 dQ^T accumulator in LDS (acc, lane-major, 8 float4 per lane)
-// is read (read_acc; else taken as zero), advanced by this step's product and written back.
+// in LDS) against the wave's 32 keys (kreg, vreg in registers).  dK^T and dV^T add up in
+// registers; the tile's dS^T goes to the wave's hand-off buffer `dst`, from which the wave
+// that owns the query tile takes its dQ^T share after the step's barrier.
 __device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dOs, const float* Ds, const float* Ls,
-                                          float4* acc, uint16_t* dst, const bf16x8 (&kreg)[4],
-                                          const bf16x8 (&vreg)[4], const bf16x8 (&kt)[2][2],
+                                          uint16_t* dst, const bf16x8 (&kreg)[4], const bf16x8 (&vreg)[4],
                                           const floatx16& s_init, floatx16 (&dkT)[2], floatx16 (&dvT)[2], int q0,
-                                          bool read_acc, float c2, int lane) {
+                                          float c2, int lane) {
     const int li = lane & 31, h = lane >> 5;
-    // the tile's dQ^T accumulator (written by earlier steps) becomes the C operand of
-    // this step's dQ^T product; fetched first so that the read is long done by then
-    floatx16 dq[2];
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        const float4 y = read_acc ? acc[g * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-        const int dh = g >> 2, i = g & 3;
-        dq[dh][4 * i] = y.x;
-        dq[dh][4 * i + 1] = y.y;
-        dq[dh][4 * i + 2] = y.z;
-        dq[dh][4 * i + 3] = y.w;
-    }
     // dP - D in one go: the MFMA's C operand holds -D of each entry's query
     floatx16 sacc = s_init, pacc;
 #pragma unroll
@@ -167,25 +154,26 @@ __device__ __forceinline__ void wave_step(const uint16_t* Qs, const uint16_t* dO
             dvT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, pb[sg], dvT[dh], 0, 0, 0);
             dkT[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, sb[sg], dkT[dh], 0, 0, 0);
         }
-    // dS^T -> scratch (row = key li, 4 consecutive queries per write)
+    // dS^T -> hand-off buffer (row = key li, 4 consecutive queries per write)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         *reinterpret_cast<bf16x4*>(dst + li * SS + 8 * i + 4 * h) =
             bf16x4{sb[i >> 1][4 * (i & 1)], sb[i >> 1][4 * (i & 1) + 1], sb[i >> 1][4 * (i & 1) + 2],
                    sb[i >> 1][4 * (i & 1) + 3]};
-    asm volatile("" ::: "memory");   // the scratch reads below follow these writes
-    // dQ^T += K_w^T dS^T: lane holds query q0 + li, channels 32 dh + 8 i + 4 h + j
+}
+
+// The owner of a query tile adds one key tile's share: dQ^T += K^T dS^T, with K^T read from
+// the K rows of that key tile (key0) and dS^T from the hand-off buffer of the wave that
+// worked on the pair.  Lane holds query li of the tile, channels 32 dh + 8 i + 4 h + j.
+__device__ __forceinline__ void owner_dq(const uint16_t* Ks, const uint16_t* src, int key0, floatx16 (&dq)[2],
+                                         int lane) {
+    const bf16x8 sbt0 = tr_operand(src, SS, 0, 0, lane), sbt1 = tr_operand(src, SS, 16, 0, lane);
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-        const bf16x8 sbt = tr_operand(dst, SS, 16 * s2, 0, lane);
-#pragma unroll
-        for (int dh = 0; dh < 2; ++dh)
-            dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt[dh][s2], sbt, dq[dh], 0, 0, 0);
-    }
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        const int dh = g >> 2, i = g & 3;
-        acc[g * 64] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
+    for (int dh = 0; dh < 2; ++dh) {
+        const bf16x8 k0 = tr_operand(Ks, RS, key0, 32 * dh, lane);
+        const bf16x8 k1 = tr_operand(Ks, RS, key0 + 16, 32 * dh, lane);
+        dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, sbt0, dq[dh], 0, 0, 0);
+        dq[dh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, sbt1, dq[dh], 0, 0, 0);
     }
 }
 
@@ -195,7 +183,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
     __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
     uint16_t* Qs = reinterpret_cast<uint16_t*>(smem + OFF_Q);
     uint16_t* dOs = reinterpret_cast<uint16_t*>(smem + OFF_DO);
-    float4* DQ = reinterpret_cast<float4*>(smem + OFF_DQ);
+    uint16_t* Ks = reinterpret_cast<uint16_t*>(smem + OFF_K);
     float* Ls = reinterpret_cast<float*>(smem + OFF_LSE);
     float* Ds = reinterpret_cast<float*>(smem + OFF_DD);
     float* DSP = reinterpret_cast<float*>(smem + OFF_DSP);
@@ -301,7 +289,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
             kreg[s] = rope_rotate_bf16x8(kreg[s], (s < 2 ? y : x) * a.rope_scale, a.rope_rev + 8 * (s & 1) + 4 * h);
     }
 
-    // ---- LDS: rows, LSE, D; the wave's K rows into its staging area (in the dQ space)
+    // ---- LDS: Q, dO and K rows, LSE, D
     float pk[8], pv[8];   // this thread's share of the pad token's gradient (8 channels)
     for (int e = 0; e < 8; ++e) pk[e] = pv[e] = 0.f;
 #pragma unroll
@@ -350,18 +338,10 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
             }
         }
     }
-    uint16_t* kstage = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * TL * RS;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-        *reinterpret_cast<bf16x8*>(kstage + li * RS + 16 * s + 8 * h) = kreg[s];
+        *reinterpret_cast<bf16x8*>(Ks + (TL * wave + li) * RS + 16 * s + 8 * h) = kreg[s];
     __syncthreads();
-
-    // K_w^T (A operand of dQ^T = K^T dS^T): lane row = channel 32 dh + li, keys along k
-    bf16x8 kt[2][2];
-#pragma unroll
-    for (int dh = 0; dh < 2; ++dh)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) kt[dh][s2] = tr_operand(kstage, RS, 16 * s2, 32 * dh, lane);
     if (KVPAD && tid < kPadPartial) {
         // every workgroup writes its share (zero without virtual slots), so the reduction
         // reads a dense array
@@ -377,20 +357,31 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
 
     // ---- 2. steps
     floatx16 dkT[2] = {floatx16{}, floatx16{}}, dvT[2] = {floatx16{}, floatx16{}};
-    uint16_t* dst = DST + wave * TL * SS;
+    floatx16 dq[2] = {floatx16{}, floatx16{}};   // dQ^T of query tile `wave`, owned by this wave
     const float c2 = a.scale_log2;
     // C operand of S = Q K^T: 0, or -inf for a key past the window's last (its P is then 0)
     floatx16 s_init;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s_init[r] = key_ok ? 0.f : -INFINITY;
+    // step t: wave w works on query tile (w + t) mod nt and hands its dS^T over (buffer t % 2);
+    // during step t + 1 the owner of that tile adds its dQ^T share
     for (int t = 0; t < nt; ++t) {
         if (wave < nt) {
+            if (t > 0) {
+                const int w = wave - t + 1 >= 0 ? wave - t + 1 : wave - t + 1 + nt;
+                owner_dq(Ks, DST + (((t - 1) & 1) * NW + w) * TL * SS, TL * w, dq, lane);
+            }
             const int T = wave + t < nt ? wave + t : wave + t - nt;
-            wave_step(Qs, dOs, Ds, Ls, DQ + T * 8 * 64 + lane, dst, kreg, vreg, kt, s_init, dkT, dvT, TL * T, t > 0,
+            wave_step(Qs, dOs, Ds, Ls, DST + ((t & 1) * NW + wave) * TL * SS, kreg, vreg, s_init, dkT, dvT, TL * T,
                       c2, lane);
         }
         __syncthreads();
     }
+    if (wave < nt) {
+        const int w = wave - nt + 1 >= 0 ? wave - nt + 1 : wave + 1;
+        owner_dq(Ks, DST + (((nt - 1) & 1) * NW + w) * TL * SS, TL * w, dq, lane);
+    }
+    __syncthreads();   // the epilogue stages dQ rows over the K rows
 
     // ---- 3. epilogue: each wave stages its 32 key rows of dK and dV (in the Q and dO rows)
     //         and its query tile of dQ (in that tile's accumulator space), then stores whole
@@ -429,15 +420,16 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
                 *reinterpret_cast<bf16x4*>(krow_s + 32 * dh + 8 * i + 4 * h) = k4;
                 *reinterpret_cast<bf16x4*>(vrow_s + 32 * dh + 8 * i + 4 * h) = v4;
             }
-        // dQ: this wave's tile is tile `wave`; read all of it before staging rows over it
-        const float4* acc = DQ + wave * 8 * 64 + lane;
+        // dQ: this wave owns tile `wave`
         float4 x[8];
 #pragma unroll
-        for (int g = 0; g < 8; ++g) x[g] = acc[g * 64];
-        asm volatile("" ::: "memory");
+        for (int g = 0; g < 8; ++g) {
+            const int dh = g >> 2, i = g & 3;
+            x[g] = make_float4(dq[dh][4 * i], dq[dh][4 * i + 1], dq[dh][4 * i + 2], dq[dh][4 * i + 3]);
+        }
         const int qi = TL * wave + li;
         const float dsp = has_pad ? DSP[qi] : 0.f;
-        uint16_t* qrow_s = reinterpret_cast<uint16_t*>(smem + OFF_DQ) + wave * 8 * 64 * 8 + li * RS;
+        uint16_t* qrow_s = Ks + (TL * wave + li) * RS;
         [[maybe_unused]] float qy = 0.f, qx = 0.f;
         if constexpr (ROPE) coords(min(qi, n - 1), qy, qx);
 #pragma unroll
@@ -459,7 +451,7 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
             *reinterpret_cast<bf16x4*>(qrow_s + ch) = o4;
         }
         asm volatile("" ::: "memory");   // staged rows are read back by other lanes
-        const uint16_t* qbase_s = reinterpret_cast<const uint16_t*>(smem + OFF_DQ) + wave * 8 * 64 * 8;
+        const uint16_t* qbase_s = Ks + TL * wave * RS;
         const int sp = lane & 7;
 #pragma unroll
         for (int it = 0; it < TL / 8; ++it) {
