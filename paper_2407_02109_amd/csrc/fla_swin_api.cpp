@@ -148,7 +148,8 @@ int check_limits(int B, int heads, int n_grids, const int* hw, int head_dim, int
     if (kv_rows >= kMaxElems || tok >= kMaxElems || kv_rows > kMaxElems / tok) return FLA_ERR_TOO_LARGE;
     if (B > kMaxElems / (kv_rows * tok)) return FLA_ERR_TOO_LARGE;
     if (!geometry(B, heads, n_grids, hw, window, shift, &pr->geo)) return FLA_ERR_TOO_LARGE;
-    if (pr->geo.n_groups > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    // one workgroup per unit or query block, in groups of 8
+    if (8 * ((pr->geo.n_groups + 7) / 8) > kMaxGroups) return FLA_ERR_TOO_LARGE;
     // the bf16 forward with several query blocks per window launches them in groups of 8 units
     const int64_t units = int64_t(B) * heads * pr->geo.n_windows;
     if (pr->geo.nqb > 1 && 8 * int64_t(pr->geo.nqb) * ((units + 7) / 8) > kMaxGroups) return FLA_ERR_TOO_LARGE;

@@ -150,7 +150,8 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
     //      workgroups of one window read adjacent 128-byte pieces of the same token rows.
-    //      With several query blocks per window (xcd_group), the blocks of one unit (b,
+    //      With one query block per window, ids go to units through xcd_rotate (every XCD
+    //      takes every head).  With several query blocks per window (xcd_group), the blocks of one unit (b,
     //      window, head) get ids 8 (nqb (u / 8) + blk) + u % 8: the dispatcher deals ids to the
     //      8 XCDs in turn, so they run on one XCD one after the other and the window's K and V
     //      rows come from HBM once, then from that XCD's L2.  The divisions are multiply-high
@@ -166,9 +167,11 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         if (unit >= (unsigned)a.n_units) return;
         id2 = a.div_heads.div(unit);
         head = (int)(unit - id2 * (unsigned)a.heads);
-    } else {
-        id1 = a.div_heads.div(id);
-        head = (int)(id - id1 * (unsigned)a.heads);
+    } else {   // one query block per window: id1 = id2
+        const unsigned u = xcd_rotate(id, 4);
+        if (u >= (unsigned)a.n_groups) return;
+        id1 = a.div_heads.div(u);
+        head = (int)(u - id1 * (unsigned)a.heads);
         id2 = a.div_nqb.div(id1);
         qblk = (int)(id1 - id2 * (unsigned)a.nqb);
     }

@@ -190,8 +190,9 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
     float* KP = reinterpret_cast<float*>(smem + OFF_KP);
     uint16_t* DST = reinterpret_cast<uint16_t*>(smem + OFF_DST);
 
-    // ---- workgroup -> (b, window, head), heads fastest
-    const unsigned id0 = blockIdx.x;
+    // ---- workgroup -> unit (b, window, head), heads fastest, XCD classes rotated
+    const unsigned id0 = xcd_rotate(blockIdx.x, 2);
+    if (id0 >= (unsigned)ba.n_units) return;
     const unsigned id1 = a.div_heads.div(id0);
     const int head = (int)(id0 - id1 * (unsigned)a.heads);
     const unsigned id2 = a.div_nwin.div(id1);
@@ -483,7 +484,7 @@ hipError_t launch_swin_bwd_bf16_window(const SwinBwdArgs& a, hipStream_t stream)
                          : reinterpret_cast<const void*>(&swin_bwd_bf16_window_kernel<true, false, false>))
                    : (kv ? reinterpret_cast<const void*>(&swin_bwd_bf16_window_kernel<false, true, false>)
                          : reinterpret_cast<const void*>(&swin_bwd_bf16_window_kernel<false, false, false>));
-    const long long groups = (long long)a.f.B * a.f.heads * a.f.n_windows;
+    const long long groups = 8 * ((a.n_units + 7) / 8);
     return hipLaunchKernel(fn, dim3((unsigned)groups), dim3(THREADS), params, 0, stream);
 }
 

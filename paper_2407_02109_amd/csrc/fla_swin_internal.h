@@ -82,10 +82,23 @@ struct SwinArgs {
 };
 
 
-// Workgroups of a bf16 forward launch: n_groups in raster order, or with xcd_group the nqb
-// query blocks of each unit on one XCD, in groups of 8 units.
+// Workgroups of a bf16 forward launch: one per unit in groups of 8 (the last one padded), or
+// with xcd_group the nqb query blocks of each unit on one XCD, in groups of 8 units.
 __host__ __device__ inline int64_t fwd_bf16_groups(const SwinArgs& a) {
-    return a.xcd_group ? 8 * (int64_t)a.nqb * ((a.n_units + 7) / 8) : a.n_groups;
+    return a.xcd_group ? 8 * (int64_t)a.nqb * ((a.n_units + 7) / 8) : 8 * ((a.n_groups + 7) / 8);
+}
+
+// Workgroup id -> unit for launches of one workgroup per unit (b, window, head), heads
+// fastest.  The dispatcher deals ids to the 8 XCDs in turn, so with ids in unit order XCD x
+// would only ever see the units u = x (mod 8): with 12 heads, the heads of one residue class
+// mod 4.  Loads of some heads run measurably slower than others' (their 128-byte rows sit at
+// a different offset in every token's record), and the XCDs holding those heads then
+// finish last.  Ids 8 g .. 8 g + 7 take the units 8 g .. 8 g + 7 rotated by g >> s: every XCD
+// passes through every class, 2^s groups at a time (mixing the classes on an XCD at a finer
+// grain measured slower).  Ids of the last group may fall past the last unit.
+__device__ __forceinline__ unsigned xcd_rotate(unsigned id, unsigned s) {
+    const unsigned g = id >> 3;
+    return (g << 3) + ((id + (g >> s)) & 7u);
 }
 
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream);
