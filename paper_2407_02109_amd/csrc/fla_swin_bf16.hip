@@ -151,11 +151,12 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     // ---- workgroup -> (b, window, query block, head); heads vary fastest so that the
     //      workgroups of one window read adjacent 128-byte pieces of the same token rows.
     //      With one query block per window, ids go to units through xcd_rotate (every XCD
-    //      takes every head).  With several query blocks per window (xcd_group), the blocks of one unit (b,
-    //      window, head) get ids 8 (nqb (u / 8) + blk) + u % 8: the dispatcher deals ids to the
-    //      8 XCDs in turn, so they run on one XCD one after the other and the window's K and V
-    //      rows come from HBM once, then from that XCD's L2.  The divisions are multiply-high
-    //      by constants the host prepared.
+    //      takes every head).  With several query blocks per window (xcd_group), the blocks
+    //      of unit u = 8 g + r (b, window, head) get ids 8 (nqb g + blk) + x with
+    //      r = (x + g / 4) mod 8: the dispatcher deals ids to the 8 XCDs in turn, so the
+    //      blocks run on XCD x one after the other and the window's K and V rows come from
+    //      HBM once, then from that XCD's L2, and the units' classes rotate over the XCDs as
+    //      in xcd_rotate.  The divisions are multiply-high by constants the host prepared.
     const unsigned id = blockIdx.x;
     unsigned id1, id2;   // id1: (b, window, query block) (raster) or (b, window) (grouped); id2: (b, window)
     int head, qblk;
@@ -163,7 +164,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         const unsigned rest = id >> 3;
         const unsigned g = a.div_nqb.div(rest);
         qblk = (int)(rest - g * (unsigned)a.nqb);
-        const unsigned unit = (g << 3) + (id & 7u);
+        const unsigned unit = (g << 3) + ((id + (g >> 2)) & 7u);   // XCD classes rotated, as in xcd_rotate
         if (unit >= (unsigned)a.n_units) return;
         id2 = a.div_heads.div(unit);
         head = (int)(unit - id2 * (unsigned)a.heads);
