@@ -56,15 +56,17 @@ constexpr int SS = TL + 4;             // bf16 stride of the dS^T hand-off rows 
 constexpr float kLog2e = 1.4426950408889634f;
 
 // LDS carve-up, bytes
-constexpr int OFF_Q = 0;                               // Q rows       [256][RS] bf16
-constexpr int OFF_DO = OFF_Q + NMAX * RS * 2;          // dO rows      [256][RS] bf16
-constexpr int OFF_K = OFF_DO + NMAX * RS * 2;          // K rows       [256][RS] bf16
-constexpr int OFF_LSE = OFF_K + NMAX * RS * 2;         // LSE * log2(e) [256] fp32
+// (LSE and D first, then Q and dO: every access the steps make to them is within reach of
+// the 16-bit immediate offset of an LDS instruction from one base register)
+constexpr int OFF_LSE = 0;                             // LSE * log2(e) [256] fp32
 constexpr int OFF_DD = OFF_LSE + NMAX * 4;             // D            [256] fp32
-constexpr int OFF_DSP = OFF_DD + NMAX * 4;             // pad-token dS [256] fp32
+constexpr int OFF_Q = OFF_DD + NMAX * 4;               // Q rows       [256][RS] bf16
+constexpr int OFF_DO = OFF_Q + NMAX * RS * 2;          // dO rows      [256][RS] bf16
+constexpr int OFF_DSP = OFF_DO + NMAX * RS * 2;        // pad-token dS [256] fp32
 constexpr int OFF_KP = OFF_DSP + NMAX * 4;             // pad-token key row [64] fp32
 constexpr int OFF_DST = OFF_KP + D * 4;                // dS^T hand-off [2][wave][32][SS] bf16
-constexpr int LDS_BYTES = OFF_DST + 2 * NW * TL * SS * 2;
+constexpr int OFF_K = OFF_DST + 2 * NW * TL * SS * 2;  // K rows       [256][RS] bf16
+constexpr int LDS_BYTES = OFF_K + NMAX * RS * 2;
 static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
 static_assert(NW * kPadPartial * 4 <= NW * TL * SS * 2, "pad partials fit in the dS^T hand-off area");
 
@@ -232,17 +234,11 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
     const int li = lane & 31;
     const int h = lane >> 5;
 
-    // ---- 1. loads.  K_w and V_w rows: lane holds row 32 * wave + li, channels 16 s + 8 h .. + 7
-    //         (the B operand of S = Q K^T and dP = dO V^T).
+    // ---- 1. loads: the Q, dO and O rows first (staged first: a wait for a load waits for every
+    //         load issued before it), then the wave's K and V rows.
     const int key = TL * wave + li;
     const bool key_ok = key < n;
     const unsigned krow = key_ok ? addr(key) : kOutside;
-    bf16x8 kreg[4], vreg[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        kreg[s] = __builtin_bit_cast(bf16x8, bload16(kr, krow + 32 * s + 16 * h));
-        vreg[s] = __builtin_bit_cast(bf16x8, bload16(vr, krow + 32 * s + 16 * h));
-    }
     // Q, dO, O: 8 threads per 128-byte row, rows r0 + 64 u
     const int part = tid & 7;
     const int r0 = tid >> 3;
@@ -265,6 +261,15 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
         const __amdgpu_buffer_rsrc_t vpr = make_rsrc(static_cast<const uint16_t*>(a.v) + pad_elems, D * 2);
         kp8 = bload16(kpr, 16 * part);
         vp8 = bload16(vpr, 16 * part);
+    }
+
+    // K_w and V_w rows: lane holds row 32 * wave + li, channels 16 s + 8 h .. + 7 (the B operand
+    // of S = Q K^T and dP = dO V^T)
+    bf16x8 kreg[4], vreg[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        kreg[s] = __builtin_bit_cast(bf16x8, bload16(kr, krow + 32 * s + 16 * h));
+        vreg[s] = __builtin_bit_cast(bf16x8, bload16(vr, krow + 32 * s + 16 * h));
     }
 
     // (row, col) grid coordinates of window-local index t
