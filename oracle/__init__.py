@@ -8,7 +8,8 @@ Every function here is a slow, obviously-correct restatement of the paper's
 definitions in float64 NumPy; see ``swin_oracle`` for the four single-grid forms,
 ``multiscale`` for the multi-scale (several grids in one sequence) forms of App. C and
 ``backward`` for the gradients (dq, dk, dv) and the log-sum-exp a training forward keeps,
-``rope`` for 2-D rotary position embedding of q and k ahead of the attention.
+``rope`` for 2-D rotary position embedding of q and k ahead of the attention, and
+``cycle_scan`` for the Cycle-scan module's selective state-space scan (Sec. 3.5).
 """
 from .swin_oracle import (  # noqa: F401
     PAD_MASK,
@@ -45,4 +46,10 @@ from .multiscale import (  # noqa: F401
     swin_attention_ms,
     swin_attention_ms_at,
     swin_attention_ms_fla,
+)
+from .cycle_scan import (  # noqa: F401
+    cycle_scan,
+    cycle_scan_channels,
+    selective_scan,
+    zoh,
 )
