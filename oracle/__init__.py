@@ -47,9 +47,4 @@ from .multiscale import (  # noqa: F401
     swin_attention_ms_at,
     swin_attention_ms_fla,
 )
-from .cycle_scan import (  # noqa: F401
-    cycle_scan,
-    cycle_scan_channels,
-    selective_scan,
-    zoh,
-)
+from . import cycle_scan  # noqa: F401  (the module: cycle_scan.cycle_scan, .selective_scan, .zoh)
