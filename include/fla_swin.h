@@ -61,8 +61,9 @@ typedef enum {
     FLA_OK = 0,
     FLA_ERR_NULL = 1,      /* a pointer is NULL on a non-empty problem (the grid list of the
                               multi-scale entry points: always)                           */
-    FLA_ERR_ALIGN = 2,     /* a pointer is not 16-byte aligned                             */
-    FLA_ERR_SHAPE = 3,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8       */
+    FLA_ERR_ALIGN = 2,     /* a pointer is not 16-byte aligned (Cycle-scan: 4-byte)         */
+    FLA_ERR_SHAPE = 3,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8;
+                              Cycle-scan: B, L, d negative, N or repeats below 1          */
     FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (supported: 64)                      */
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
@@ -76,9 +77,10 @@ typedef enum {
                               more (min(window, Hgrid) * Wgrid * heads * head_dim * element
                               bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
     FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE forward or backward with min(window, H) or
-                                 min(window, W) above 32                                  */
-    FLA_ERR_WORKSPACE = 13, /* backward: workspace NULL or smaller than
-                               fla_swin_attn_bwd_workspace() reports                      */
+                                 min(window, W) above 32; Cycle-scan with N not a power
+                                 of two up to 32                                          */
+    FLA_ERR_WORKSPACE = 13, /* backward, Cycle-scan: workspace NULL or smaller than the
+                               matching _workspace() function reports                     */
     FLA_ERR_ROPE = 14,     /* RoPE entry points: rope_theta not finite and > 0, or
                               rope_scale not finite                                       */
     FLA_ERR_SCRATCH = 15   /* allocation-free backward: the problem needs more workspace than
@@ -296,6 +298,54 @@ int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const vo
 int fla_swin_attn_bwd_work(int B, int heads, int n_grids, const int* grid_hw, int head_dim,
                            int window, int shift, int pad_mode, int elem_bytes,
                            double* flops, double* bytes);
+
+/* ---- Cycle-scan (HRSAM Sec. 3.5) -------------------------------------------------------
+ *
+ * The Cycle-scan module's state space model over the token sequence, fp32.  Every channel
+ * c of a d-channel sequence is scanned on its own with N states, a diagonal A, and the
+ * zero-order hold of the SSM equations of Sec. 3.5 (Delta, B and C given per token, as in
+ * the selective scan of Mamba, which the paper uses):
+ *   h_t = Abar_t h_{t-1} + Bbar_t x_t,   y_t = sum_n C_t[n] h_t[n],
+ *   Abar_t[n] = exp(delta_t[c] A[c][n]),  Bbar_t[n] = (exp(delta_t[c] A[c][n]) - 1) / A[c][n] * B_t[n].
+ * Cycle-scan lays the sequence out `repeats` times one after the other (the paper uses 3),
+ * scans the repeats * L tokens in that order from h = 0 (the state runs on from one copy
+ * into the next), cuts the output into the copies and sums them:
+ *   y[b, t, c] = sum_{k<repeats} (scan output at position k L + t).
+ * The copies are never formed; the kernels take two passes over the data (see the kernel
+ * source for the algebra).
+ *
+ * Layout (fp32, contiguous, row-major, device pointers, 4-byte aligned):
+ *   x, delta, y [B, L, d]  (token-major, channels contiguous: the attention's token layout);
+ *   A [d, N]               (the diagonal of each channel's A: negative, as Mamba's -exp(A_log);
+ *                           A = 0 is not supported and yields NaN);
+ *   Bm, Cm [B, L, N]       (B_t and C_t of each token, shared by the channels).
+ * delta holds the step sizes (positive; softplus already applied).  N (states per channel)
+ * is one of 1, 2, 4, 8, 16, 32 (the paper's Cycle-scan uses 32).
+ * Errors, in this order: FLA_ERR_SHAPE (B, L or d negative, N or repeats below 1); then an
+ * empty problem (B, L or d equal to 0) returns FLA_OK and ignores the pointers;
+ * FLA_ERR_NULL; FLA_ERR_ALIGN (4 bytes); FLA_ERR_UNSUPPORTED (N not one of those); FLA_ERR_TOO_LARGE
+ * (x or Bm of 2^40 elements or more, or 2^23 workgroups or more); FLA_ERR_WORKSPACE;
+ * FLA_ERR_ALIAS (y or the workspace overlapping an input or each other; inputs may alias
+ * each other); FLA_ERR_ARCH; FLA_ERR_LAUNCH.  Nothing is launched and y is not touched on
+ * error.  Asynchronous on `stream` (three kernels). */
+
+/* Workspace of fla_cycle_scan, in bytes: 4 (N + 1) floats per (batch entry, chunk, channel)
+ * with chunks of 32 to 256 tokens.  Errors as for fla_cycle_scan up to FLA_ERR_TOO_LARGE
+ * (bytes must be non-NULL). */
+int fla_cycle_scan_workspace(int B, int L, int d, int N, int repeats, size_t* bytes);
+
+/* The Cycle-scan described above.  workspace: device memory of at least
+ * fla_cycle_scan_workspace() bytes, contents ignored on entry and overwritten. */
+int fla_cycle_scan(const float* x, const float* delta, const float* A, const float* Bm,
+                   const float* Cm, float* y, void* workspace, size_t workspace_bytes, int B,
+                   int L, int d, int N, int repeats, hipStream_t stream);
+
+/* Algorithmic work of one fla_cycle_scan call (host arithmetic only):
+ *   *exps  = B * L * d * N: the exponentials exp(delta A) of the definition, one per
+ *            (batch entry, token, channel, state) -- the copies repeat them;
+ *   *bytes = 4 * (3 B L d + 2 B L N + d N): x, delta, Bm, Cm, A read once, y written once.
+ * Errors: FLA_ERR_SHAPE as for fla_cycle_scan; FLA_ERR_NULL for a NULL output. */
+int fla_cycle_scan_work(int B, int L, int d, int N, int repeats, double* exps, double* bytes);
 
 #ifdef __cplusplus
 }

@@ -1,4 +1,4 @@
-"""Flash Swin attention for AMD MI355X (gfx950).
+"""Flash Swin attention (and HRSAM's Cycle-scan) for AMD MI355X (gfx950).
 
 The compute lives in the HIP library ``libfla_swin.so`` built from ``csrc/``; this
 package only marshals arguments to its C ABI (see ``binding``).  Importing the package
@@ -32,6 +32,10 @@ from .binding import (  # noqa: F401
     swin_attn_rope_fwd_train,
     swin_attn_rope_bwd,
     swin_attention,
+    fla_cycle_scan,
+    fla_cycle_scan_workspace,
+    fla_cycle_scan_work,
+    cycle_scan,
     library_path,
     load_library,
 )

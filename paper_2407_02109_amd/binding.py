@@ -77,6 +77,12 @@ def _declare(lib):
     lib.fla_swin_attn_rope_fwd_lse.restype = I
     lib.fla_swin_attn_rope_bwd.argtypes = [P] * 10 + [Z, I, I, I, I, I, I, I, I, F, F, P]
     lib.fla_swin_attn_rope_bwd.restype = I
+    lib.fla_cycle_scan.argtypes = [P] * 7 + [Z, I, I, I, I, I, P]
+    lib.fla_cycle_scan.restype = I
+    lib.fla_cycle_scan_workspace.argtypes = [I, I, I, I, I, ctypes.POINTER(Z)]
+    lib.fla_cycle_scan_workspace.restype = I
+    lib.fla_cycle_scan_work.argtypes = [I, I, I, I, I, D, D]
+    lib.fla_cycle_scan_work.restype = I
 
 
 def load_library():
@@ -522,3 +528,55 @@ def swin_attention(q, k, v, grids, window, shift, pad_mode=FLA_PAD_MASK, rope=No
             raise ValueError("RoPE takes a single grid")
         rope = (float(rope[0]), float(rope[1]))
     return _swin_attention_function().apply(q, k, v, grids, int(window), int(shift), int(pad_mode), rope)
+
+
+# ---- Cycle-scan (Sec. 3.5) ----------------------------------------------------------------
+
+def fla_cycle_scan_workspace(B, L, d, N, repeats=3) -> int:
+    """Workspace bytes of one fla_cycle_scan call."""
+    n = ctypes.c_size_t()
+    _check(load_library().fla_cycle_scan_workspace(B, L, d, N, repeats, ctypes.byref(n)))
+    return n.value
+
+
+def fla_cycle_scan(x, delta, A, Bm, Cm, y, workspace, workspace_bytes, B, L, d, N, repeats=3, stream=None,
+                   check=True) -> int:
+    """fp32 Cycle-scan through the C ABI.  Tensors or raw device addresses."""
+    rc = load_library().fla_cycle_scan(_ptr(x), _ptr(delta), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(y), _ptr(workspace),
+                                       workspace_bytes, B, L, d, N, repeats, _stream(stream))
+    if check:
+        _check(rc)
+    return rc
+
+
+def fla_cycle_scan_work(B, L, d, N, repeats=3):
+    """(exponentials, bytes) of one Cycle-scan call."""
+    e, b = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().fla_cycle_scan_work(B, L, d, N, repeats, ctypes.byref(e), ctypes.byref(b)))
+    return e.value, b.value
+
+
+def cycle_scan(x, delta, A, Bm, Cm, repeats=3, out=None, stream=None):
+    """Cycle-scan of x [B, L, d] with delta [B, L, d], A [d, N], Bm, Cm [B, L, N] (contiguous fp32
+    device tensors); returns y [B, L, d].  Allocates the output (unless given) and the workspace."""
+    import torch
+    for t in (x, delta, A, Bm, Cm):
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("Cycle-scan tensors must be contiguous float32 device tensors")
+    if x.dim() != 3 or tuple(delta.shape) != tuple(x.shape):
+        raise ValueError("x and delta must be [B, L, d] of one shape")
+    B, L, d = x.shape
+    if A.dim() != 2 or A.shape[0] != d:
+        raise ValueError("A must be [d, N], got %s" % (tuple(A.shape),))
+    N = A.shape[1]
+    for name, t in (("Bm", Bm), ("Cm", Cm)):
+        if tuple(t.shape) != (B, L, N):
+            raise ValueError("%s must be %s, got %s" % (name, (B, L, N), tuple(t.shape)))
+    y = torch.empty_like(x) if out is None else out
+    if tuple(y.shape) != tuple(x.shape) or y.dtype != torch.float32 or not y.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor of x's shape")
+    nws = fla_cycle_scan_workspace(B, L, d, N, repeats)
+    ws = torch.empty(max(nws, 4), dtype=torch.uint8, device=x.device)
+    fla_cycle_scan(x, delta, A, Bm, Cm, y, ws, ws.numel(), B, L, d, N, repeats, stream)
+    return y
+

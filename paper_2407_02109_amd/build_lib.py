@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 SOURCES = ["fla_swin_api.cpp", "fla_swin_bf16.hip", "fla_swin_f32.hip", "fla_swin_bwd_bf16_window.hip",
-           "fla_swin_bwd_bf16_blocks.hip", "fla_swin_bwd_f32.hip", "fla_swin_scratch.hip"]
+           "fla_swin_bwd_bf16_blocks.hip", "fla_swin_bwd_f32.hip", "fla_swin_scratch.hip", "fla_cycle_scan.hip"]
 LIB = os.path.join(PKG, "libfla_swin.so")
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 ALU instructions.

@@ -1,0 +1,194 @@
+// Cycle-scan (HRSAM Sec. 3.5), fp32, gfx950: the selective state-space scan of every
+// channel over the token sequence laid out `repeats` times, the output summed over the copies.
+//
+// Per channel and state (diagonal A, zero-order hold of the SSM equations of Sec. 3.5):
+//   h_t = Abar_t h_{t-1} + Bbar_t x_t,  y_t = sum_n C_t[n] h_t[n],
+//   Abar_t = exp(Delta_t a),  Bbar_t = (exp(Delta_t a) - 1) / a * B_t.
+// The copies are never laid out.  The scan is linear in its initial state, so the state at
+// token t of copy k + 1 is h1_t + P_t S_k, with h1 the scan of one copy from zero, P_t the
+// decay from the sequence start to t and S_k the state at the end of copy k
+// (S_k = (1 + P_L + ... + P_L^{k-1}) S_1).  Summed over the r copies:
+//   sum_k h_t^(k) = r h1_t + P_t G,   G = sum_{j=0}^{r-2} (r-1-j) P_L^j S_1,
+// which is the scan of r x started from G instead of zero.  Over chunks of T tokens:
+//   pass A  (cycle_scan_chunks): every chunk scanned from zero; its end state and its sum of
+//           Delta go to the workspace;
+//   pass B  (cycle_scan_carries): per (batch entry, channel, state), the chunks' carries in
+//           order: the state entering chunk c, H_{c-1}, the state S_1 after the sequence, and
+//           E_c = r H_{c-1} + P(start -> chunk c) G, the state from which chunk c of the summed
+//           scan starts;
+//   pass C  (cycle_scan_outputs): every chunk scanned from E_c with input r x, y written.
+// Two passes of exponentials over the data, where scanning the laid-out copies takes r.
+//
+// A wave takes 64 channels of one chunk: a lane holds one channel's N states in registers;
+// x and Delta of a token are one coalesced 256-byte read per wave, and B_t, C_t, the same for
+// every channel, are wave-uniform reads.  Bound by the vector ALU (one exponential per
+// token, channel and state in each of passes A and C).
+#include "fla_swin_device.h"
+
+namespace fla {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// The N entries of a row of B or C.  The row is the same for the whole wave and read-only
+// for the kernel's life: read through the constant address space, so that it comes in by
+// scalar loads into scalar registers.
+typedef __attribute__((address_space(4))) const float const_float;
+template <int N>
+__device__ __forceinline__ void load_row(const float* p, float (&w)[N]) {
+    const const_float* q = (const const_float*)p;
+#pragma unroll
+    for (int n = 0; n < N; ++n) w[n] = q[n];
+}
+
+template <int N>
+__global__ __launch_bounds__(64) void cycle_scan_chunks(CycleArgs c) {
+    const int cg = blockIdx.x % c.cgroups;
+    const int rest = blockIdx.x / c.cgroups;
+    const int chunk = rest % c.nch;
+    const int b = rest / c.nch;
+    const int ch = cg * 64 + (int)threadIdx.x;
+    const bool ok = ch < c.d;
+    const int chs = ok ? ch : c.d - 1;
+    float a2[N], ia[N], h[N];
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+        const float a = c.A[(size_t)chs * N + n];
+        a2[n] = a * kLog2e;
+        ia[n] = 1.f / a;
+        h[n] = 0.f;
+    }
+    const int t0 = chunk * c.T;
+    const int t1 = min(t0 + c.T, c.L);
+    float sd = 0.f;
+    for (int t = t0; t < t1; ++t) {
+        const size_t row = (size_t)b * c.L + t;
+        const float u = ok ? c.x[row * c.d + ch] : 0.f;
+        const float dl = ok ? c.delta[row * c.d + ch] : 0.f;
+        float w[N];
+        load_row<N>(c.Bm + row * N, w);
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+            const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
+            const float z = u * w[n] * ia[n];
+            h[n] = __builtin_fmaf(dA, h[n] + z, -z);   // dA h + (dA - 1) z
+        }
+        sd += dl;
+    }
+    if (ok) {
+        float* hw = c.ws_h + (((size_t)b * c.nch + chunk) * c.d + ch) * N;
+#pragma unroll
+        for (int n = 0; n < N; ++n) hw[n] = h[n];
+        c.ws_s[((size_t)b * c.nch + chunk) * c.d + ch] = sd;
+    }
+}
+
+// One thread per (batch entry, channel, state): the chunks' carries, in chunk order.
+__global__ __launch_bounds__(256) void cycle_scan_carries(CycleArgs c) {
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long per_b = (long long)c.d * c.N;
+    if (i >= (long long)c.B * per_b) return;
+    const int b = (int)(i / per_b);
+    const int cn = (int)(i - (long long)b * per_b);   // ch * N + n
+    const int ch = cn / c.N;
+    const float a2 = c.A[cn] * kLog2e;
+    const size_t hbase = (size_t)b * c.nch * per_b + cn;              // + chunk * d * N
+    const size_t sbase = (size_t)b * c.nch * c.d + ch;                // + chunk * d
+    // the state after one copy, and the decay over it
+    float H = 0.f, cum = 0.f;
+    for (int k = 0; k < c.nch; ++k) {
+        const float s = c.ws_s[sbase + (size_t)k * c.d];
+        H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * s), H, c.ws_h[hbase + (size_t)k * per_b]);
+        cum += s;
+    }
+    const float PL = __builtin_amdgcn_exp2f(a2 * cum);
+    float g = 0.f;   // sum_{j=0}^{r-2} (r-1-j) PL^j, Horner from the top power
+    for (int j = c.repeats - 2; j >= 0; --j) g = __builtin_fmaf(g, PL, (float)(c.repeats - 1 - j));
+    const float G = g * H;
+    // E_c = r H_{c-1} + P(start -> chunk c) G, over the end states from zero
+    H = 0.f;
+    cum = 0.f;
+    const float r = (float)c.repeats;
+    for (int k = 0; k < c.nch; ++k) {
+        const size_t hi = hbase + (size_t)k * per_b;
+        const float hend = c.ws_h[hi];
+        const float s = c.ws_s[sbase + (size_t)k * c.d];
+        c.ws_h[hi] = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cum), G, r * H);
+        H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * s), H, hend);
+        cum += s;
+    }
+}
+
+template <int N>
+__global__ __launch_bounds__(64) void cycle_scan_outputs(CycleArgs c) {
+    const int cg = blockIdx.x % c.cgroups;
+    const int rest = blockIdx.x / c.cgroups;
+    const int chunk = rest % c.nch;
+    const int b = rest / c.nch;
+    const int ch = cg * 64 + (int)threadIdx.x;
+    const bool ok = ch < c.d;
+    const int chs = ok ? ch : c.d - 1;
+    const float* hw = c.ws_h + (((size_t)b * c.nch + chunk) * c.d + chs) * N;
+    float a2[N], ia[N], h[N];
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+        const float a = c.A[(size_t)chs * N + n];
+        a2[n] = a * kLog2e;
+        ia[n] = 1.f / a;
+        h[n] = hw[n];
+    }
+    const float r = (float)c.repeats;
+    const int t0 = chunk * c.T;
+    const int t1 = min(t0 + c.T, c.L);
+    for (int t = t0; t < t1; ++t) {
+        const size_t row = (size_t)b * c.L + t;
+        const float u = ok ? r * c.x[row * c.d + ch] : 0.f;
+        const float dl = ok ? c.delta[row * c.d + ch] : 0.f;
+        float w[N], cv[N];
+        load_row<N>(c.Bm + row * N, w);
+        load_row<N>(c.Cm + row * N, cv);
+        float acc = 0.f;
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+            const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
+            const float z = u * w[n] * ia[n];
+            h[n] = __builtin_fmaf(dA, h[n] + z, -z);
+            acc = __builtin_fmaf(cv[n], h[n], acc);
+        }
+        if (ok) c.y[row * c.d + ch] = acc;
+    }
+}
+
+template <int N>
+hipError_t launch_n(const CycleArgs& a, hipStream_t stream) {
+    CycleArgs args = a;
+    void* params[] = {&args};
+    const long long scan_groups = (long long)a.B * a.nch * a.cgroups;
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&cycle_scan_chunks<N>), dim3((unsigned)scan_groups),
+                                   dim3(64), params, 0, stream);
+    if (e != hipSuccess) return e;
+    const long long carry_groups = ((long long)a.B * a.d * a.N + 255) / 256;
+    e = hipLaunchKernel(reinterpret_cast<const void*>(&cycle_scan_carries), dim3((unsigned)carry_groups), dim3(256),
+                        params, 0, stream);
+    if (e != hipSuccess) return e;
+    return hipLaunchKernel(reinterpret_cast<const void*>(&cycle_scan_outputs<N>), dim3((unsigned)scan_groups),
+                           dim3(64), params, 0, stream);
+}
+
+}  // namespace
+
+bool cycle_states_supported(int N) { return N == 1 || N == 2 || N == 4 || N == 8 || N == 16 || N == 32; }
+
+hipError_t launch_cycle_scan(const CycleArgs& a, hipStream_t stream) {
+    switch (a.N) {
+        case 1: return launch_n<1>(a, stream);
+        case 2: return launch_n<2>(a, stream);
+        case 4: return launch_n<4>(a, stream);
+        case 8: return launch_n<8>(a, stream);
+        case 16: return launch_n<16>(a, stream);
+        case 32: return launch_n<32>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace fla

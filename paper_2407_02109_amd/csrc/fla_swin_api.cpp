@@ -626,6 +626,106 @@ const char* fla_status_string(int status) {
     }
 }
 
+// ---- Cycle-scan ---------------------------------------------------------------------------
+
+// Sizes of a Cycle-scan call: FLA_ERR_SHAPE for negative sizes or N, repeats below 1; *empty
+// when there is nothing to compute.
+static int cycle_shape(int B, int L, int d, int N, int repeats, bool* empty) {
+    if (B < 0 || L < 0 || d < 0 || N < 1 || repeats < 1) return FLA_ERR_SHAPE;
+    *empty = B == 0 || L == 0 || d == 0;
+    return FLA_OK;
+}
+
+static int cycle_limits(int B, int L, int d, int N) {
+    if (!fla::cycle_states_supported(N)) return FLA_ERR_UNSUPPORTED;
+    if (int64_t(B) * L * d >= kMaxElems || int64_t(B) * L * N >= kMaxElems) return FLA_ERR_TOO_LARGE;
+    const int T = fla::cycle_chunk(L);
+    const int64_t groups = int64_t(B) * ((L + T - 1) / T) * ((d + 63) / 64);
+    if (groups > kMaxGroups || (int64_t(B) * d * N + 255) / 256 > kMaxGroups) return FLA_ERR_TOO_LARGE;
+    return FLA_OK;
+}
+
+int fla_cycle_scan_workspace(int B, int L, int d, int N, int repeats, size_t* bytes) {
+    bool empty = false;
+    int st = cycle_shape(B, L, d, N, repeats, &empty);
+    if (st != FLA_OK) return st;
+    if (!bytes) return FLA_ERR_NULL;
+    if (empty) {
+        *bytes = 0;
+        return FLA_OK;
+    }
+    st = cycle_limits(B, L, d, N);
+    if (st != FLA_OK) return st;
+    *bytes = (size_t)fla::cycle_workspace_floats(B, L, d, N) * 4;
+    return FLA_OK;
+}
+
+int fla_cycle_scan_work(int B, int L, int d, int N, int repeats, double* exps, double* bytes) {
+    bool empty = false;
+    int st = cycle_shape(B, L, d, N, repeats, &empty);
+    if (st != FLA_OK) return st;
+    if (!exps || !bytes) return FLA_ERR_NULL;
+    // one exponential exp(Delta a) per (batch entry, token, channel, state) of the
+    // definition; every input read and the output written once
+    *exps = double(B) * L * d * N;
+    *bytes = 4.0 * (3.0 * B * L * d + 2.0 * B * L * N + double(d) * N);
+    return FLA_OK;
+}
+
+int fla_cycle_scan(const float* x, const float* delta, const float* A, const float* Bm, const float* Cm,
+                   float* y, void* workspace, size_t workspace_bytes, int B, int L, int d, int N,
+                   int repeats, hipStream_t stream) {
+    bool empty = false;
+    int st = cycle_shape(B, L, d, N, repeats, &empty);
+    if (st != FLA_OK) return st;
+    if (empty) return FLA_OK;
+    if (!x || !delta || !A || !Bm || !Cm || !y) return FLA_ERR_NULL;
+    const void* ptrs[] = {x, delta, A, Bm, Cm, y, workspace};
+    for (const void* p : ptrs)
+        if (reinterpret_cast<uintptr_t>(p) & 3u) return FLA_ERR_ALIGN;
+    st = cycle_limits(B, L, d, N);
+    if (st != FLA_OK) return st;
+    const int64_t need = fla::cycle_workspace_floats(B, L, d, N) * 4;
+    if (!workspace || workspace_bytes < (size_t)need) return FLA_ERR_WORKSPACE;
+    const int64_t xd = int64_t(B) * L * d * 4, bn = int64_t(B) * L * N * 4, an = int64_t(d) * N * 4;
+    struct Range {
+        const void* p;
+        int64_t n;
+    };
+    const Range inputs[] = {{x, xd}, {delta, xd}, {A, an}, {Bm, bn}, {Cm, bn}};
+    const Range outputs[] = {{y, xd}, {workspace, need}};
+    for (int i = 0; i < 2; ++i) {
+        for (const Range& r : inputs)
+            if (overlaps(outputs[i].p, outputs[i].n, r.p, r.n)) return FLA_ERR_ALIAS;
+        if (i == 1 && overlaps(outputs[1].p, outputs[1].n, outputs[0].p, outputs[0].n)) return FLA_ERR_ALIAS;
+    }
+    int cus = 0;
+    st = check_arch(&cus);
+    if (st != FLA_OK) return st;
+    fla::CycleArgs a{};
+    a.x = x;
+    a.delta = delta;
+    a.A = A;
+    a.Bm = Bm;
+    a.Cm = Cm;
+    a.y = y;
+    a.T = fla::cycle_chunk(L);
+    a.nch = (L + a.T - 1) / a.T;
+    a.cgroups = (d + 63) / 64;
+    a.ws_h = static_cast<float*>(workspace);
+    a.ws_s = a.ws_h + int64_t(B) * a.nch * d * N;
+    a.B = B;
+    a.L = L;
+    a.d = d;
+    a.N = N;
+    a.repeats = repeats;
+    if (fla::launch_cycle_scan(a, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        return FLA_ERR_LAUNCH;
+    }
+    return FLA_OK;
+}
+
 int fla_swin_attn_work(int B, int heads, int Hgrid, int Wgrid, int head_dim, int window,
                        int shift, int pad_mode, int elem_bytes, double* flops, double* bytes) {
     const int hw[2] = {Hgrid, Wgrid};

@@ -1,4 +1,4 @@
-"""Seeded synthetic inputs for Flash Swin attention.
+"""Seeded synthetic inputs for Flash Swin attention and for Cycle-scan.
 
 This module draws random numbers and nothing else: it holds none of the attention
 arithmetic, so both the GPU tests and the fp64 oracle can consume its output.
@@ -182,3 +182,49 @@ def random_queries(wl: Workload, n: int, seed: int):
                 corners.append((bb, yy, xx))
     pts.append(torch.tensor(corners, dtype=torch.int64))
     return torch.cat(pts, dim=0)
+
+
+# ---- Cycle-scan (Sec. 3.5) ----------------------------------------------------------------
+
+@dataclass(frozen=True)
+class CycleWorkload:
+    name: str
+    B: int
+    L: int          # tokens
+    d: int          # channels
+    N: int          # states per channel
+    repeats: int    # copies of the sequence (3 in the paper)
+    seed: int
+    kind: str = "mamba"
+    note: str = field(default="", compare=False)
+
+
+CYCLE_WORKLOADS = {
+    "cyclescan_img4096": CycleWorkload(
+        "cyclescan_img4096", 1, 256 * 256, 768, 32, 3, 21,
+        note="4096^2 image: 256x256 tokens of the ViT-B width 768, 32 states (Sec. 3.5, App. D), three copies"),
+    "cyclescan_img1024": CycleWorkload(
+        "cyclescan_img1024", 1, 64 * 64, 768, 32, 3, 22, note="1024^2 image: 64x64 tokens"),
+}
+
+
+def make_cycle_inputs(B, L, d, N, seed, kind="mamba", device="cpu"):
+    """(x, delta, A, Bm, Cm) as fp32 tensors: x, delta [B, L, d]; A [d, N]; Bm, Cm [B, L, N].
+    kind "mamba" follows Mamba's initialisation: step sizes log-uniform in [0.001, 0.1],
+    A = -(1, 2, ..., N) for every channel (the real S4D start), x, B, C i.i.d. N(0, 1).
+    kind "wide": step sizes exp(N(-1.5, 0.5)), A uniform in [-3, -0.25] per entry."""
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn(B, L, d, generator=g)
+    Bm = torch.randn(B, L, N, generator=g)
+    Cm = torch.randn(B, L, N, generator=g)
+    if kind == "mamba":
+        u = torch.rand(B, L, d, generator=g)
+        delta = torch.exp(torch.log(torch.tensor(1e-3)) + u * (torch.log(torch.tensor(1e-1)) - torch.log(torch.tensor(1e-3))))
+        A = -torch.arange(1, N + 1, dtype=torch.float32).repeat(d, 1)
+    elif kind == "wide":
+        delta = torch.exp(-1.5 + 0.5 * torch.randn(B, L, d, generator=g))
+        A = -(0.25 + 2.75 * torch.rand(d, N, generator=g))
+    else:
+        raise ValueError(kind)
+    return tuple(t.to(torch.float32).contiguous().to(device) for t in (x, delta, A, Bm, Cm))
+

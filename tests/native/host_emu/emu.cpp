@@ -1,5 +1,6 @@
 // The launch emulation behind hip_runtime.h (see there), a device that reports gfx950, and
-// stand-ins for the bf16 launchers (which the host build does not contain).
+// stand-ins for the bf16 launchers (which the host build does not contain; it builds the fp32
+// attention kernels and the Cycle-scan kernels).
 #include <barrier>
 #include <thread>
 #include <vector>
@@ -23,7 +24,7 @@ hipError_t hipGetLastError() { return hipSuccess; }
 
 // every kernel the host build launches takes one argument struct; which one is told by the
 // caller (emu_kernel_args) before each API call
-int emu_kernel_args = 0;   // 0: SwinArgs, 1: SwinBwdArgs
+int emu_kernel_args = 0;   // 0: SwinArgs, 1: SwinBwdArgs, 2: CycleArgs
 
 hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, size_t, hipStream_t) {
     std::barrier<> bar((std::ptrdiff_t)block.x);
@@ -37,9 +38,12 @@ hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, s
                 blockIdx = {b, 0, 0};
                 if (emu_kernel_args == 0)
                     reinterpret_cast<void (*)(fla::SwinArgs)>(const_cast<void*>(fn))(*static_cast<fla::SwinArgs*>(args[0]));
-                else
+                else if (emu_kernel_args == 1)
                     reinterpret_cast<void (*)(fla::SwinBwdArgs)>(const_cast<void*>(fn))(
                         *static_cast<fla::SwinBwdArgs*>(args[0]));
+                else
+                    reinterpret_cast<void (*)(fla::CycleArgs)>(const_cast<void*>(fn))(
+                        *static_cast<fla::CycleArgs*>(args[0]));
             });
         for (auto& th : threads) th.join();
     }

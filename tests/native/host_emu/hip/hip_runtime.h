@@ -39,6 +39,7 @@ inline float2 make_float2(float a, float b) { return float2{a, b}; }
 
 typedef int hipError_t;
 constexpr hipError_t hipSuccess = 0;
+constexpr hipError_t hipErrorInvalidValue = 1;
 typedef void* hipStream_t;
 struct hipDeviceProp_t {
     char gcnArchName[256];

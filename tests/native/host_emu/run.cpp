@@ -2,8 +2,10 @@
 // emulation, with every buffer an exact-size heap allocation (AddressSanitizer reports any
 // access outside), and writes inputs and outputs as raw float32 files for the test to compare
 // with the oracle.
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 #include <random>
 
 #include "fla_swin.h"
@@ -25,7 +27,46 @@ static void dump(const char* dir, const char* name, const float* p, size_t n) {
     std::fclose(f);
 }
 
+// Cycle-scan through the C ABI: run cycle B L d N repeats outdir
+static int run_cycle(int argc, char** argv) {
+    if (argc != 8) {
+        std::fprintf(stderr, "usage: run cycle B L d N repeats outdir\n");
+        return 2;
+    }
+    const int B = std::atoi(argv[2]), L = std::atoi(argv[3]), d = std::atoi(argv[4]), N = std::atoi(argv[5]);
+    const int r = std::atoi(argv[6]);
+    const char* dir = argv[7];
+    const size_t nx = (size_t)B * L * d, nb = (size_t)B * L * N, na = (size_t)d * N;
+    std::mt19937 g(4321);
+    float* x = alloc_random(nx, g);
+    float* delta = alloc_random(nx, g);
+    float* A = alloc_random(na, g);
+    float* Bm = alloc_random(nb, g);
+    float* Cm = alloc_random(nb, g);
+    float* y = alloc_random(nx, g);
+    for (size_t i = 0; i < nx; ++i) delta[i] = std::log1p(std::exp(delta[i] - 2.f));   // positive steps
+    for (size_t i = 0; i < na; ++i) A[i] = -0.25f - std::fabs(A[i]);                   // negative diagonal
+    size_t nws = 0;
+    if (fla_cycle_scan_workspace(B, L, d, N, r, &nws) != 0) return 1;
+    void* ws = std::aligned_alloc(16, ((nws + 15) / 16) * 16);
+    emu_kernel_args = 2;
+    const int rc = fla_cycle_scan(x, delta, A, Bm, Cm, y, ws, nws, B, L, d, N, r, nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "cycle scan: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    dump(dir, "x", x, nx);
+    dump(dir, "delta", delta, nx);
+    dump(dir, "A", A, na);
+    dump(dir, "Bm", Bm, nb);
+    dump(dir, "Cm", Cm, nb);
+    dump(dir, "y", y, nx);
+    std::printf("ok\n");
+    return 0;
+}
+
 int main(int argc, char** argv) {
+    if (argc > 1 && std::strcmp(argv[1], "cycle") == 0) return run_cycle(argc, argv);
     if (argc != 9) {
         std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
         return 2;

@@ -43,7 +43,8 @@ def test_header_declares_the_entry_points():
         "fla_swin_attn_ms_fwd_lse_f32", "fla_swin_attn_bwd_workspace", "fla_swin_attn_bwd",
         "fla_swin_attn_bwd_f32", "fla_swin_attn_ms_bwd", "fla_swin_attn_ms_bwd_f32",
         "fla_swin_attn_bwd_work", "fla_swin_attn_rope_fwd", "fla_swin_attn_rope_fwd_f32",
-        "fla_swin_attn_rope_fwd_lse", "fla_swin_attn_rope_bwd", "fla_swin_attn_bwd_noalloc"])
+        "fla_swin_attn_rope_fwd_lse", "fla_swin_attn_rope_bwd", "fla_swin_attn_bwd_noalloc",
+        "fla_cycle_scan", "fla_cycle_scan_workspace", "fla_cycle_scan_work"])
 
 
 def test_library_exports_every_header_symbol(lib):
@@ -616,3 +617,88 @@ def test_swin_attention_rope_takes_one_grid():
     q = _FakeCuda((1, 80, 2, 64))
     with pytest.raises(ValueError):
         fb.swin_attention(q, q, q, [(8, 8), (4, 4)], 4, 0, 0, rope=(1e4, 1.0))
+
+
+# ---- Cycle-scan ------------------------------------------------------------------------------
+
+_CS_BASE = 1 << 40   # fake device addresses, far apart (nothing is dereferenced)
+
+
+def _cs_call(B=1, L=100, d=64, N=32, repeats=3, **over):
+    nx, nb, na = B * L * d * 4, B * L * N * 4, d * N * 4
+    p = {"x": _CS_BASE, "delta": _CS_BASE + (1 << 36), "A": _CS_BASE + (2 << 36), "Bm": _CS_BASE + (3 << 36),
+         "Cm": _CS_BASE + (4 << 36), "y": _CS_BASE + (5 << 36), "ws": _CS_BASE + (6 << 36), "ws_bytes": 1 << 34}
+    p.update(over)
+    return fb.load_library().fla_cycle_scan(p["x"], p["delta"], p["A"], p["Bm"], p["Cm"], p["y"], p["ws"],
+                                            p["ws_bytes"], B, L, d, N, repeats, None)
+
+
+def _st(name):
+    return _header_enum("FLA")[name]
+
+
+@pytest.mark.parametrize("status,kw", [
+    ("FLA_ERR_SHAPE", dict(B=-1)), ("FLA_ERR_SHAPE", dict(L=-1)), ("FLA_ERR_SHAPE", dict(d=-1)),
+    ("FLA_ERR_SHAPE", dict(N=0)), ("FLA_ERR_SHAPE", dict(repeats=0)),
+    ("FLA_ERR_NULL", dict(x=None)), ("FLA_ERR_NULL", dict(Cm=None)), ("FLA_ERR_NULL", dict(y=None)),
+    ("FLA_ERR_ALIGN", dict(delta=_CS_BASE + (1 << 36) + 2)), ("FLA_ERR_ALIGN", dict(ws=_CS_BASE + (6 << 36) + 1)),
+    ("FLA_ERR_UNSUPPORTED", dict(N=3)), ("FLA_ERR_UNSUPPORTED", dict(N=64)),
+    ("FLA_ERR_TOO_LARGE", dict(B=1 << 10, L=1 << 20, d=1 << 10)),
+    ("FLA_ERR_WORKSPACE", dict(ws=None)), ("FLA_ERR_WORKSPACE", dict(ws_bytes=16)),
+    ("FLA_ERR_ALIAS", dict(y=_CS_BASE + 4)), ("FLA_ERR_ALIAS", dict(ws=_CS_BASE + (5 << 36) + 64)),
+    ("FLA_ERR_ALIAS", dict(y=_CS_BASE + (2 << 36))),
+])
+def test_cycle_scan_argument_checks(lib, status, kw):
+    assert _cs_call(**kw) == _st(status), kw
+
+
+def test_cycle_scan_check_order(lib):
+    # shape before null, null before alignment, alignment before the state count, ...
+    assert _cs_call(N=0, x=None) == _st("FLA_ERR_SHAPE")
+    assert _cs_call(x=None, delta=_CS_BASE + 2) == _st("FLA_ERR_NULL")
+    assert _cs_call(N=3, delta=_CS_BASE + (1 << 36) + 2) == _st("FLA_ERR_ALIGN")
+    assert _cs_call(N=3, ws=None) == _st("FLA_ERR_UNSUPPORTED")
+    assert _cs_call(ws=None, y=_CS_BASE) == _st("FLA_ERR_WORKSPACE")
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(L=0), dict(d=0)])
+def test_cycle_scan_empty_is_ok_and_ignores_pointers(lib, kw):
+    assert _cs_call(x=None, delta=None, A=None, Bm=None, Cm=None, y=None, ws=None, ws_bytes=0, **kw) == 0
+
+
+def test_cycle_scan_inputs_may_alias(lib):
+    # x, delta, Bm and Cm may share memory (they are only read); the outputs may not
+    if not _gpu_visible():
+        assert _cs_call(delta=_CS_BASE, Bm=_CS_BASE, Cm=_CS_BASE) == _st("FLA_ERR_ARCH")
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+def test_cycle_scan_no_device_reports_arch(lib):
+    assert _cs_call() == _st("FLA_ERR_ARCH")
+
+
+@pytest.mark.parametrize("B,L,d,N", [(1, 65536, 768, 32), (2, 37, 70, 4), (1, 1, 1, 1), (3, 5000, 5, 16),
+                                     (1, 2048, 64, 8), (1, 2049, 64, 8)])
+def test_cycle_scan_workspace_size(lib, B, L, d, N):
+    # chunks of T tokens, T the smallest power of two from 32 to 256 giving at most 64 chunks
+    # (256 tokens past 16384); (N + 1) floats per (batch entry, chunk, channel)
+    T = 32
+    while T < 256 and T * 64 < L:
+        T *= 2
+    nch = -(-L // T)
+    assert fb.fla_cycle_scan_workspace(B, L, d, N, 3) == 4 * B * nch * d * (N + 1)
+
+
+def test_cycle_scan_workspace_errors(lib):
+    n = ctypes.c_size_t()
+    assert lib.fla_cycle_scan_workspace(1, 10, 4, 4, 3, None) == _st("FLA_ERR_NULL")
+    assert lib.fla_cycle_scan_workspace(-1, 10, 4, 4, 3, ctypes.byref(n)) == _st("FLA_ERR_SHAPE")
+    assert lib.fla_cycle_scan_workspace(1, 10, 4, 5, 3, ctypes.byref(n)) == _st("FLA_ERR_UNSUPPORTED")
+    assert lib.fla_cycle_scan_workspace(0, 10, 4, 4, 3, ctypes.byref(n)) == 0 and n.value == 0
+
+
+def test_cycle_scan_work_counts(lib):
+    e, b = fb.fla_cycle_scan_work(2, 1000, 96, 16, 3)
+    assert e == 2 * 1000 * 96 * 16
+    assert b == 4 * (3 * 2 * 1000 * 96 + 2 * 2 * 1000 * 16 + 96 * 16)
+

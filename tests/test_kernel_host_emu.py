@@ -40,13 +40,15 @@ def emu_binary(tmp_path_factory):
     # include finds it first
     shutil.copy(os.path.join(CSRC, "fla_swin_bwd_f32.hip"), src / "fla_swin_bwd_f32.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_f32.hip"), src / "fla_swin_f32.cpp")
+    shutil.copy(os.path.join(CSRC, "fla_cycle_scan.hip"), src / "fla_cycle_scan.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_api.cpp"), src / "fla_swin_api.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_internal.h"), src / "fla_swin_internal.h")
     shutil.copy(os.path.join(EMU, "fla_swin_device.h"), src / "fla_swin_device.h")
     exe = str(d / "run")
     cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-pthread",
            "-I", EMU, "-I", str(src), "-I", os.path.join(ROOT, "include"),
-           str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_swin_api.cpp"),
+           str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_cycle_scan.cpp"),
+           str(src / "fla_swin_api.cpp"),
            os.path.join(EMU, "emu.cpp"), os.path.join(EMU, "run.cpp"), "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     if r.returncode != 0:
@@ -87,3 +89,31 @@ def test_fp32_kernels_on_the_host(emu_binary, tmp_path, case):
     for name, got, ref in zip(("dq", "dk", "dv"), (ld("dq", L), ld("dk", rows), ld("dv", rows)), refs):
         m = max(1.0, np.abs(ref).max())
         assert np.abs(got - ref).max() <= 2e-5 * m, name
+
+
+CYCLE_CASES = [  # B, L, d, N, repeats
+    (2, 37, 70, 4, 3),     # two chunks (the second of 5 tokens), channels past a multiple of 64
+    (1, 200, 64, 32, 3),   # 32 states, seven chunks
+    (1, 65, 5, 1, 2),      # one state, three chunks, two copies
+    (2, 33, 3, 16, 1),     # one copy: the plain scan
+    (1, 3000, 8, 8, 4),    # chunks of 64 tokens, four copies
+]
+
+
+@pytest.mark.parametrize("case", CYCLE_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_cycle_scan_kernels_on_the_host(emu_binary, tmp_path, case):
+    """The Cycle-scan kernels (their unmodified source, built for the host with
+    AddressSanitizer on exact-size buffers) against the oracle's definition."""
+    from oracle import cycle_scan as CS
+    B, L, d, N, r = case
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
+    res = subprocess.run([emu_binary, "cycle", *map(str, case), str(tmp_path)], capture_output=True, text=True,
+                         timeout=900, env=env)
+    assert res.returncode == 0 and "ok" in res.stdout, res.stderr[-4000:]
+    ld = lambda name, shape: np.fromfile(str(tmp_path / (name + ".f32")), dtype=np.float32).astype(np.float64).reshape(shape)
+    x, delta, y = ld("x", (B, L, d)), ld("delta", (B, L, d)), ld("y", (B, L, d))
+    A, Bm, Cm = ld("A", (d, N)), ld("Bm", (B, L, N)), ld("Cm", (B, L, N))
+    ref = CS.cycle_scan(x, delta, A, Bm, Cm, r)
+    err = np.abs(y - ref).max() / max(1.0, np.abs(ref).max())
+    assert err <= 1e-4, err
+
