@@ -29,6 +29,8 @@ namespace fla {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kBatch = 32;   // chunk values per load batch of the carry pass
+constexpr int kTokens = 4;   // tokens whose x and Delta the scan passes load together
 
 // The N entries of a row of B or C.  The row is the same for the whole wave and read-only
 // for the kernel's life: read through the constant address space, so that it comes in by
@@ -50,35 +52,53 @@ __global__ __launch_bounds__(64) void cycle_scan_chunks(CycleArgs c) {
     const int ch = cg * 64 + (int)threadIdx.x;
     const bool ok = ch < c.d;
     const int chs = ok ? ch : c.d - 1;
-    float a2[N], ia[N], h[N];
+    // the state scaled by a, g = a h, takes one product less per step:
+    // g <- dA g + (dA - 1) u b
+    float a2[N], g[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) {
-        const float a = c.A[(size_t)chs * N + n];
-        a2[n] = a * kLog2e;
-        ia[n] = 1.f / a;
-        h[n] = 0.f;
+        a2[n] = c.A[(size_t)chs * N + n] * kLog2e;
+        g[n] = 0.f;
     }
     const int t0 = chunk * c.T;
     const int t1 = min(t0 + c.T, c.L);
+    const float* xp = c.x + (size_t)b * c.L * c.d + chs;
+    const float* dp = c.delta + (size_t)b * c.L * c.d + chs;
+    const float* bp = c.Bm + (size_t)b * c.L * N;
     float sd = 0.f;
-    for (int t = t0; t < t1; ++t) {
-        const size_t row = (size_t)b * c.L + t;
-        const float u = ok ? c.x[row * c.d + ch] : 0.f;
-        const float dl = ok ? c.delta[row * c.d + ch] : 0.f;
+    auto step = [&](int t, float u, float dl) {
         float w[N];
-        load_row<N>(c.Bm + row * N, w);
+        load_row<N>(bp + (size_t)t * N, w);
 #pragma unroll
         for (int n = 0; n < N; ++n) {
             const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
-            const float z = u * w[n] * ia[n];
-            h[n] = __builtin_fmaf(dA, h[n] + z, -z);   // dA h + (dA - 1) z
+            const float z = u * w[n];
+            g[n] = __builtin_fmaf(dA, g[n] + z, -z);   // dA g + (dA - 1) z
         }
         sd += dl;
+    };
+    // whole groups of kTokens tokens: their x and Delta loaded together, one wait per group
+    const int tfull = t0 + (t1 - t0) / kTokens * kTokens;
+    for (int tg = t0; tg < tfull; tg += kTokens) {
+        float uu[kTokens], dd[kTokens];
+#pragma unroll
+        for (int j = 0; j < kTokens; ++j) {
+            uu[j] = xp[(size_t)(tg + j) * c.d];
+            dd[j] = dp[(size_t)(tg + j) * c.d];
+        }
+#pragma unroll
+        for (int j = 0; j < kTokens; ++j) step(tg + j, uu[j], dd[j]);
     }
+    for (int t = tfull; t < t1; ++t) step(t, xp[(size_t)t * c.d], dp[(size_t)t * c.d]);
     if (ok) {
+        // A is read in full before any store (a store to the workspace could alias it, so
+        // interleaved, every load would wait for the store before it)
+        float a[N];
+#pragma unroll
+        for (int n = 0; n < N; ++n) a[n] = c.A[(size_t)ch * N + n];
         float* hw = c.ws_h + (((size_t)b * c.nch + chunk) * c.d + ch) * N;
 #pragma unroll
-        for (int n = 0; n < N; ++n) hw[n] = h[n];
+        for (int n = 0; n < N; ++n) hw[n] = g[n] / a[n];
         c.ws_s[((size_t)b * c.nch + chunk) * c.d + ch] = sd;
     }
 }
@@ -94,12 +114,23 @@ __global__ __launch_bounds__(256) void cycle_scan_carries(CycleArgs c) {
     const float a2 = c.A[cn] * kLog2e;
     const size_t hbase = (size_t)b * c.nch * per_b + cn;              // + chunk * d * N
     const size_t sbase = (size_t)b * c.nch * c.d + ch;                // + chunk * d
-    // the state after one copy, and the decay over it
+    // the state after one copy, and the decay over it; the chunks' values come in batches of
+    // kBatch loads issued before the recurrence over them (one memory round trip per batch)
     float H = 0.f, cum = 0.f;
-    for (int k = 0; k < c.nch; ++k) {
-        const float s = c.ws_s[sbase + (size_t)k * c.d];
-        H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * s), H, c.ws_h[hbase + (size_t)k * per_b]);
-        cum += s;
+    for (int k0 = 0; k0 < c.nch; k0 += kBatch) {
+        float sv[kBatch], hv[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int k = min(k0 + j, c.nch - 1);
+            sv[j] = c.ws_s[sbase + (size_t)k * c.d];
+            hv[j] = c.ws_h[hbase + (size_t)k * per_b];
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (k0 + j < c.nch) {
+                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[j]), H, hv[j]);
+                cum += sv[j];
+            }
     }
     const float PL = __builtin_amdgcn_exp2f(a2 * cum);
     float g = 0.f;   // sum_{j=0}^{r-2} (r-1-j) PL^j, Horner from the top power
@@ -109,13 +140,21 @@ __global__ __launch_bounds__(256) void cycle_scan_carries(CycleArgs c) {
     H = 0.f;
     cum = 0.f;
     const float r = (float)c.repeats;
-    for (int k = 0; k < c.nch; ++k) {
-        const size_t hi = hbase + (size_t)k * per_b;
-        const float hend = c.ws_h[hi];
-        const float s = c.ws_s[sbase + (size_t)k * c.d];
-        c.ws_h[hi] = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cum), G, r * H);
-        H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * s), H, hend);
-        cum += s;
+    for (int k0 = 0; k0 < c.nch; k0 += kBatch) {
+        float sv[kBatch], hv[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int k = min(k0 + j, c.nch - 1);
+            sv[j] = c.ws_s[sbase + (size_t)k * c.d];
+            hv[j] = c.ws_h[hbase + (size_t)k * per_b];
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (k0 + j < c.nch) {
+                c.ws_h[hbase + (size_t)(k0 + j) * per_b] = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cum), G, r * H);
+                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[j]), H, hv[j]);
+                cum += sv[j];
+            }
     }
 }
 
@@ -140,23 +179,39 @@ __global__ __launch_bounds__(64) void cycle_scan_outputs(CycleArgs c) {
     const float r = (float)c.repeats;
     const int t0 = chunk * c.T;
     const int t1 = min(t0 + c.T, c.L);
-    for (int t = t0; t < t1; ++t) {
-        const size_t row = (size_t)b * c.L + t;
-        const float u = ok ? r * c.x[row * c.d + ch] : 0.f;
-        const float dl = ok ? c.delta[row * c.d + ch] : 0.f;
+    const float* xp = c.x + (size_t)b * c.L * c.d + chs;
+    const float* dp = c.delta + (size_t)b * c.L * c.d + chs;
+    const size_t rb = (size_t)b * c.L;
+    auto step = [&](int t, float xv, float dl) {
+        const size_t row = rb + t;
+        const float u = r * xv;
         float w[N], cv[N];
         load_row<N>(c.Bm + row * N, w);
         load_row<N>(c.Cm + row * N, cv);
-        float acc = 0.f;
+        float acc[2] = {0.f, 0.f};   // two sums, two dependency chains
 #pragma unroll
         for (int n = 0; n < N; ++n) {
             const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
             const float z = u * w[n] * ia[n];
             h[n] = __builtin_fmaf(dA, h[n] + z, -z);
-            acc = __builtin_fmaf(cv[n], h[n], acc);
+            acc[n & 1] = __builtin_fmaf(cv[n], h[n], acc[n & 1]);
         }
-        if (ok) c.y[row * c.d + ch] = acc;
+        // lanes past the last channel compute channel d - 1 from the same inputs: the value
+        // they store there is the same
+        c.y[row * c.d + chs] = acc[0] + acc[1];
+    };
+    const int tfull = t0 + (t1 - t0) / kTokens * kTokens;
+    for (int tg = t0; tg < tfull; tg += kTokens) {
+        float uu[kTokens], dd[kTokens];
+#pragma unroll
+        for (int j = 0; j < kTokens; ++j) {
+            uu[j] = xp[(size_t)(tg + j) * c.d];
+            dd[j] = dp[(size_t)(tg + j) * c.d];
+        }
+#pragma unroll
+        for (int j = 0; j < kTokens; ++j) step(tg + j, uu[j], dd[j]);
     }
+    for (int t = tfull; t < t1; ++t) step(t, xp[(size_t)t * c.d], dp[(size_t)t * c.d]);
 }
 
 template <int N>
