@@ -9,8 +9,10 @@ resident in HBM before timing starts.
 
 Prints one JSON line: microseconds per layer (the headline), TFLOP/s and the fraction of
 the bf16 matrix-core peak, the HBM roofline of the kernel, the fp64 CPU oracle timed on
-this host as a baseline, and a "backward" object: the same layer's training forward and
-backward pass (dq, dk, dv) with their own roofline.
+this host as a baseline, a "backward" object: the same layer's training forward and
+backward pass (dq, dk, dv) with their own roofline, and a "cycle_scan" object: HRSAM's
+Cycle-scan (Sec. 3.5) over the token sequence of a 4096^2 image (65536 tokens, 768 channels,
+32 states, three copies), with its vector-ALU roofline and the oracle timed on a sample.
 
 Headline mode.  A layer whose bytes exceed the 256 MB last-level cache (MALL) is timed
 cold: before each timed call a read-only pass over a 1 GiB buffer evicts the inputs from
@@ -36,6 +38,9 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+# transcendental rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, exponentials at a quarter of
+# the plain fp32 rate
+PEAK_EXP_TPS = 256 * 4 * 16 * 2.4e9 / 4 / 1e12
 SIMDS = 256 * 4               # MI355X: 256 compute units of 4 SIMDs
 XCDS = 8                      # accelerator complex dies; rocprofv3 sums GRBM_GUI_ACTIVE over them
 MALL_BYTES = 256 << 20        # MI355X last-level (Infinity) cache
@@ -49,6 +54,10 @@ KERNELS = {
                               "paper_2407_02109_amd/csrc/fla_swin_bwd_bf16_blocks.hip",
                               "paper_2407_02109_amd/csrc/fla_swin_internal.h",
                               "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
+    "cycle": ("cycle_scan", ["paper_2407_02109_amd/csrc/fla_cycle_scan.hip",
+                             "paper_2407_02109_amd/csrc/fla_cycle_scan.h",
+                             "paper_2407_02109_amd/csrc/fla_swin_internal.h",
+                             "paper_2407_02109_amd/csrc/fla_swin_device.h"]),
 }
 
 
@@ -219,6 +228,81 @@ def summarize(prof_dir: str, workload: str, command: str, leg: str = "fwd", out_
                        "avg_duration_us": st.mean(durs) / 1e3 if durs else None,
                        "avg_cold_us": st.mean(cold_durs) / 1e3 if cold_durs else None,
                        "avg_warm_us": st.mean(warm_durs) / 1e3 if warm_durs else None}, f, indent=1)
+    print("\n".join(lines))
+
+
+def summarize_cycle(prof_dir: str, command: str, out_dir: str = ""):
+    """rocprofv3 CSV output of a bench run into profiles/cycle_scan_cyclescan_img4096.md: per
+    Cycle-scan kernel (chunk scans, carries, output scans) the launches, their average
+    duration cold (right after the read-only flush) and warm, and, when the FETCH_SIZE /
+    WRITE_SIZE passes are there, HBM bytes per launch scaled by the 512 MiB copy."""
+    out_dir = out_dir or os.path.join(ROOT, "profiles")
+    import csv
+    import glob
+    import statistics as st
+
+    def rows(pattern):
+        out = []
+        for path in glob.glob(os.path.join(prof_dir, pattern), recursive=True):
+            with open(path) as f:
+                out.extend(csv.DictReader(f))
+        return out
+
+    def short(name):
+        m = re.search(r"(cycle_scan_\w+(?:<\d+>)?)", name)
+        return m.group(1) if m else None
+
+    all_rows = sorted(rows("trace/**/*kernel_trace.csv"), key=lambda r: int(r["Start_Timestamp"]))
+    durs = collections.defaultdict(lambda: ([], []))   # kernel -> (cold, warm) durations in ns
+    prev, cold_call = None, False
+    for r in all_rows:
+        k = short(r["Kernel_Name"])
+        if k is None:
+            prev = r
+            continue
+        if k.startswith("cycle_scan_chunks"):   # a call starts with its chunk scans
+            cold_call = prev is not None and "reduce_kernel" in prev["Kernel_Name"] and "at::native" in prev["Kernel_Name"]
+        durs[k][0 if cold_call else 1].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        prev = r
+    counters = collections.defaultdict(dict)
+    copies = {}
+    for name in ("FETCH_SIZE", "WRITE_SIZE"):
+        per, per_copy = collections.defaultdict(dict), {}
+        for r in rows("%s/**/*counter_collection.csv" % name.lower()):
+            if r["Counter_Name"] != name:
+                continue
+            k = short(r["Kernel_Name"])
+            if k is not None:
+                per[k][r["Dispatch_Id"]] = per[k].get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+            elif "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= 65536:
+                per_copy[r["Dispatch_Id"]] = per_copy.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        for k, d in per.items():
+            counters[k][name] = st.median(d.values())
+        copies[name] = st.median(per_copy.values()) if per_copy else None
+    scale = {n: (512 << 20) / (copies[n] * 1024) if copies.get(n) else None for n in ("FETCH_SIZE", "WRITE_SIZE")}
+    lines = ["# rocprofv3 summary: Cycle-scan kernels, workload cyclescan_img4096 "
+             "(65536 tokens, 768 channels, 32 states, 3 copies)", "",
+             "Command (run from the repository root on the GPU host):", "", "```", command, "```", "",
+             "| kernel | cold launches | cold avg us | warm launches | warm avg us | HBM fetch MB | HBM write MB |",
+             "|---|---|---|---|---|---|---|"]
+    total = [0.0, 0.0]
+    for k in sorted(durs, key=lambda k: ("chunks" not in k, "carries" not in k)):
+        cold, warm = durs[k]
+        c = st.mean(cold) / 1e3 if cold else None
+        w = st.mean(warm) / 1e3 if warm else None
+        total[0] += c or 0.0
+        total[1] += w or 0.0
+        mb = lambda n: ("%.1f" % (counters[k][n] * 1024 * scale[n] / 1e6)) if counters[k].get(n) and scale[n] else "-"
+        lines.append("| %s | %d | %s | %d | %s | %s | %s |" % (k, len(cold), "%.2f" % c if c else "-", len(warm),
+                                                               "%.2f" % w if w else "-", mb("FETCH_SIZE"), mb("WRITE_SIZE")))
+    lines += ["| sum (one call) | | %.2f | | %.2f | | |" % tuple(total), "",
+              "Copy calibration (512 MiB device copy, KiB per dispatch): FETCH_SIZE %s, WRITE_SIZE %s"
+              % (copies.get("FETCH_SIZE"), copies.get("WRITE_SIZE")),
+              "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (scale["FETCH_SIZE"], scale["WRITE_SIZE"]),
+              "Kernel source hash: %s" % kernel_hash("cycle"), ""]
+    os.makedirs(out_dir, exist_ok=True)
+    with open(os.path.join(out_dir, "cycle_scan_cyclescan_img4096.md"), "w") as f:
+        f.write("\n".join(lines))
     print("\n".join(lines))
 
 
@@ -446,6 +530,72 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int, mode: str, 
                        "cold_p50_us": c50, "cold_p90_us": c90}}
 
 
+def cycle_scan_leg(binding, synth, stream, steps: int, flush) -> dict:
+    """Cycle-scan at the token scale of a 4096^2 image: one fla_cycle_scan call (its three
+    kernels) timed warm (back to back, between one pair of events) and cold (after the
+    read-only flush, each call between its own events).  The work unit is one exponential
+    exp(Delta a) per token, channel and state, B L d N per call whatever the number of copies;
+    the roofline is the chip's transcendental rate.  The bytes are those a call must move (x,
+    Delta, y, B, C, A once each): their rate is reported beside it."""
+    import torch
+    wl = synth.CYCLE_WORKLOADS["cyclescan_img4096"]
+    dev = torch.device("cuda:0")
+    x, delta, A, Bm, Cm = (t.to(dev) for t in synth.make_cycle_inputs(wl.B, wl.L, wl.d, wl.N, wl.seed, wl.kind))
+    y = torch.empty_like(x)
+    nws = binding.fla_cycle_scan_workspace(wl.B, wl.L, wl.d, wl.N, wl.repeats)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=dev)
+
+    def call():
+        binding.fla_cycle_scan(x, delta, A, Bm, Cm, y, ws, nws, wl.B, wl.L, wl.d, wl.N, wl.repeats, stream)
+
+    for _ in range(max(steps // 4, 10)):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        call()
+    e1.record(stream)
+    e1.synchronize()
+    warm_us = e0.elapsed_time(e1) * 1e3 / steps
+    p10, p50, p90 = percentiles(per_call_us(call, stream, 50))
+    cold = per_call_us(call, stream, 30, before=flush)
+    cold_us = statistics.mean(cold)
+    assert torch.isfinite(y[:, :64]).all()
+    exps, nbytes = binding.fla_cycle_scan_work(wl.B, wl.L, wl.d, wl.N, wl.repeats)
+
+    def alu(us):
+        t = exps / (us * 1e-6) / 1e12
+        return {"bound": "alu", "achieved": round(t, 3), "peak": round(PEAK_EXP_TPS, 3), "unit": "Texp/s",
+                "frac": round(t / PEAK_EXP_TPS, 4), "traffic": None}
+
+    return {"workload": wl.name, "B": wl.B, "L": wl.L, "d": wl.d, "N": wl.N, "repeats": wl.repeats,
+            "dtype": "f32", "us_per_call": round(warm_us, 3), "mode": "warm", "steps": steps,
+            "roofline": alu(warm_us), "roofline_cold": alu(cold_us),
+            "alg_exps": exps, "alg_bytes": nbytes,
+            "hbm_gbs": round(nbytes / (warm_us * 1e-6) / 1e9, 1),
+            "hbm_frac": round(nbytes / (warm_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "timing": {"warm_mean_us": round(warm_us, 3), "warm_p10_us": p10, "warm_p50_us": p50,
+                       "warm_p90_us": p90, "cold_mean_us": round(cold_us, 3)}}
+
+
+def cycle_scan_cpu_baseline(synth, channels: int = 128) -> dict:
+    """The fp64 Cycle-scan oracle on this host: the three copies laid out and scanned, over the
+    whole sequence of the 4096^2 workload for `channels` evenly spaced channels (the channels
+    are independent), scaled to all of them."""
+    import numpy as np
+    import oracle
+    wl = synth.CYCLE_WORKLOADS["cyclescan_img4096"]
+    x, delta, A, Bm, Cm = (t.numpy() for t in synth.make_cycle_inputs(wl.B, wl.L, wl.d, wl.N, wl.seed, wl.kind))
+    ch = np.arange(channels) * (wl.d // channels)
+    t0 = time.perf_counter()
+    oracle.cycle_scan.cycle_scan_channels(x, delta, A, Bm, Cm, ch, wl.repeats)
+    dt = time.perf_counter() - t0
+    return {"value": round(dt * wl.d / channels * 1e6, 1), "unit": "us/call", "cores": 1, "kind": "oracle",
+            "sample": "fp64 oracle (sequence laid out %d times, scanned token by token) on %d of %d channels "
+                      "over all %d tokens, one run of %.1f s, scaled to all channels; host %s"
+                      % (wl.repeats, channels, wl.d, wl.L, dt, cpu_model())}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -467,14 +617,19 @@ def main() -> int:
                     help="summarise rocprofv3 CSV output into profiles/ and exit (no GPU needed)")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize")
     ap.add_argument("--summary-dir", default="", help="where --summarize writes (default: profiles/)")
-    ap.add_argument("--leg", default="fwd", choices=["fwd", "bwd"],
-                    help="kernel --summarize is about: the forward or the backward")
+    ap.add_argument("--leg", default="fwd", choices=["fwd", "bwd", "cycle"],
+                    help="kernel --summarize is about: the forward, the backward or the Cycle-scan kernels")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward leg")
     ap.add_argument("--bwd-steps", type=int, default=500, help="timed backward calls")
+    ap.add_argument("--no-cycle-scan", action="store_true", help="skip the Cycle-scan leg")
+    ap.add_argument("--cycle-steps", type=int, default=100, help="timed Cycle-scan calls")
     args = ap.parse_args()
 
     if args.summarize:
-        summarize(args.summarize, args.workload, args.command, args.leg, args.summary_dir)
+        if args.leg == "cycle":
+            summarize_cycle(args.summarize, args.command, args.summary_dir)
+        else:
+            summarize(args.summarize, args.workload, args.command, args.leg, args.summary_dir)
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -620,6 +775,9 @@ def main() -> int:
     if not args.no_backward:
         print("[bench] backward", file=sys.stderr, flush=True)
         rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps, mode, flush)
+    if not args.no_cycle_scan:
+        print("[bench] Cycle-scan", file=sys.stderr, flush=True)
+        rec["cycle_scan"] = cycle_scan_leg(binding, synth, stream, args.cycle_steps, flush)
     del flush
     torch.cuda.synchronize()
     if args.copy_calibration:
@@ -627,6 +785,9 @@ def main() -> int:
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_budget)
+        if "cycle_scan" in rec:
+            print("[bench] timing the CPU Cycle-scan oracle", file=sys.stderr, flush=True)
+            rec["cycle_scan"]["cpu_baseline"] = cycle_scan_cpu_baseline(synth)
     print(json.dumps(rec), flush=True)
     return 0
 

@@ -23,6 +23,7 @@
 // x and Delta of a token are one coalesced 256-byte read per wave, and B_t, C_t, the same for
 // every channel, are wave-uniform reads.  Bound by the vector ALU (one exponential per
 // token, channel and state in each of passes A and C).
+#include "fla_cycle_scan.h"
 #include "fla_swin_device.h"
 
 namespace fla {

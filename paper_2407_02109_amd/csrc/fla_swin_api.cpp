@@ -8,6 +8,7 @@
 #include <cstdint>
 #include <cstring>
 
+#include "fla_cycle_scan.h"
 #include "fla_swin_internal.h"
 
 static_assert(fla::kScratchBytes == FLA_SCRATCH_BYTES, "static scratch size of the header and the kernels");

@@ -151,36 +151,6 @@ hipError_t scratch_address(void** ptr);
 // sums the partials of ws into row L of dk and dv (elem_bytes 2: bf16, 4: fp32)
 hipError_t launch_swin_bwd_pad_reduce(const SwinBwdArgs& a, int elem_bytes, hipStream_t stream);
 
-// Cycle-scan (fla_cycle_scan.hip): selective scan over the sequence laid out `repeats` times.
-struct CycleArgs {
-    const float* x;       // [B, L, d]
-    const float* delta;   // [B, L, d]
-    const float* A;       // [d, N]
-    const float* Bm;      // [B, L, N]
-    const float* Cm;      // [B, L, N]
-    float* y;             // [B, L, d]
-    float* ws_h;          // [B, nch, d, N]: chunk end states, then the chunks' starting states
-    float* ws_s;          // [B, nch, d]: sum of Delta over each chunk
-    int B, L, d, N, repeats;
-    int T;                // tokens per chunk
-    int nch;              // chunks: ceil(L / T)
-    int cgroups;          // groups of 64 channels: ceil(d / 64)
-};
-bool cycle_states_supported(int N);   // N in {1, 2, 4, 8, 16, 32}
-// Tokens per chunk: enough chunks to fill the chip at the sizes of an image layer, at
-// least 32 tokens (a power of two from 32 to 256).
-inline int cycle_chunk(int L) {
-    int T = 32;
-    while (T < 256 && (int64_t)T * 64 < L) T *= 2;
-    return T;
-}
-inline int64_t cycle_workspace_floats(int B, int L, int d, int N) {
-    const int T = cycle_chunk(L);
-    const int64_t nch = (L + T - 1) / T;
-    return (int64_t)B * nch * d * (N + 1);
-}
-hipError_t launch_cycle_scan(const CycleArgs& a, hipStream_t stream);
-
 // Window `win` (numbered over all grids, raster order within a grid), clipped to its grid.
 struct WindowRect {
     int y0, x0, rows, cols;

@@ -5,6 +5,7 @@
 #include <thread>
 #include <vector>
 
+#include "fla_cycle_scan.h"
 #include "fla_swin_internal.h"
 
 thread_local emu_index threadIdx, blockIdx;

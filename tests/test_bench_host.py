@@ -85,3 +85,32 @@ def test_roofline_follows_arithmetic_intensity():
     r = bench.roofline(512e9, 1e9, 1000.0, None)
     assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s" and r["achieved"] == pytest.approx(512.0)
     assert r["frac"] == pytest.approx(512.0 / 2500.0)
+
+
+def test_cycle_summary_splits_cold_and_warm_calls_and_scales_counters(tmp_path):
+    prof = tmp_path / "prof"
+    ch, ca, co = ("void fla::(anonymous namespace)::cycle_scan_chunks<32>(fla::CycleArgs)",
+                  "fla::(anonymous namespace)::cycle_scan_carries(fla::CycleArgs)",
+                  "void fla::(anonymous namespace)::cycle_scan_outputs<32>(fla::CycleArgs)")
+    flush = "void at::native::reduce_kernel<512, 1>(x)"
+    # one cold call (after the flush: 30, 4, 40 us) and one warm call (20, 2, 30 us)
+    trace = [[flush, "1", 0, 500], [ch, "3072", 1000, 31000], [ca, "96", 31000, 35000], [co, "3072", 35000, 75000],
+             [ch, "3072", 80000, 100000], [ca, "96", 100000, 102000], [co, "3072", 102000, 132000]]
+    _write(str(prof / "trace" / "run_kernel_trace.csv"), ["Kernel_Name", "Grid_Size_X", "Start_Timestamp",
+                                                          "End_Timestamp"], trace)
+    hdr = ["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"]
+    # FETCH_SIZE of the copy reads half its 512 MiB: every fetch figure is scaled by 2
+    _write(str(prof / "fetch_size" / "run_counter_collection.csv"), hdr,
+           [[1, ch, 196608, "FETCH_SIZE", 1000.0], [1, ch, 196608, "FETCH_SIZE", 1000.0],
+            [9, "__amd_rocclr_copyBuffer", 1 << 20, "FETCH_SIZE", 262144.0]])
+    _write(str(prof / "write_size" / "run_counter_collection.csv"), hdr,
+           [[3, co, 196608, "WRITE_SIZE", 4000.0],
+            [9, "__amd_rocclr_copyBuffer", 1 << 20, "WRITE_SIZE", 524288.0]])
+    out = tmp_path / "out"
+    bench.summarize_cycle(str(prof), "rocprofv3 ... -- python3 bench.py", str(out))
+    text = (out / "cycle_scan_cyclescan_img4096.md").read_text()
+    assert "| cycle_scan_chunks<32> | 1 | 30.00 | 1 | 20.00 | %.1f | - |" % (2000 * 1024 * 2 / 1e6) in text
+    assert "| cycle_scan_carries | 1 | 4.00 | 1 | 2.00 | - | - |" in text
+    assert "| cycle_scan_outputs<32> | 1 | 40.00 | 1 | 30.00 | - | %.1f |" % (4000 * 1024 / 1e6) in text
+    assert "| sum (one call) | | 74.00 | | 52.00 | | |" in text
+    assert "Kernel source hash: %s" % bench.kernel_hash("cycle") in text

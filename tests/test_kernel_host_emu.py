@@ -43,6 +43,7 @@ def emu_binary(tmp_path_factory):
     shutil.copy(os.path.join(CSRC, "fla_cycle_scan.hip"), src / "fla_cycle_scan.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_api.cpp"), src / "fla_swin_api.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_internal.h"), src / "fla_swin_internal.h")
+    shutil.copy(os.path.join(CSRC, "fla_cycle_scan.h"), src / "fla_cycle_scan.h")
     shutil.copy(os.path.join(EMU, "fla_swin_device.h"), src / "fla_swin_device.h")
     exe = str(d / "run")
     cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-pthread",
