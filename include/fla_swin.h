@@ -329,8 +329,8 @@ int fla_swin_attn_bwd_work(int B, int heads, int n_grids, const int* grid_hw, in
  * each other); FLA_ERR_ARCH; FLA_ERR_LAUNCH.  Nothing is launched and y is not touched on
  * error.  Asynchronous on `stream` (three kernels). */
 
-/* Workspace of fla_cycle_scan, in bytes: 4 (N + 1) floats per (batch entry, chunk, channel)
- * with chunks of 32 to 256 tokens.  Errors as for fla_cycle_scan up to FLA_ERR_TOO_LARGE
+/* Workspace of fla_cycle_scan, in bytes: N + 1 floats (4 (N + 1) bytes) per (batch entry,
+ * chunk, channel), with chunks of 32 to 256 tokens.  Errors as for fla_cycle_scan up to FLA_ERR_TOO_LARGE
  * (bytes must be non-NULL). */
 int fla_cycle_scan_workspace(int B, int L, int d, int N, int repeats, size_t* bytes);
 
