@@ -90,3 +90,31 @@ def test_cycle_scan_wrapper_and_empty_calls():
     assert fb.fla_cycle_scan(e, e, A, Bm, Cm, e, None, 0, 1, 0, 64, 8, 3) == 0
     with pytest.raises(ValueError):
         fb.cycle_scan(x, delta, A[:, :4], Bm, Cm)
+
+
+def test_cycle_scan_beyond_2gib():
+    """11 batch entries of the 65536-token, 768-channel sequence: x, Delta and y hold 2.2 GB each, so the last
+    entries lie past 2^31 bytes from the tensors' start.  Inputs are drawn on the GPU from a seeded generator;
+    sampled channels of the first and the last entry are checked against the oracle on that entry alone."""
+    B, L, d, N, r = 11, 65536, 768, 32, 3
+    assert B * L * d * 4 > 2 ** 31
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev).manual_seed(2024)
+    x = torch.randn(B, L, d, device=dev, generator=g)
+    delta = torch.exp(-4.0 + 2.0 * torch.rand(B, L, d, device=dev, generator=g))   # in [e^-4, e^-2]
+    A = -(0.5 + 3.0 * torch.rand(d, N, device=dev, generator=g))
+    Bm = torch.randn(B, L, N, device=dev, generator=g)
+    Cm = torch.randn(B, L, N, device=dev, generator=g)
+    y = fb.cycle_scan(x, delta, A, Bm, Cm, repeats=r)
+    torch.cuda.synchronize()
+    ch = [0, 767]
+    tol = 4.0 * 2.0 ** -24 / (delta.amin().item() * A.abs().min().item()) + 1e-6
+    for b in (0, B - 1):
+        sl = lambda t: t[b:b + 1].cpu().double().numpy()
+        ref = CS.cycle_scan_channels(sl(x), sl(delta), A.cpu().double().numpy(), sl(Bm), sl(Cm), ch, r)
+        got = y[b:b + 1][:, :, ch].cpu().double().numpy()
+        assert np.isfinite(got).all()
+        err = np.abs(got - ref).max() / np.abs(ref).max()
+        assert err <= tol, (b, err, tol)
+    del x, delta, y
+    torch.cuda.empty_cache()
