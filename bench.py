@@ -71,7 +71,7 @@ def kernel_hash(leg: str = "fwd") -> str:
 
 def traffic_path(leg: str, workload: str, out_dir: str = "") -> str:
     return os.path.join(out_dir or os.path.join(ROOT, "profiles"),
-                        "traffic_%s%s.json" % ("" if leg == "fwd" else "bwd_", workload))
+                        "traffic_%s%s.json" % ({"fwd": "", "bwd": "bwd_"}.get(leg, leg + "_"), workload))
 
 
 def roofline(flops: float, nbytes: float, us: float, traffic):
@@ -295,7 +295,12 @@ def summarize_cycle(prof_dir: str, command: str, out_dir: str = ""):
         mb = lambda n: ("%.1f" % (counters[k][n] * 1024 * scale[n] / 1e6)) if counters[k].get(n) and scale[n] else "-"
         lines.append("| %s | %d | %s | %d | %s | %s | %s |" % (k, len(cold), "%.2f" % c if c else "-", len(warm),
                                                                "%.2f" % w if w else "-", mb("FETCH_SIZE"), mb("WRITE_SIZE")))
+    per_call = None
+    if all(counters[k].get("FETCH_SIZE") and counters[k].get("WRITE_SIZE") for k in durs) and all(scale.values()):
+        per_call = sum(counters[k]["FETCH_SIZE"] * 1024 * scale["FETCH_SIZE"]
+                       + counters[k]["WRITE_SIZE"] * 1024 * scale["WRITE_SIZE"] for k in durs)
     lines += ["| sum (one call) | | %.2f | | %.2f | | |" % tuple(total), "",
+              "HBM bytes per call (the three kernels, scaled): %s" % (None if per_call is None else int(per_call)),
               "Copy calibration (512 MiB device copy, KiB per dispatch): FETCH_SIZE %s, WRITE_SIZE %s"
               % (copies.get("FETCH_SIZE"), copies.get("WRITE_SIZE")),
               "Scale factors (true bytes / counter bytes): fetch %s, write %s" % (scale["FETCH_SIZE"], scale["WRITE_SIZE"]),
@@ -303,6 +308,12 @@ def summarize_cycle(prof_dir: str, command: str, out_dir: str = ""):
     os.makedirs(out_dir, exist_ok=True)
     with open(os.path.join(out_dir, "cycle_scan_cyclescan_img4096.md"), "w") as f:
         f.write("\n".join(lines))
+    if per_call is not None:
+        with open(traffic_path("cycle", "cyclescan_img4096", out_dir), "w") as f:
+            json.dump({"workload": "cyclescan_img4096", "kernel": "cycle_scan_chunks, cycle_scan_carries, "
+                       "cycle_scan_outputs", "kernel_hash": kernel_hash("cycle"), "bytes_per_launch": int(per_call),
+                       "per_kernel_kib": {k: counters[k] for k in durs}, "fetch_scale": scale["FETCH_SIZE"],
+                       "write_scale": scale["WRITE_SIZE"]}, f, indent=1)
     print("\n".join(lines))
 
 
@@ -563,10 +574,12 @@ def cycle_scan_leg(binding, synth, stream, steps: int, flush) -> dict:
     assert torch.isfinite(y[:, :64]).all()
     exps, nbytes = binding.fla_cycle_scan_work(wl.B, wl.L, wl.d, wl.N, wl.repeats)
 
+    traffic = measured_traffic(wl.name, "cycle")
+
     def alu(us):
         t = exps / (us * 1e-6) / 1e12
         return {"bound": "alu", "achieved": round(t, 3), "peak": round(PEAK_EXP_TPS, 3), "unit": "Texp/s",
-                "frac": round(t / PEAK_EXP_TPS, 4), "traffic": None}
+                "frac": round(t / PEAK_EXP_TPS, 4), "traffic": traffic}
 
     return {"workload": wl.name, "B": wl.B, "L": wl.L, "d": wl.d, "N": wl.N, "repeats": wl.repeats,
             "dtype": "f32", "us_per_call": round(warm_us, 3), "mode": "warm", "steps": steps,
