@@ -2,8 +2,8 @@
 which is a HIP graph on ROCm), compared with eager launches on the default stream.
 
 Every entry point is asynchronous on the stream it is given and allocates nothing, so a
-layer (forward, training forward, backward with its pad reduction) can be captured once and
-replayed.  The graphs are replayed several times with eager work and synchronisations in
+layer (forward, training forward, backward with its pad reduction) or a Cycle-scan call (three
+kernels) can be captured once and replayed.  The graphs are replayed several times with eager work and synchronisations in
 between, and every replay is checked bit for bit against the eager result."""
 import pytest
 import torch
@@ -92,3 +92,48 @@ def test_graph_replays_match_eager(pm):
         torch.cuda.synchronize()
         for key, r in ref.items():
             assert torch.equal(bufs[key], r), (rep, key)
+
+
+def _cycle_setup():
+    B, L, d, N, r = 2, 1500, 130, 16, 3   # several chunks, a partial channel group
+    ins = [t.cuda() for t in synth.make_cycle_inputs(B, L, d, N, seed=88)]
+    nws = fb.fla_cycle_scan_workspace(B, L, d, N, r)
+    bufs = dict(y=torch.empty((B, L, d), dtype=torch.float32, device="cuda"),
+                ws=torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda"))
+    return (B, L, d, N, r), ins, bufs, nws
+
+
+def _cycle(shape, ins, bufs, nws, stream):
+    B, L, d, N, r = shape
+    fb.fla_cycle_scan(*ins, bufs["y"], bufs["ws"], nws, B, L, d, N, r, stream)
+
+
+def test_cycle_scan_side_stream_and_graph_replays_match_eager():
+    _say("Cycle-scan side stream and graph")
+    shape, ins, bufs, nws = _cycle_setup()
+    _cycle(shape, ins, bufs, nws, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    ref = bufs["y"].clone()
+    bufs["y"].zero_()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        _cycle(shape, ins, bufs, nws, side)
+    side.synchronize()
+    assert torch.equal(bufs["y"], ref)
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        _cycle(shape, ins, bufs, nws, cap)
+    cap.synchronize()
+    with torch.cuda.graph(graph, stream=cap):
+        _cycle(shape, ins, bufs, nws, cap)   # three kernels, nothing else
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in bufs.values():
+            t.fill_(7)                       # output and workspace overwritten between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bufs["y"], ref), rep
