@@ -64,7 +64,8 @@ typedef enum {
     FLA_ERR_ALIGN = 2,     /* a pointer is not 16-byte aligned (Cycle-scan: 4-byte)         */
     FLA_ERR_SHAPE = 3,     /* B, heads, Hgrid or Wgrid negative; n_grids not in 1..8;
                               Cycle-scan: B, L, d negative, N or repeats below 1          */
-    FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (supported: 64)                      */
+    FLA_ERR_HEAD_DIM = 4,  /* head_dim is not supported (64; the plain forwards, bf16 and
+                              fp32, one grid or several, also take 32 and 128)            */
     FLA_ERR_WINDOW = 5,    /* window < 1                                                   */
     FLA_ERR_SHIFT = 6,     /* shift < 0 or shift >= window                                 */
     FLA_ERR_PAD_MODE = 7,  /* pad_mode is neither FLA_PAD_MASK nor FLA_PAD_KVTOKEN         */
@@ -89,13 +90,15 @@ typedef enum {
 
 /* bf16 forward (storage: 16-bit bfloat16, round-to-nearest-even on output).
  * Q.K^T and P.V run on bf16 matrix cores with fp32 accumulation; softmax in fp32;
- * P is rounded to bf16 before P.V.  Returns an fla_status. */
+ * P is rounded to bf16 before P.V.  head_dim 64 (the model's), 32 or 128.  Returns an
+ * fla_status. */
 int fla_swin_attn_fwd(const void* q, const void* k, const void* v, void* out,
                       int B, int heads, int Hgrid, int Wgrid, int head_dim,
                       int window, int shift, int pad_mode, hipStream_t stream);
 
 /* fp32 forward: same operation and layout with float tensors, computed entirely in
- * fp32 (used for tight-tolerance checks on small grids).  Returns an fla_status. */
+ * fp32 (used for tight-tolerance checks on small grids); head_dim 64, 32 or 128.  Returns
+ * an fla_status. */
 int fla_swin_attn_fwd_f32(const float* q, const float* k, const float* v, float* out,
                           int B, int heads, int Hgrid, int Wgrid, int head_dim,
                           int window, int shift, int pad_mode, hipStream_t stream);
@@ -153,7 +156,7 @@ int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int
  * FLA_PAD_KVTOKEN mode has no position and is not rotated.  The rotation runs in fp32 on
  * the loaded values (bf16: rounded back to bf16 before the products), so no rotated copy of
  * q or k is written.  rope_theta = 10000, rope_scale = 1 is RoFormer's choice.  Errors as
- * for fla_swin_attn_fwd, plus FLA_ERR_ROPE, and FLA_ERR_UNSUPPORTED (after FLA_ERR_TOO_LARGE)
+ * for fla_swin_attn_fwd (head_dim 64 only), plus FLA_ERR_ROPE, and FLA_ERR_UNSUPPORTED (after FLA_ERR_TOO_LARGE)
  * when the bf16 kernel gets a window of more than 32 rows or columns (its per-window
  * cos/sin table covers 32 x 32; the fp32 entry point takes any window). */
 int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out,
@@ -189,7 +192,8 @@ int fla_swin_attn_rope_fwd_lse(const void* q, const void* k, const void* v, void
  * --------------------------------------------------------------------------------------- */
 
 /* Training forward: fla_swin_attn_fwd, and also lse [B, heads, L] (fp32, contiguous):
- * LSE_i above, the natural log of each query's softmax denominator.  lse is a device
+ * LSE_i above, the natural log of each query's softmax denominator.  Training (this, the
+ * backward and RoPE) takes head_dim 64 only.  lse is a device
  * pointer, non-NULL, 16-byte aligned, and must not overlap q, k, v or out.  In bf16 the
  * denominator is the sum of the bf16-rounded probabilities the output uses. */
 int fla_swin_attn_fwd_lse(const void* q, const void* k, const void* v, void* out, float* lse,

@@ -92,8 +92,10 @@ int check_sizes(int B, int heads, int n, const int* hw, bool* empty) {
     return FLA_OK;
 }
 
-int check_scalars(int head_dim, int window, int shift, int pad_mode) {
-    if (head_dim != fla::kHeadDim) return FLA_ERR_HEAD_DIM;
+// plain_forward: the head_dim instances of the plain forward kernels (32, 64, 128) are
+// admitted; every other path takes 64.
+int check_scalars(int head_dim, int window, int shift, int pad_mode, bool plain_forward = false) {
+    if (plain_forward ? !fla::fwd_head_dim_ok(head_dim) : head_dim != fla::kHeadDim) return FLA_ERR_HEAD_DIM;
     if (window < 1) return FLA_ERR_WINDOW;
     if (shift < 0 || shift >= window) return FLA_ERR_SHIFT;
     if (pad_mode != FLA_PAD_MASK && pad_mode != FLA_PAD_KVTOKEN) return FLA_ERR_PAD_MODE;
@@ -203,6 +205,7 @@ fla::SwinArgs make_args(const Problem& pr, const void* q, const void* k, const v
     a.div_heads = fla::FastDiv::make((unsigned)heads);
     a.div_nqb = fla::FastDiv::make((unsigned)geo.nqb);
     a.div_nwin = fla::FastDiv::make((unsigned)geo.n_windows);
+    a.head_dim = head_dim;
     a.rope = 0;
     a.rope_scale = 0.f;
     for (float& f : a.rope_rev) f = 0.f;
@@ -242,7 +245,7 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
     if (!q || !k || !v || !out || (want_lse && !lse)) return FLA_ERR_NULL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || (want_lse && !aligned16(lse)))
         return FLA_ERR_ALIGN;
-    st = check_scalars(head_dim, window, shift, pad_mode);
+    st = check_scalars(head_dim, window, shift, pad_mode, !rope && !want_lse);
     if (st != FLA_OK) return st;
     if (rope && !rope_ok(*rope)) return FLA_ERR_ROPE;
     Problem pr;

@@ -42,29 +42,55 @@
 namespace fla {
 namespace {
 
-constexpr int D = kHeadDim;     // 64 channels per head
 constexpr int THREADS = 512;    // 8 waves of 64
 constexpr int QW = 32;          // queries per wave
 constexpr int KC = 256;         // keys staged in LDS at a time
 constexpr int KT = 32;          // keys per inner tile
 constexpr int KH = KC / 2;      // keys per half chunk (staged and computed in turn)
-constexpr int KS = D + 8;       // K row stride in LDS, bf16 elements (144 B)
 constexpr int VS = KC + 4;      // V^T row stride in LDS, bf16 elements (520 B)
+
+// Per head_dim D (64; the plain forward also has instances for 32 and 128): the K row stride
+// in LDS (D + 8 bf16: 144 B at D = 64), the threads that load one K row 16 bytes each, the K
+// pieces a thread holds, the (4 keys x 8 channels) pieces of V, and the waves per SIMD the
+// registers and LDS allow (at D = 128, K and V^T take 136 KB: one workgroup per CU).
+template <int D>
+struct Cfg {
+    static constexpr int KS = D + 8;
+    static constexpr int DLOG = D == 32 ? 5 : D == 64 ? 6 : 7;
+    static constexpr int TPR = D / 8;               // threads per K row
+    static constexpr int TPR_LOG = DLOG - 3;
+    static constexpr int RPP = THREADS / TPR;       // K rows per pass of the workgroup
+    static constexpr int KREG = KC / RPP;           // K pieces per thread
+    static constexpr int VUNITS = (KC / 4) * (D / 8);
+    static constexpr int VPT = (VUNITS + THREADS - 1) / THREADS;   // V pieces per thread
+    static constexpr int WAVES = D > 64 ? 2 : 4;
+};
 constexpr float kLazyThreshold = 8.f;   // exp2-domain headroom before the max is raised
 constexpr float kLn2 = 0.693147180559945309f;
 
-template <bool MASKED>
+// f(B), f(B + 1), ..., f(E - 1) as separate calls with constant arguments (the same code as
+// writing the calls out; an unrolled loop is scheduled differently)
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(B);
+        static_for<B + 1, E>(f);
+    }
+}
+
+template <int D, bool MASKED>
 __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, const uint16_t* __restrict__ Vt,
                                             int t0, int kc0, int nk, int n, float pad_bias_raw,
-                                            const bf16x8 (&qop)[4], floatx16 (&o)[2],
+                                            const bf16x8 (&qop)[D / 16], floatx16 (&o)[D / 32],
                                             float& m_run, float& neg_mc, float& l_run, float c_log2, int lane) {
+    constexpr int KS = Cfg<D>::KS;
     const int li = lane & 31;
     const int h = lane >> 5;
     // ---- S^T = K . Q^T for 32 keys x 32 queries: s[r] holds key 8*(r/4) + 4*h + r%4
     //      of query li
     const uint16_t* krow = Ks + (t0 + li) * KS + 8 * h;
     floatx16 s = {};
-    for (int st = 0; st < 4; ++st)
+    for (int st = 0; st < D / 16; ++st)
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * st),
                                                     qop[st], s, 0, 0, 0);
     if constexpr (MASKED) {
@@ -92,8 +118,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
         m_run = m_new;
         l_run *= alpha;
-        o[0] *= alpha;
-        o[1] *= alpha;
+        for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
         neg_mc = -m_run * c_log2;
     }
     bf16x8 pb[2];
@@ -108,7 +133,7 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         for (int j = 0; j < 8; j += 2)
             l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[sg][j], pb[sg][j + 1]}, ones, l_run, false);
     for (int sg = 0; sg < 2; ++sg)
-        for (int db = 0; db < 2; ++db) {
+        for (int db = 0; db < D / 32; ++db) {
             const uint16_t* vrow = Vt + (32 * db + li) * VS + t0 + 16 * sg + 4 * h;
             const bf16x4 va = *reinterpret_cast<const bf16x4*>(vrow);
             const bf16x4 vb = *reinterpret_cast<const bf16x4*>(vrow + 8);
@@ -117,8 +142,8 @@ __device__ __forceinline__ void attend_tile(const uint16_t* __restrict__ Ks, con
         }
 }
 
-// 4 waves per SIMD: at most 128 VGPRs, and the LDS footprint (2 x 69 KB) admits the two
-// workgroups per CU that this takes.
+// D = 64: 4 waves per SIMD, at most 128 VGPRs, and the LDS footprint (2 x 69 KB) admits the
+// two workgroups per CU that this takes.
 // (row, col) of window-local index t inside the window's rectangle
 __device__ __forceinline__ void window_rc(const WindowAddr& addr, int t, int& r, int& c) {
     const unsigned ru = __umulhi((unsigned)t, addr.magic) + ((unsigned)t & addr.one_mask);
@@ -140,9 +165,11 @@ __device__ __forceinline__ void rope_rotate8_tab(uint16_t (&x)[8], const float2*
 
 constexpr int kRopeTab = kRopeMaxSide;   // window rows / columns covered by the per-workgroup RoPE table
 
-template <bool MULTI, bool ROPE>
-__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(4, 4)))
+template <bool MULTI, bool ROPE, int D>
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(Cfg<D>::WAVES, Cfg<D>::WAVES)))
 void swin_fwd_bf16_kernel(SwinArgs a) {
+    static_assert(!ROPE || D == kHeadDim, "RoPE: head_dim 64 only");
+    constexpr int KS = Cfg<D>::KS, TPR = Cfg<D>::TPR, TPR_LOG = Cfg<D>::TPR_LOG, RPP = Cfg<D>::RPP;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[KC * KS];
     __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
     // RoPE: (cos, sin) of the window's row positions [0][r][j] and column positions [1][c][j]
@@ -237,15 +264,16 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         }
     }
 
-    bf16x8 qop[4];
+    bf16x8 qop[D / 16];
     if (nq > 0) {
         const unsigned row = addr(min(wq0 + li, n - 1));
-        for (int st = 0; st < 4; ++st)
+        for (int st = 0; st < D / 16; ++st)
             qop[st] = __builtin_bit_cast(bf16x8, bload16(qr, row + 32 * st + 16 * h));
     }
     float m_run = -INFINITY, l_run = 0.f;
     float neg_mc = 0.f;   // -m_run * log2(e) / sqrt(d); the first tile always raises the max and sets it
-    floatx16 o[2] = {floatx16{}, floatx16{}};   // O^T: [channel block]
+    floatx16 o[D / 32];   // O^T: [channel block]
+    for (int db = 0; db < D / 32; ++db) o[db] = floatx16{};
 
     for (int kc0 = 0; kc0 < nk; kc0 += KC) {
         const int ck = min(KC, nk - kc0);
@@ -253,64 +281,75 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
         // ---- issue every global load of the chunk before the first LDS write, so a
         //      workgroup waits for one round trip to HBM, not one per load.
-        //      K: 8 threads per 128-byte row (coalesced), rows tid/8 + 64*it.
+        //      K: D/8 threads per row of 2D bytes (coalesced; 8 per 128-byte row at D = 64),
+        //      rows tid/(D/8) + RPP*it.
         //      V: a thread takes 4 consecutive keys (quad) x 8 channels (vpart) and writes
-        //      them transposed: 4 keys of one channel are one 8-byte LDS store.
+        //      them transposed: 4 keys of one channel are one 8-byte LDS store (at D = 128 a
+        //      thread takes two such pieces, at D = 32 half the threads take one).
         //      The chunk is consumed in two halves of 128 keys: V and the first half of K are
         //      written to LDS and that half is computed while the K rows of the second half
         //      are still arriving (deferring V as well would exceed 128 VGPRs).  Loads are
         //      issued in the order they are consumed, since a wave waits for its loads in
         //      issue order.
-        uint4 kreg[KC / 64];
-        uint4 vreg[4];
-        const int part = tid & 7;
-        const int vpart = (tid >> 3) & 7;
-        const int quad = (tid & 7) + ((tid >> 6) << 3);
+        constexpr int VUNITS = Cfg<D>::VUNITS, VPT = Cfg<D>::VPT;
+        uint4 kreg[Cfg<D>::KREG];
+        uint4 vreg[VPT][4];
+        const int part = tid & (TPR - 1);
+        // V piece j of this thread: unit tid + j THREADS, whose (vpart, quad) are
+        // ((unit / 8) mod D/8, unit mod 8 + 8 (unit / D)) = (vpart, quad + j 8 THREADS / D)
+        const int vpart = (tid >> 3) & (D / 8 - 1);
+        const int quad = (tid & 7) + ((tid >> Cfg<D>::DLOG) << 3);
         auto load_k = [&](int it) {
-            const int t = kc0 + (tid >> 3) + 64 * it;
+            const int t = kc0 + (tid >> TPR_LOG) + RPP * it;
             kreg[it] = bload16(kr, (t < n ? addr(t) : kOutside) + part * 16);
-        };
-        load_k(0);
-        load_k(1);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int t = kc0 + quad * 4 + u;
-            vreg[u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
-        }
-        load_k(2);
-        load_k(3);
-
-        auto write_v = [&]() {
-            const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-            const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-            const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-            const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                uint2 lo, hi;
-                lo.x = (w0[m] & 0xffffu) | (w1[m] << 16);
-                lo.y = (w2[m] & 0xffffu) | (w3[m] << 16);
-                hi.x = (w0[m] >> 16) | (w1[m] & 0xffff0000u);
-                hi.y = (w2[m] >> 16) | (w3[m] & 0xffff0000u);
-                const int ch = vpart * 8 + 2 * m;
-                *reinterpret_cast<uint2*>(&Vt[ch * VS + quad * 4]) = lo;
-                *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + quad * 4]) = hi;
-            }
         };
         // K rows of this half (and all of V^T with the first); RoPE on the K rows in place;
         // the pad token if its slot falls in this half; then the barrier
         constexpr int kh = KH;
-        constexpr int its = kh / 64;   // K rows per thread in one half
+        constexpr int its = kh / RPP;   // K rows per thread in one half
+        static_for<0, its>(load_k);
+        for (int j = 0; j < VPT; ++j) {   // (plain loops here: a lambda or an unroll pragma changes the schedule)
+            if (VUNITS % THREADS == 0 || tid < VUNITS) {   // (a partial last piece only at D = 32, j = 0)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int t = kc0 + (quad + j * 8 * (THREADS >> Cfg<D>::DLOG)) * 4 + u;
+                    vreg[j][u] = bload16(vr, (t < n ? addr(t) : kOutside) + vpart * 16);
+                }
+            }
+        }
+        static_for<its, 2 * its>(load_k);
+
+        auto write_v = [&]() {
+            for (int j = 0; j < VPT; ++j) {
+                if (VUNITS % THREADS != 0 && tid >= VUNITS) continue;
+                const int qj = quad + j * 8 * (THREADS >> Cfg<D>::DLOG);
+                const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[j][0]);
+                const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[j][1]);
+                const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[j][2]);
+                const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[j][3]);
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    uint2 lo, hi;
+                    lo.x = (w0[m] & 0xffffu) | (w1[m] << 16);
+                    lo.y = (w2[m] & 0xffffu) | (w3[m] << 16);
+                    hi.x = (w0[m] >> 16) | (w1[m] & 0xffff0000u);
+                    hi.y = (w2[m] >> 16) | (w3[m] & 0xffff0000u);
+                    const int ch = vpart * 8 + 2 * m;
+                    *reinterpret_cast<uint2*>(&Vt[ch * VS + qj * 4]) = lo;
+                    *reinterpret_cast<uint2*>(&Vt[(ch + 1) * VS + qj * 4]) = hi;
+                }
+            }
+        };
         auto stage_half = [&](int half) {
             for (int it = its * half; it < its * (half + 1); ++it)
-                *reinterpret_cast<uint4*>(&Ks[((tid >> 3) + 64 * it) * KS + part * 8]) = kreg[it];
+                *reinterpret_cast<uint4*>(&Ks[((tid >> TPR_LOG) + RPP * it) * KS + part * 8]) = kreg[it];
             if (half == 0) write_v();
             if constexpr (ROPE) {
                 // RoPE on this thread's pieces of the K rows it just wrote (8 channels per row:
                 // the row half for part < 4), in place in LDS
                 if (kc0 == 0 && half == 0) __syncthreads();   // the cos / sin table is complete
                 for (int it = its * half; it < its * (half + 1); ++it) {
-                    const int key = (tid >> 3) + 64 * it;
+                    const int key = (tid >> TPR_LOG) + RPP * it;
                     if (kc0 + key < n) {
                         int kr_, kc_;
                         window_rc(addr, kc0 + key, kr_, kc_);
@@ -327,7 +366,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 // the pad token is key n of the window: its slot was zero-filled above; after
                 // the barrier, 8 threads put its K row and its V^T column in place
                 __syncthreads();
-                if (tid < 8) {
+                if (tid < D / 8) {
                     *reinterpret_cast<uint4*>(&Ks[slot * KS + tid * 8]) = bload16(kpr, tid * 16);
                     const uint4 vv = bload16(vpr, tid * 16);
                     const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
@@ -358,10 +397,10 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
         auto attend_range = [&](int t_begin, int t_end) {
             const int t_plain = min(t_end, t_begin + max(0, (n - kc0 - t_begin) / KT) * KT);
             for (int t0 = t_begin; t0 < t_plain; t0 += KT)
-                attend_tile<false>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
+                attend_tile<D, false>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
                                    a.scale_log2, lane);
             for (int t0 = t_plain; t0 < t_end; t0 += KT)
-                attend_tile<true>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
+                attend_tile<D, true>(Ks, Vt, t0, kc0, nk, n, pad_bias_raw, qop, o, m_run, neg_mc, l_run,
                                   a.scale_log2, lane);
         };
         if (nq > 0) attend_range(0, min(ck, kh));
@@ -373,8 +412,8 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
     // ---- epilogue: normalise, round to bf16 (RNE), and store each query row at its own
     //      token.  The wave's 32 x 64 result is staged in LDS (in the K tile, free once every
-    //      wave is past its last tile) so that the stores are whole 128-byte rows: 8 lanes
-    //      per row, 16 bytes per lane.
+    //      wave is past its last tile) so that the stores are whole rows: D/8 lanes per row
+    //      (8 per 128-byte row at D = 64), 16 bytes per lane.
     __syncthreads();
     if (nq > 0) {
         const float lsum = xhalf_sum(l_run);
@@ -386,15 +425,16 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
             a.lse[row] = (m_run * a.scale_log2 + log2f(lsum)) * kLn2;
         }
         uint16_t* orow = Ks + (wave * QW + li) * KS;
-        for (int db = 0; db < 2; ++db)
+        for (int db = 0; db < D / 32; ++db)
             for (int rg = 0; rg < 4; ++rg) {
                 bf16x4 r4;
                 for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][4 * rg + u] * inv);
                 *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * rg + 4 * h) = r4;
             }
-        const int part = lane & 7;
-        for (int i = 0; i < QW / 8; ++i) {
-            const int r = 8 * i + (lane >> 3);
+        const int part = lane & (TPR - 1);
+        constexpr int rows = 64 / TPR;   // rows per store instruction
+        for (int i = 0; i < QW / rows; ++i) {
+            const int r = rows * i + (lane >> TPR_LOG);
             const uint4 v = *reinterpret_cast<const uint4*>(Ks + (wave * QW + r) * KS + 8 * part);
             const unsigned off = r < nq ? addr(wq0 + r) + 16 * part : kOutside;   // tail rows: dropped
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orr, off, 0, 0);
@@ -404,13 +444,21 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
 
 }  // namespace
 
+template <int D>
+const void* plain_kernel(const SwinArgs& a) {
+    return a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, false, D>)
+                         : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, false, D>);
+}
+
 hipError_t launch_swin_fwd_bf16(const SwinArgs& a, hipStream_t stream) {
     SwinArgs args = a;
     void* params[] = {&args};
-    const void* fn = a.rope ? (a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, true>)
-                                             : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, true>))
-                            : (a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, false>)
-                                             : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, false>));
+    const void* fn;
+    if (a.rope)   // head_dim 64 only (the host checks)
+        fn = a.n_grids > 1 ? reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<true, true, kHeadDim>)
+                           : reinterpret_cast<const void*>(&swin_fwd_bf16_kernel<false, true, kHeadDim>);
+    else
+        fn = a.head_dim == 32 ? plain_kernel<32>(a) : a.head_dim == 128 ? plain_kernel<128>(a) : plain_kernel<64>(a);
     return hipLaunchKernel(fn, dim3((unsigned)fwd_bf16_groups(a)), dim3(THREADS), params, 0, stream);
 }
 

@@ -11,11 +11,12 @@
 namespace fla {
 namespace {
 
-constexpr int D = kHeadDim;
 constexpr int THREADS = kQueryBlock;   // one query per thread
 constexpr int KC = 64;                 // keys per LDS chunk
 constexpr int KG = 16;                 // keys per rescale step
 
+// D: head_dim (64; the plain forward also has instances for 32 and 128)
+template <int D>
 __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
     __shared__ __attribute__((aligned(16))) float Kf[KC * D];
     __shared__ __attribute__((aligned(16))) float Vf[KC * D];
@@ -146,8 +147,10 @@ __global__ __launch_bounds__(THREADS) void swin_fwd_f32_kernel(SwinArgs a) {
 hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream) {
     SwinArgs args = a;
     void* params[] = {&args};
-    return hipLaunchKernel(reinterpret_cast<const void*>(&swin_fwd_f32_kernel),
-                           dim3((unsigned)a.n_groups), dim3(THREADS), params, 0, stream);
+    const void* fn = a.head_dim == 32    ? reinterpret_cast<const void*>(&swin_fwd_f32_kernel<32>)
+                     : a.head_dim == 128 ? reinterpret_cast<const void*>(&swin_fwd_f32_kernel<128>)
+                                         : reinterpret_cast<const void*>(&swin_fwd_f32_kernel<kHeadDim>);
+    return hipLaunchKernel(fn, dim3((unsigned)a.n_groups), dim3(THREADS), params, 0, stream);
 }
 
 }  // namespace fla

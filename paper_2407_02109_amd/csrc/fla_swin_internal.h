@@ -31,7 +31,9 @@ struct FastDiv {
     }
 };
 
-constexpr int kHeadDim = 64;    // head_dim supported by the kernels
+constexpr int kHeadDim = 64;    // head_dim of every kernel (the training, RoPE and backward paths)
+// head_dim values of the plain forward kernels (bf16 and fp32): 64, and the instances 32 and 128
+__host__ __device__ constexpr bool fwd_head_dim_ok(int d) { return d == 32 || d == 64 || d == 128; }
 constexpr int kQueryBlock = 256; // queries of one window handled by one workgroup
 
 constexpr int kMaxGrids = 8;    // token grids of one multi-scale sequence
@@ -79,6 +81,7 @@ struct SwinArgs {
     float rope_scale;
     float rope_rev[kHeadDim / 4];
     double rope_freq[kHeadDim / 4];
+    int head_dim;               // channels per head (the forward kernels' instance)
 };
 
 

@@ -115,7 +115,8 @@ CASES = [
     ("FLA_ERR_NULL", dict(out=0)),
     ("FLA_ERR_ALIGN", dict(q=Q + 8)), ("FLA_ERR_ALIGN", dict(out=OUT + 2)),
     ("FLA_ERR_ALIGN", dict(v=V + 4)), ("FLA_ERR_ALIGN", dict(k=K + 1)),
-    ("FLA_ERR_HEAD_DIM", dict(head_dim=32)), ("FLA_ERR_HEAD_DIM", dict(head_dim=0)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=48)), ("FLA_ERR_HEAD_DIM", dict(head_dim=0)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=16)), ("FLA_ERR_HEAD_DIM", dict(head_dim=256)),
     ("FLA_ERR_WINDOW", dict(window=0)), ("FLA_ERR_WINDOW", dict(window=-4, shift=0)),
     ("FLA_ERR_SHIFT", dict(shift=16)), ("FLA_ERR_SHIFT", dict(shift=-1)),
     ("FLA_ERR_SHIFT", dict(window=1, shift=1)),
@@ -187,6 +188,24 @@ def test_no_device_reports_arch(lib):
     assert _call(fb.fla_swin_attn_fwd_f32) == _header_enum("FLA")["FLA_ERR_ARCH"]
 
 
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible")
+@pytest.mark.parametrize("d", [32, 128])
+def test_plain_forwards_take_head_dim_32_and_128(lib, d):
+    """The plain forwards (bf16 and fp32, one grid or several) pass every argument check with
+    head_dim 32 or 128 (here: FLA_ERR_ARCH, the last check, on a host without the GPU); the
+    training forward, RoPE and the backward take 64 only."""
+    codes = _header_enum("FLA")
+    assert _call(fb.fla_swin_attn_fwd, head_dim=d) == codes["FLA_ERR_ARCH"]
+    assert _call(fb.fla_swin_attn_fwd_f32, head_dim=d) == codes["FLA_ERR_ARCH"]
+    assert _call_ms(fb.fla_swin_attn_ms_fwd, head_dim=d) == codes["FLA_ERR_ARCH"]
+    assert _call_ms(fb.fla_swin_attn_ms_fwd_f32, head_dim=d) == codes["FLA_ERR_ARCH"]
+    assert _call_lse(head_dim=d) == codes["FLA_ERR_HEAD_DIM"]
+    assert _call_lse(f32=True, head_dim=d) == codes["FLA_ERR_HEAD_DIM"]
+    assert _call_bwd(head_dim=d) == codes["FLA_ERR_HEAD_DIM"]
+    assert _call_rope(head_dim=d) == codes["FLA_ERR_HEAD_DIM"]
+    assert _call_rope(f32=True, head_dim=d) == codes["FLA_ERR_HEAD_DIM"]
+
+
 @pytest.mark.parametrize("B,heads,H,W,k,s,pm", [
     (1, 12, 64, 64, 16, 8, 0), (1, 12, 256, 256, 16, 8, 0), (4, 12, 150, 203, 16, 8, 0),
     (1, 1, 32, 32, 8, 4, 0), (1, 1, 32, 32, 8, 0, 0), (2, 3, 20, 13, 8, 4, 1),
@@ -222,7 +241,7 @@ MS_CASES = [
     ("FLA_ERR_SHAPE", dict(grids=[])), ("FLA_ERR_SHAPE", dict(grids=[(4, 4)] * 9)),
     ("FLA_ERR_SHAPE", dict(grids=[(64, 64), (-1, 32)])), ("FLA_ERR_SHAPE", dict(B=-1)),
     ("FLA_ERR_NULL", dict(q=0)), ("FLA_ERR_ALIGN", dict(out=OUT + 4)),
-    ("FLA_ERR_HEAD_DIM", dict(head_dim=128)), ("FLA_ERR_SHIFT", dict(shift=16)),
+    ("FLA_ERR_HEAD_DIM", dict(head_dim=96)), ("FLA_ERR_SHIFT", dict(shift=16)),
     ("FLA_ERR_PAD_MODE", dict(pad_mode=3)),
     ("FLA_ERR_TOO_LARGE", dict(grids=[(64, 64), (4, 1 << 21)], window=8, shift=0)),
     ("FLA_ERR_ALIAS", dict(out=Q + (64 * 64 + 32 * 32 - 1) * 12 * 64 * 2)),   # last row of q

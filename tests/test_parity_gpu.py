@@ -90,6 +90,53 @@ def test_shapes(shape, pad_mode, dtype):
     _compare(out, ref, dtype)
 
 
+# head_dim 32 and 128, the plain forwards' other instances: ragged tails and B > 1, a grid
+# smaller than the window, window 32 (four query blocks per window), global attention with
+# several key chunks, a thin tall grid
+HD_SHAPES = [(2, 3, 20, 13, 8, 4), (1, 2, 5, 3, 16, 8), (1, 1, 64, 64, 32, 16), (1, 2, 24, 40, 64, 0),
+             (1, 1, 9, 300, 16, 15)]
+
+
+@pytest.mark.parametrize("d", [32, 128])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("pad_mode", [0, 1], ids=["mask", "kvtoken"])
+@pytest.mark.parametrize("shape", HD_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_head_dims(shape, pad_mode, dtype, d):
+    B, heads, H, W, window, shift = shape
+    _say("head_dim %d shape %s pad_mode %d %s" % (d, shape, pad_mode, dtype))
+    wl = synth.Workload("case", B, heads, H, W, d, window, shift, "bf16" if dtype == torch.bfloat16 else "f32",
+                        seed=(hash(shape) + d) % 1000, pad_mode=pad_mode)
+    q, k, v = synth.make_inputs(wl)
+    ref = O.swin_attention_textbook(synth.to_f64_numpy(q), synth.to_f64_numpy(k), synth.to_f64_numpy(v),
+                                    H, W, window, shift, pad_mode)
+    out = _run(q.cuda(), k.cuda(), v.cuda(), H, W, window, shift, pad_mode)
+    _compare(out, ref, dtype)
+
+
+@pytest.mark.parametrize("d,heads", [(32, 24), (128, 6)], ids=["d32", "d128"])
+def test_head_dim_full_size(d, heads):
+    """The 4096^2 layer's 256 x 256 grid at the ViT-B width of 768 channels as 24 heads of 32 or
+    6 of 128, bf16, whole output against the textbook oracle; and a multi-scale launch (the
+    128 x 128 grid and the 32 x 32 anchor grid, KV-token mode) of the same head shape."""
+    wl = synth.Workload("case", 1, heads, 256, 256, d, 16, 8, "bf16", seed=40 + d)
+    _say("head_dim %d full size" % d)
+    q, k, v = synth.make_inputs(wl)
+    out = _run(q.cuda(), k.cuda(), v.cuda(), 256, 256, 16, 8, 0)
+    ref = O.swin_attention_textbook(synth.to_f64_numpy(q), synth.to_f64_numpy(k), synth.to_f64_numpy(v),
+                                    256, 256, 16, 8, 0)
+    mx, mean = _compare(out, ref, torch.bfloat16)
+    print("[result] head_dim %d max %.3e mean %.3e" % (d, mx, mean), flush=True)
+    grids = [(128, 128), (32, 32)]
+    L = sum(h * w for h, w in grids)
+    g = torch.Generator().manual_seed(50 + d)
+    q, k, v = (torch.randn(1, L + extra, heads, d, generator=g).to(torch.bfloat16) for extra in (0, 1, 1))
+    out = torch.full_like(q, float("nan")).cuda()
+    fb.fla_swin_attn_ms_fwd(q.cuda(), k.cuda(), v.cuda(), out, 1, heads, grids, d, 16, 8, 1)
+    torch.cuda.synchronize()
+    ref = O.swin_attention_ms(synth.to_f64_numpy(q), synth.to_f64_numpy(k), synth.to_f64_numpy(v), grids, 16, 8, 1)
+    _compare(out, ref, torch.bfloat16)
+
+
 def test_global_window_equals_sdpa():
     """window >= grid with no shift is global attention: check against PyTorch's own."""
     _say("global vs sdpa")
