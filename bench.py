@@ -317,8 +317,9 @@ def summarize_cycle(prof_dir: str, command: str, out_dir: str = ""):
     print("\n".join(lines))
 
 
-def cpu_baseline(wl, q, k, v, budget_s: float):
-    """Time the fp64 oracle (textbook Plain Swin form) on this host's cores."""
+def cpu_baseline(wl, q, k, v, budget_s: float, out=None):
+    """Time the fp64 oracle (textbook Plain Swin form) on this host's cores; with the GPU's
+    output `out` of the same inputs, also its error on the heads the oracle computed."""
     import oracle
     from paper_2407_02109_amd import synth
     try:
@@ -333,31 +334,38 @@ def cpu_baseline(wl, q, k, v, budget_s: float):
 
     def layer(nh):
         if wl.rope:
-            oracle.swin_attention_rope(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], wl.H, wl.W, wl.window,
-                                       wl.shift, wl.pad_mode, wl.rope[0], wl.rope[1])
-        elif wl.grids:
-            oracle.swin_attention_ms(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], list(wl.grid_list),
-                                     wl.window, wl.shift, wl.pad_mode)
-        else:
-            oracle.swin_attention_textbook(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh],
-                                           wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
+            return oracle.swin_attention_rope(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], wl.H, wl.W, wl.window,
+                                              wl.shift, wl.pad_mode, wl.rope[0], wl.rope[1])
+        if wl.grids:
+            return oracle.swin_attention_ms(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh], list(wl.grid_list),
+                                            wl.window, wl.shift, wl.pad_mode)
+        return oracle.swin_attention_textbook(q64[:, :, :nh], k64[:, :, :nh], v64[:, :, :nh],
+                                              wl.H, wl.W, wl.window, wl.shift, wl.pad_mode)
 
     t0 = time.perf_counter()
     layer(1)
     per_head = time.perf_counter() - t0
     use_heads = int(max(1, min(heads, budget_s / 3.0 / max(per_head, 1e-6))))
     times = []
+    ref = None
     while len(times) < 3:
         t0 = time.perf_counter()
-        layer(use_heads)
+        ref = layer(use_heads)
         times.append((time.perf_counter() - t0) * heads / use_heads)
+    check = None
+    if out is not None:   # the GPU output of the timed entry point on the same inputs
+        import numpy as np
+        err = np.abs(synth.to_f64_numpy(out[:, :, :use_heads].cpu()) - ref)
+        check = {"heads": use_heads, "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean()),
+                 "bound_max": 2e-2, "bound_mean": 2e-3,
+                 "pass": bool(np.isfinite(err).all() and err.max() <= 2e-2 and err.mean() <= 2e-3)}
     return {"value": statistics.median(times) * 1e6, "unit": "us/layer", "cores": int(threads),
             "kind": "oracle",
             "sample": "fp64 textbook oracle on %d of %d heads of the %s layer, median of 3, "
                       "scaled to the whole layer; host %s with %d usable cores"
                       % (use_heads, heads, wl.name, cpu_model(), len(os.sched_getaffinity(0))),
             "cpu_model": cpu_model(), "usable_cores": len(os.sched_getaffinity(0)),
-            "bruteforce_tiny_us": bruteforce_tiny()}
+            "bruteforce_tiny_us": bruteforce_tiny(), "gpu_vs_oracle": check}
 
 
 def cpu_model() -> str:
@@ -388,6 +396,19 @@ def bruteforce_tiny() -> dict:
             times.append(time.perf_counter() - t0)
         res[name] = round(statistics.median(times) * 1e6, 1)
     return res
+
+
+def build_info(torch) -> dict:
+    """What the numbers were measured with: ROCm and torch versions, and the source hash of each
+    leg's kernels (the same hash the committed counter summaries carry)."""
+    rocm = None
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            rocm = f.read().strip()
+    except OSError:
+        pass
+    return {"rocm": rocm, "torch": torch.__version__, "hip": getattr(torch.version, "hip", None),
+            "kernel_hash": {leg: kernel_hash(leg) for leg in KERNELS}}
 
 
 def device_info(torch) -> dict:
@@ -591,22 +612,29 @@ def cycle_scan_leg(binding, synth, stream, steps: int, flush) -> dict:
                        "warm_p90_us": p90, "cold_mean_us": round(cold_us, 3)}}
 
 
-def cycle_scan_cpu_baseline(synth, channels: int = 128) -> dict:
+def cycle_scan_cpu_baseline(binding, synth, channels: int = 128) -> dict:
     """The fp64 Cycle-scan oracle on this host: the three copies laid out and scanned, over the
     whole sequence of the 4096^2 workload for `channels` evenly spaced channels (the channels
-    are independent), scaled to all of them."""
+    are independent), scaled to all of them; and the GPU's output on those channels against it."""
     import numpy as np
     import oracle
+    import torch
     wl = synth.CYCLE_WORKLOADS["cyclescan_img4096"]
-    x, delta, A, Bm, Cm = (t.numpy() for t in synth.make_cycle_inputs(wl.B, wl.L, wl.d, wl.N, wl.seed, wl.kind))
+    ins = synth.make_cycle_inputs(wl.B, wl.L, wl.d, wl.N, wl.seed, wl.kind)
+    x, delta, A, Bm, Cm = (t.numpy() for t in ins)
     ch = np.arange(channels) * (wl.d // channels)
     t0 = time.perf_counter()
-    oracle.cycle_scan.cycle_scan_channels(x, delta, A, Bm, Cm, ch, wl.repeats)
+    ref = oracle.cycle_scan.cycle_scan_channels(x, delta, A, Bm, Cm, ch, wl.repeats)
     dt = time.perf_counter() - t0
+    y = binding.cycle_scan(*(t.cuda() for t in ins), repeats=wl.repeats)
+    got = y[:, :, torch.as_tensor(ch, device=y.device)].double().cpu().numpy()
+    rel = float(np.abs(got - ref).max() / np.abs(ref).max())
+    bound = 4.0 * 2.0 ** -24 / float((ins[1].amin(dim=(0, 1))[:, None] * ins[2].abs()).min()) + 1e-6
     return {"value": round(dt * wl.d / channels * 1e6, 1), "unit": "us/call", "cores": 1, "kind": "oracle",
             "sample": "fp64 oracle (sequence laid out %d times, scanned token by token) on %d of %d channels "
                       "over all %d tokens, one run of %.1f s, scaled to all channels; host %s"
-                      % (wl.repeats, channels, wl.d, wl.L, dt, cpu_model())}
+                      % (wl.repeats, channels, wl.d, wl.L, dt, cpu_model()),
+            "gpu_vs_oracle": {"channels": channels, "max_err_rel_to_max": rel, "bound": bound, "pass": rel <= bound}}
 
 
 def main() -> int:
@@ -785,6 +813,7 @@ def main() -> int:
                      "settle_s": round(settle_s, 3), "settle_calls": settle_calls}
     rec["stream_ceiling"] = stream_ceiling(torch, qd, kd, vd, out, stream, flush)
     rec["device"] = device_info(torch)
+    rec["build"] = build_info(torch)
     if not args.no_backward:
         print("[bench] backward", file=sys.stderr, flush=True)
         rec["backward"] = backward_leg(binding, synth, wl, qd, kd, vd, stream, args.bwd_steps, mode, flush)
@@ -797,10 +826,12 @@ def main() -> int:
         copy_calibration()
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_budget)
+        step()   # the layer's output again (the streaming probe reused its buffer), for the oracle check
+        torch.cuda.synchronize()
+        rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, args.cpu_budget, out)
         if "cycle_scan" in rec:
             print("[bench] timing the CPU Cycle-scan oracle", file=sys.stderr, flush=True)
-            rec["cycle_scan"]["cpu_baseline"] = cycle_scan_cpu_baseline(synth)
+            rec["cycle_scan"]["cpu_baseline"] = cycle_scan_cpu_baseline(binding, synth)
     print(json.dumps(rec), flush=True)
     return 0
 
