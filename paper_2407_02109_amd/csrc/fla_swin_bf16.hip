@@ -43,6 +43,7 @@ namespace fla {
 namespace {
 
 constexpr int THREADS = 512;    // 8 waves of 64
+constexpr int kStoreNT = 2;     // cache policy of the output stores: non-temporal (nt)
 constexpr int QW = 32;          // queries per wave
 constexpr int KC = 256;         // keys staged in LDS at a time
 constexpr int KT = 32;          // keys per inner tile
@@ -437,7 +438,9 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
             const int r = rows * i + (lane >> TPR_LOG);
             const uint4 v = *reinterpret_cast<const uint4*>(Ks + (wave * QW + r) * KS + 8 * part);
             const unsigned off = r < nq ? addr(wq0 + r) + 16 * part : kOutside;   // tail rows: dropped
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orr, off, 0, 0);
+            // non-temporal: the output is not read again by this layer, and its lines should not
+            // displace inputs that a layer fitting the last-level cache reads again
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orr, off, 0, kStoreNT);
         }
     }
 }

@@ -187,7 +187,7 @@ def test_error_leaves_out_untouched():
     rc = fb.fla_swin_attn_fwd(q, k, v, out, 1, 2, 16, 16, 64, 8, 8, 0, check=False)
     torch.cuda.synchronize()
     assert rc == 6 and torch.isnan(out.float()).all()
-    rc = fb.fla_swin_attn_fwd(q, k, v, out, 1, 2, 16, 16, 32, 8, 4, 0, check=False)
+    rc = fb.fla_swin_attn_fwd(q, k, v, out, 1, 2, 16, 16, 48, 8, 4, 0, check=False)   # no head_dim 48 instance
     torch.cuda.synchronize()
     assert rc == 4 and torch.isnan(out.float()).all()
 
