@@ -16,6 +16,7 @@ static_assert(fla::kScratchBytes == FLA_SCRATCH_BYTES, "static scratch size of t
 namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;
+constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;   // MI355X Infinity Cache
 constexpr int64_t kMaxGroups = (int64_t(1) << 23) - 1;   // grid.x * 512 threads < 2^32
 
 // Windows of a grid list: the canvas has `origin` virtual tokens in front of each axis;
@@ -377,6 +378,8 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     a.div_2nbb = fla::FastDiv::make(2u * (unsigned)pr.geo.nbb);
     a.n_units = units;
     a.scale = (float)(1.0 / std::sqrt((double)head_dim));
+    // the call's bytes (q, k, v, out, dout read; dq, dk, dv written) against the 256 MB last-level cache
+    a.store_nt = 8.0 * B * double(pr.L) * double(pr.tok) * elem_bytes <= double(kLastLevelCacheBytes) ? 1 : 0;
     const hipStream_t s = stream;
     hipError_t e = elem_bytes != 2   ? fla::launch_swin_bwd_f32(a, s)
                    : window_kernel   ? fla::launch_swin_bwd_bf16_window(a, s)

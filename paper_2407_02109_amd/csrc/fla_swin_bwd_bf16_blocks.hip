@@ -464,15 +464,17 @@ __device__ __forceinline__ void key_role(const SwinBwdArgs& ba, const Block& k, 
         const __amdgpu_buffer_rsrc_t dkr = make_rsrc(static_cast<uint16_t*>(ba.dk) + kv_base, kv_bytes);
         const __amdgpu_buffer_rsrc_t dvr = make_rsrc(static_cast<uint16_t*>(ba.dv) + kv_base, kv_bytes);
         const int sp = lane & 7;
+        with_store_policy(ba.store_nt, [&](auto nt) {
 #pragma unroll
-        for (int it = 0; it < TL / 8; ++it) {
-            const int rl = TL * wave + 8 * it + (lane >> 3);
-            const unsigned off = rl < nkeys ? k.addr(key0 + rl) + 16 * sp : kOutside;
-            const uint4 kx = *reinterpret_cast<const uint4*>(Xs + sw(rl, 8 * sp));
-            const uint4 vx = *reinterpret_cast<const uint4*>(Ys + sw(rl, 8 * sp));
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, kx), dkr, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, vx), dvr, off, 0, 0);
-        }
+            for (int it = 0; it < TL / 8; ++it) {
+                const int rl = TL * wave + 8 * it + (lane >> 3);
+                const unsigned off = rl < nkeys ? k.addr(key0 + rl) + 16 * sp : kOutside;
+                const uint4 kx = *reinterpret_cast<const uint4*>(Xs + sw(rl, 8 * sp));
+                const uint4 vx = *reinterpret_cast<const uint4*>(Ys + sw(rl, 8 * sp));
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, kx), dkr, off);
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, vx), dvr, off);
+            }
+        });
     }
 }
 
@@ -604,13 +606,15 @@ __device__ __forceinline__ void query_role(const SwinBwdArgs& ba, const Block& k
         const __amdgpu_buffer_rsrc_t dqr =
             make_rsrc(static_cast<uint16_t*>(ba.dq) + q_base, ((long long)a.B * a.q_batch_stride - q_base) * 2);
         const int sp = lane & 7;
+        with_store_policy(ba.store_nt, [&](auto nt) {
 #pragma unroll
-        for (int it = 0; it < TL / 8; ++it) {
-            const int rl = TL * wave + 8 * it + (lane >> 3);
-            const unsigned off = rl < nq ? k.addr(q0 + rl) + 16 * sp : kOutside;
-            const uint4 qx4 = *reinterpret_cast<const uint4*>(Xs + sw(rl, 8 * sp));
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, qx4), dqr, off, 0, 0);
-        }
+            for (int it = 0; it < TL / 8; ++it) {
+                const int rl = TL * wave + 8 * it + (lane >> 3);
+                const unsigned off = rl < nq ? k.addr(q0 + rl) + 16 * sp : kOutside;
+                const uint4 qx4 = *reinterpret_cast<const uint4*>(Xs + sw(rl, 8 * sp));
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, qx4), dqr, off);
+            }
+        });
     }
 }
 

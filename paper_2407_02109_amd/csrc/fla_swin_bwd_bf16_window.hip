@@ -459,18 +459,20 @@ __global__ __launch_bounds__(THREADS) void swin_bwd_bf16_window_kernel(SwinBwdAr
         asm volatile("" ::: "memory");   // staged rows are read back by other lanes
         const uint16_t* qbase_s = Ks + TL * wave * RS;
         const int sp = lane & 7;
+        with_store_policy(ba.store_nt, [&](auto nt) {
 #pragma unroll
-        for (int it = 0; it < TL / 8; ++it) {
-            const int rl = 8 * it + (lane >> 3);
-            const int tok = TL * wave + rl;
-            const unsigned off = tok < n ? addr(tok) + 16 * sp : kOutside;
-            const uint4 kx = *reinterpret_cast<const uint4*>(Qs + tok * RS + 8 * sp);
-            const uint4 vx = *reinterpret_cast<const uint4*>(dOs + tok * RS + 8 * sp);
-            const uint4 qx = *reinterpret_cast<const uint4*>(qbase_s + rl * RS + 8 * sp);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, kx), dkr, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, vx), dvr, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, qx), dqr, off, 0, 0);
-        }
+            for (int it = 0; it < TL / 8; ++it) {
+                const int rl = 8 * it + (lane >> 3);
+                const int tok = TL * wave + rl;
+                const unsigned off = tok < n ? addr(tok) + 16 * sp : kOutside;
+                const uint4 kx = *reinterpret_cast<const uint4*>(Qs + tok * RS + 8 * sp);
+                const uint4 vx = *reinterpret_cast<const uint4*>(dOs + tok * RS + 8 * sp);
+                const uint4 qx = *reinterpret_cast<const uint4*>(qbase_s + rl * RS + 8 * sp);
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, kx), dkr, off);
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, vx), dvr, off);
+                store_row<decltype(nt)::value>(__builtin_bit_cast(u32x4, qx), dqr, off);
+            }
+        });
     }
 }
 

@@ -33,6 +33,24 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, lo
     const int n = bytes < kMaxRecords ? (int)bytes : kMaxRecords;
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
+
+// A 16-byte row piece of a result, with the non-temporal cache policy (NT) or the ordinary one.
+// The backward stores its gradients non-temporally when the call's bytes fit the last-level
+// cache: the next call then finds its inputs still there (at 64x64 tokens 11% faster); beyond
+// that cache ordinary stores measured ~2% faster.  The caller picks NT once per workgroup
+// (with_store_policy), so the store loop has no branch.
+template <bool NT>
+__device__ __forceinline__ void store_row(u32x4 v, __amdgpu_buffer_rsrc_t r, unsigned off) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, NT ? 2 : 0);
+}
+template <typename F>
+__device__ __forceinline__ void with_store_policy(bool nt, F&& f) {
+    if (nt)
+        f(std::integral_constant<bool, true>{});
+    else
+        f(std::integral_constant<bool, false>{});
+}
+
 __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, unsigned off) {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }

@@ -132,6 +132,7 @@ struct SwinBwdArgs {
     FastDiv div_2nbb;           // bf16 workgroup decode: division by 2 * nbb
     int64_t n_units;            // bf16: B * heads * windows
     float scale;                // 1 / sqrt(head_dim)
+    int store_nt;               // bf16: gradient rows stored non-temporally (see store_row)
 };
 
 // Workgroups of one bf16 backward launch: both roles of every block of every unit, in
