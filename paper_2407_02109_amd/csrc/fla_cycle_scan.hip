@@ -10,19 +10,22 @@
 // (S_k = (1 + P_L + ... + P_L^{k-1}) S_1).  Summed over the r copies:
 //   sum_k h_t^(k) = r h1_t + P_t G,   G = sum_{j=0}^{r-2} (r-1-j) P_L^j S_1,
 // which is the scan of r x started from G instead of zero.  Over chunks of T tokens:
-//   pass A  (cycle_scan_chunks): every chunk scanned from zero; its end state and its sum of
-//           Delta go to the workspace;
+//   pass A  (cycle_scan_chunks): every chunk scanned from zero; its output y1_t = C_t . h1_t
+//           goes to y, its end state and its sum of Delta to the workspace;
 //   pass B  (cycle_scan_carries): per (batch entry, channel, state), the chunks' carries in
 //           order: the state entering chunk c, H_{c-1}, the state S_1 after the sequence, and
 //           E_c = r H_{c-1} + P(start -> chunk c) G, the state from which chunk c of the summed
 //           scan starts;
-//   pass C  (cycle_scan_outputs): every chunk scanned from E_c with input r x, y written.
+//   pass C  (cycle_scan_outputs): within chunk c the summed scan's state is r h1_t + P_t E_c
+//           (P_t: the decay from the chunk's start to t), so y_t = r y1_t +
+//           sum_n C_t[n] exp(a_n cum_t) E_c[n], cum_t the sum of Delta from the chunk's start
+//           to t; no recurrence, y overwritten in place.
 // Two passes of exponentials over the data, where scanning the laid-out copies takes r.
 //
 // A wave takes 64 channels of one chunk: a lane holds one channel's N states in registers;
-// x and Delta of a token are one coalesced 256-byte read per wave, and B_t, C_t, the same for
-// every channel, are wave-uniform reads.  Bound by the vector ALU (one exponential per
-// token, channel and state in each of passes A and C).
+// x (pass C: y1) and Delta of a token are one coalesced 256-byte read per wave, and B_t, C_t,
+// the same for every channel, are wave-uniform reads.  Bound by the vector ALU (one
+// exponential per token, channel and state in each of passes A and C).
 #include "fla_cycle_scan.h"
 #include "fla_swin_device.h"
 
@@ -54,29 +57,38 @@ __global__ __launch_bounds__(64) void cycle_scan_chunks(CycleArgs c) {
     const bool ok = ch < c.d;
     const int chs = ok ? ch : c.d - 1;
     // the state scaled by a, g = a h, takes one product less per step:
-    // g <- dA g + (dA - 1) u b
-    float a2[N], g[N];
+    // g <- dA g + (dA - 1) u b; the output C . h = sum_n (C[n] / a[n]) g[n]
+    float a2[N], ia[N], g[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) {
-        a2[n] = c.A[(size_t)chs * N + n] * kLog2e;
+        const float a = c.A[(size_t)chs * N + n];
+        a2[n] = a * kLog2e;
+        ia[n] = 1.f / a;
         g[n] = 0.f;
     }
     const int t0 = chunk * c.T;
     const int t1 = min(t0 + c.T, c.L);
     const float* xp = c.x + (size_t)b * c.L * c.d + chs;
     const float* dp = c.delta + (size_t)b * c.L * c.d + chs;
-    const float* bp = c.Bm + (size_t)b * c.L * N;
+    const size_t rb = (size_t)b * c.L;
     float sd = 0.f;
     auto step = [&](int t, float u, float dl) {
-        float w[N];
-        load_row<N>(bp + (size_t)t * N, w);
+        const size_t row = rb + t;
+        float w[N], cv[N];
+        load_row<N>(c.Bm + row * N, w);
+        load_row<N>(c.Cm + row * N, cv);
+        float acc[2] = {0.f, 0.f};   // two sums, two dependency chains
 #pragma unroll
         for (int n = 0; n < N; ++n) {
             const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
             const float z = u * w[n];
             g[n] = __builtin_fmaf(dA, g[n] + z, -z);   // dA g + (dA - 1) z
+            acc[n & 1] = __builtin_fmaf(cv[n] * ia[n], g[n], acc[n & 1]);
         }
         sd += dl;
+        // lanes past the last channel compute channel d - 1 from the same inputs: the value
+        // they store there is the same
+        c.y[row * c.d + chs] = acc[0] + acc[1];
     };
     // whole groups of kTokens tokens: their x and Delta loaded together, one wait per group
     const int tfull = t0 + (t1 - t0) / kTokens * kTokens;
@@ -169,50 +181,47 @@ __global__ __launch_bounds__(64) void cycle_scan_outputs(CycleArgs c) {
     const bool ok = ch < c.d;
     const int chs = ok ? ch : c.d - 1;
     const float* hw = c.ws_h + (((size_t)b * c.nch + chunk) * c.d + chs) * N;
-    float a2[N], ia[N], h[N];
+    float a2[N], e[N];
 #pragma unroll
     for (int n = 0; n < N; ++n) {
-        const float a = c.A[(size_t)chs * N + n];
-        a2[n] = a * kLog2e;
-        ia[n] = 1.f / a;
-        h[n] = hw[n];
+        a2[n] = c.A[(size_t)chs * N + n] * kLog2e;
+        e[n] = hw[n];   // E_c
     }
     const float r = (float)c.repeats;
     const int t0 = chunk * c.T;
     const int t1 = min(t0 + c.T, c.L);
-    const float* xp = c.x + (size_t)b * c.L * c.d + chs;
-    const float* dp = c.delta + (size_t)b * c.L * c.d + chs;
     const size_t rb = (size_t)b * c.L;
-    auto step = [&](int t, float xv, float dl) {
+    float* yp = c.y + rb * c.d + chs;
+    const float* dp = c.delta + rb * c.d + chs;
+    float cum = 0.f;   // sum of Delta from the chunk's start to t
+    auto step = [&](int t, float y1, float dl) {
         const size_t row = rb + t;
-        const float u = r * xv;
-        float w[N], cv[N];
-        load_row<N>(c.Bm + row * N, w);
+        float cv[N];
         load_row<N>(c.Cm + row * N, cv);
-        float acc[2] = {0.f, 0.f};   // two sums, two dependency chains
+        cum += dl;
+        float acc[2] = {r * y1, 0.f};
 #pragma unroll
         for (int n = 0; n < N; ++n) {
-            const float dA = __builtin_amdgcn_exp2f(dl * a2[n]);
-            const float z = u * w[n] * ia[n];
-            h[n] = __builtin_fmaf(dA, h[n] + z, -z);
-            acc[n & 1] = __builtin_fmaf(cv[n], h[n], acc[n & 1]);
+            const float p = __builtin_amdgcn_exp2f(a2[n] * cum);   // decay from the chunk's start
+            acc[n & 1] = __builtin_fmaf(cv[n], p * e[n], acc[n & 1]);
         }
-        // lanes past the last channel compute channel d - 1 from the same inputs: the value
-        // they store there is the same
-        c.y[row * c.d + chs] = acc[0] + acc[1];
+        // each lane reads y1 and then writes y at its own address; lanes past the last
+        // channel, which repeat channel d - 1, must not write there (the lane of channel d - 1
+        // may already have replaced the y1 they read)
+        if (ok) yp[(size_t)t * c.d] = acc[0] + acc[1];
     };
     const int tfull = t0 + (t1 - t0) / kTokens * kTokens;
     for (int tg = t0; tg < tfull; tg += kTokens) {
-        float uu[kTokens], dd[kTokens];
+        float yy[kTokens], dd[kTokens];
 #pragma unroll
         for (int j = 0; j < kTokens; ++j) {
-            uu[j] = xp[(size_t)(tg + j) * c.d];
+            yy[j] = yp[(size_t)(tg + j) * c.d];
             dd[j] = dp[(size_t)(tg + j) * c.d];
         }
 #pragma unroll
-        for (int j = 0; j < kTokens; ++j) step(tg + j, uu[j], dd[j]);
+        for (int j = 0; j < kTokens; ++j) step(tg + j, yy[j], dd[j]);
     }
-    for (int t = tfull; t < t1; ++t) step(t, xp[(size_t)t * c.d], dp[(size_t)t * c.d]);
+    for (int t = tfull; t < t1; ++t) step(t, yp[(size_t)t * c.d], dp[(size_t)t * c.d]);
 }
 
 template <int N>
