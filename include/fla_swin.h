@@ -77,9 +77,7 @@ typedef enum {
                               2^23 workgroups or more, the rows of one window span 2 GiB or
                               more (min(window, Hgrid) * Wgrid * heads * head_dim * element
                               bytes), or min(window,Hgrid) * min(window,Wgrid)^2 > 2^32     */
-    FLA_ERR_UNSUPPORTED = 12, /* bf16 RoPE forward or backward with min(window, H) or
-                                 min(window, W) above 32; Cycle-scan with N not a power
-                                 of two up to 32                                          */
+    FLA_ERR_UNSUPPORTED = 12, /* Cycle-scan with N not a power of two up to 32          */
     FLA_ERR_WORKSPACE = 13, /* backward, Cycle-scan: workspace NULL or smaller than the
                                matching _workspace() function reports                     */
     FLA_ERR_ROPE = 14,     /* RoPE entry points: rope_theta not finite and > 0, or
@@ -155,10 +153,11 @@ int fla_swin_attn_ms_work(int B, int heads, int n_grids, const int* grid_hw, int
  * j = 0 .. head_dim/4 - 1; likewise k.  (y, x) are grid coordinates; the pad token of
  * FLA_PAD_KVTOKEN mode has no position and is not rotated.  The rotation runs in fp32 on
  * the loaded values (bf16: rounded back to bf16 before the products), so no rotated copy of
- * q or k is written.  rope_theta = 10000, rope_scale = 1 is RoFormer's choice.  Errors as
- * for fla_swin_attn_fwd (head_dim 64 only), plus FLA_ERR_ROPE, and FLA_ERR_UNSUPPORTED (after FLA_ERR_TOO_LARGE)
- * when the bf16 kernel gets a window of more than 32 rows or columns (its per-window
- * cos/sin table covers 32 x 32; the fp32 entry point takes any window). */
+ * q or k is written.  rope_theta = 10000, rope_scale = 1 is RoFormer's choice.  Any window:
+ * the bf16 kernel takes (cos, sin) from a per-window table when the window's rectangle fits
+ * 32 x 32 and computes them per rotated piece otherwise, with the same fp32 arithmetic, so
+ * the result does not depend on the route.  Errors as for fla_swin_attn_fwd (head_dim 64
+ * only), plus FLA_ERR_ROPE. */
 int fla_swin_attn_rope_fwd(const void* q, const void* k, const void* v, void* out,
                            int B, int heads, int Hgrid, int Wgrid, int head_dim,
                            int window, int shift, int pad_mode, float rope_theta,
@@ -285,9 +284,7 @@ int fla_swin_attn_ms_bwd_f32(const float* q, const float* k, const float* v, con
  * rotation (dq = R^T dq', dk = R^T dk'); dv is unchanged, and the pad token, which is never
  * rotated, gets its gradient as in fla_swin_attn_bwd.  out and lse are those of
  * fla_swin_attn_rope_fwd_lse.  Arguments and errors as for fla_swin_attn_bwd, plus
- * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE) and FLA_ERR_UNSUPPORTED (checked after
- * FLA_ERR_TOO_LARGE) for windows of more than 32 rows or columns, the limit of the bf16 RoPE
- * forward whose out and lse it takes. */
+ * FLA_ERR_ROPE (checked after FLA_ERR_PAD_MODE). */
 int fla_swin_attn_rope_bwd(const void* q, const void* k, const void* v, const void* out,
                            const void* dout, const float* lse, void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, int B, int heads, int Hgrid,

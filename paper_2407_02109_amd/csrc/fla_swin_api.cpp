@@ -252,11 +252,6 @@ int forward(const void* q, const void* k, const void* v, void* out, float* lse, 
     Problem pr;
     st = check_limits(B, heads, n_grids, hw, head_dim, window, shift, pad_mode, elem_bytes, &pr);
     if (st != FLA_OK) return st;
-    if (rope && elem_bytes == 2)   // the bf16 kernel's per-window RoPE table covers 32 x 32
-        for (int i = 0; i < n_grids; ++i)
-            if ((window < hw[2 * i] ? window : hw[2 * i]) > fla::kRopeMaxSide ||
-                (window < hw[2 * i + 1] ? window : hw[2 * i + 1]) > fla::kRopeMaxSide)
-                return FLA_ERR_UNSUPPORTED;
 
     const int64_t q_bytes = int64_t(B) * pr.L * pr.tok * elem_bytes;
     const int64_t kv_bytes = int64_t(B) * pr.kv_rows * pr.tok * elem_bytes;
@@ -318,13 +313,8 @@ int backward(const void* q, const void* k, const void* v, const void* out, const
     // the bf16 launch: both roles of every block of every (batch entry, window, head)
     const int64_t units = int64_t(B) * heads * pr.geo.n_windows;
     if (elem_bytes == 2 && fla::bwd_bf16_groups(units, pr.geo.nbb) > kMaxGroups) return FLA_ERR_TOO_LARGE;
-    // RoPE training is bf16 only, with the RoPE forward's window limit
+    // RoPE training is bf16 only (no fp32 RoPE backward entry point exists)
     if (rope && elem_bytes != 2) return FLA_ERR_UNSUPPORTED;
-    if (rope)
-        for (int i = 0; i < n_grids; ++i)
-            if ((window < hw[2 * i] ? window : hw[2 * i]) > fla::kRopeMaxSide ||
-                (window < hw[2 * i + 1] ? window : hw[2 * i + 1]) > fla::kRopeMaxSide)
-                return FLA_ERR_UNSUPPORTED;
     const int64_t need = workspace_bytes(B, heads, pr.geo, pad_mode);
     if (static_scratch) {
         if (need > fla::kScratchBytes) return FLA_ERR_SCRATCH;
@@ -625,7 +615,7 @@ const char* fla_status_string(int status) {
         case FLA_ERR_ALIAS: return "an output overlaps an input or another output";
         case FLA_ERR_ARCH: return "no gfx950 (MI355X) device is current";
         case FLA_ERR_LAUNCH: return "kernel launch failed";
-        case FLA_ERR_UNSUPPORTED: return "window too large for the bf16 RoPE entry points (32 x 32), or RoPE training in fp32";
+        case FLA_ERR_UNSUPPORTED: return "unsupported: Cycle-scan state size N not a power of two up to 32";
         case FLA_ERR_WORKSPACE: return "workspace missing or smaller than fla_swin_attn_bwd_workspace()";
         case FLA_ERR_ROPE: return "rope_theta must be finite and > 0, rope_scale finite";
         case FLA_ERR_SCRATCH: return "problem needs more workspace than the 16 MiB static scratch of the allocation-free backward";

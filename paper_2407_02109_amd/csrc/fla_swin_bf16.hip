@@ -164,7 +164,15 @@ __device__ __forceinline__ void rope_rotate8_tab(uint16_t (&x)[8], const float2*
     }
 }
 
-constexpr int kRopeTab = kRopeMaxSide;   // window rows / columns covered by the per-workgroup RoPE table
+// The same rotation with (cos, sin) taken directly at position pos: the table's entries come
+// from the same fp32 expression (rope_cs), so both give the same bits.
+__device__ __forceinline__ void rope_rotate8_at(uint16_t (&x)[8], float pos, const float* rev) {
+    float2 cs[4];
+    for (int i = 0; i < 4; ++i) cs[i] = rope_cs(pos, rev[i]);
+    rope_rotate8_tab(x, cs);
+}
+
+constexpr int kRopeTab = 32;   // window rows / columns covered by the per-workgroup RoPE table
 
 template <bool MULTI, bool ROPE, int D>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(Cfg<D>::WAVES, Cfg<D>::WAVES)))
@@ -252,11 +260,12 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
     const int nq = min(QW, n - wq0);   // queries of this wave (<= 0: the wave only loads)
 
     // ---- Q in registers, B-operand layout: lane holds q[query li][16*st + 8*h .. +8]
+    // RoPE: windows whose rectangle fits kRopeTab x kRopeTab take (cos, sin) from one table per
+    // workgroup for their row and column positions (1024 entries, two per thread, filled
+    // before anything else is live in registers); wider ones compute them per rotated piece
+    const bool rope_tab = ROPE && wr.rows <= kRopeTab && wr.cols <= kRopeTab;
     if constexpr (ROPE) {
-        // one (cos, sin) table per workgroup for the window's row and column positions (1024
-        // entries, two per thread; the host admits only windows whose rectangle fits
-        // kRopeTab x kRopeTab), filled before anything else is live in registers
-        for (int e = tid; e < 2 * kRopeTab * (D / 4); e += THREADS) {
+        for (int e = tid; rope_tab && e < 2 * kRopeTab * (D / 4); e += THREADS) {
             const int axis = e / (kRopeTab * (D / 4)), p = (e / (D / 4)) % kRopeTab, j = e % (D / 4);
             const float pos = (float)(axis ? wr.x0 + p : wr.y0 + p) * a.rope_scale;
             float t = pos * a.rope_rev[j];
@@ -356,8 +365,12 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                         window_rc(addr, kc0 + key, kr_, kc_);
                         uint16_t e[8];
                         __builtin_memcpy(e, &Ks[key * KS + part * 8], 16);
-                        rope_rotate8_tab(e, Rtab + ((part < 4 ? 0 : kRopeTab) + (part < 4 ? kr_ : kc_)) * (D / 4) +
-                                                4 * (part & 3));
+                        if (rope_tab)
+                            rope_rotate8_tab(e, Rtab + ((part < 4 ? 0 : kRopeTab) + (part < 4 ? kr_ : kc_)) * (D / 4) +
+                                                    4 * (part & 3));
+                        else
+                            rope_rotate8_at(e, (float)(part < 4 ? wr.y0 + kr_ : wr.x0 + kc_) * a.rope_scale,
+                                            a.rope_rev + 4 * (part & 3));
                         __builtin_memcpy(&Ks[key * KS + part * 8], e, 16);
                     }
                 }
@@ -388,7 +401,11 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                     uint16_t e[8];
                     __builtin_memcpy(e, &qop[st], 16);
                     const int j0 = 8 * (st & 1) + 4 * h;
-                    rope_rotate8_tab(e, Rtab + ((st < 2 ? 0 : kRopeTab) + (st < 2 ? qr_ : qc_)) * (D / 4) + j0);
+                    if (rope_tab)
+                        rope_rotate8_tab(e, Rtab + ((st < 2 ? 0 : kRopeTab) + (st < 2 ? qr_ : qc_)) * (D / 4) + j0);
+                    else
+                        rope_rotate8_at(e, (float)(st < 2 ? wr.y0 + qr_ : wr.x0 + qc_) * a.rope_scale,
+                                        a.rope_rev + j0);
                     __builtin_memcpy(&qop[st], e, 16);
                 }
             }

@@ -109,7 +109,6 @@ hipError_t launch_swin_fwd_f32(const SwinArgs& a, hipStream_t stream);
 
 constexpr int kBwdBlock = 128;    // tokens of one bf16 backward block (and of one streamed chunk)
 constexpr int kPadPartial = 2 * kHeadDim;   // floats per pad-gradient partial: dk then dv
-constexpr int kRopeMaxSide = 32;   // bf16 RoPE forward: window rows and columns it takes
 
 // Backward pass: the forward's geometry plus the gradient tensors.  Inputs q, k, v (in f),
 // out, dout and lse; outputs dq, dk, dv.  ws holds one pad-gradient partial per (b, head,

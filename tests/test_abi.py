@@ -372,20 +372,24 @@ def test_bwd_argument_checks(lib, f32, status, kw):
     assert _call_bwd(f32=f32, **kw) == _header_enum("FLA")[status]
 
 
-def test_bwd_wide_windows_supported_except_rope(lib):
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible (the calls would launch on fake pointers)")
+def test_bwd_wide_windows_supported(lib):
+    """Every argument check passes (the call gets as far as the device query) for windows of
+    more than 256 tokens, also with RoPE: windows wider than the bf16 RoPE forward's 32 x 32
+    cos / sin table take (cos, sin) per rotated piece."""
     codes = _header_enum("FLA")
     # 17 x 17 = 289 tokens per window: three 128-token blocks of the bf16 kernel; the fp32
     # kernels take it as well
-    assert _call_bwd(window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_bwd(f32=True, window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    # the RoPE backward follows the bf16 RoPE forward's 32 x 32 window limit
-    assert _call_rope_bwd(window=17, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_rope_bwd(window=32, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_rope_bwd(window=33, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_rope_bwd(Hgrid=4, window=64, shift=0) == codes["FLA_ERR_UNSUPPORTED"]
-    assert _call_rope_bwd(Hgrid=4, Wgrid=32, window=64, shift=0) != codes["FLA_ERR_UNSUPPORTED"]
+    assert _call_bwd(window=17, shift=0) == codes["FLA_ERR_ARCH"]
+    assert _call_bwd(f32=True, window=17, shift=0) == codes["FLA_ERR_ARCH"]
+    for kw in (dict(window=17), dict(window=32), dict(window=33), dict(Hgrid=4, window=64),
+               dict(Hgrid=64, Wgrid=64, window=64)):
+        assert _call_rope_bwd(shift=0, **kw) == codes["FLA_ERR_ARCH"]
+        assert fb.fla_swin_attn_rope_fwd(Q, K, V, OUT, 1, 12, kw.get("Hgrid", 64), kw.get("Wgrid", 64), 64,
+                                         kw["window"], 0, 0, 1e4, 1.0, 0, check=False) == codes["FLA_ERR_ARCH"]
 
 
+@pytest.mark.skipif(_gpu_visible(), reason="a GPU is visible (the calls would launch on fake pointers)")
 def test_bwd_mask_mode_needs_no_workspace(lib):
     codes = _header_enum("FLA")
     for kw in (dict(), dict(window=17, shift=0), dict(window=32, shift=16)):

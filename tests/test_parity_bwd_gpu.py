@@ -171,27 +171,6 @@ def test_bf16_backward_wide_windows_multi_scale(pm):
         _check_grad(name, got, ref, False)
 
 
-def test_bf16_rope_backward_window_limit():
-    """The RoPE backward takes the windows the bf16 RoPE forward takes (at most 32 rows and
-    columns) and refuses wider ones without touching its outputs."""
-    B, heads, H, W = 1, 1, 40, 24
-    wl = _wl(B, heads, H, W, 20, 10, "bf16", 0, 1)
-    q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
-    z = torch.zeros_like(q)
-    lse = torch.zeros((B, heads, H * W), dtype=torch.float32, device="cuda")
-    dq = torch.full_like(q, float("nan"))
-    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, dq, torch.empty_like(kk),
-                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 40, 0, 0, 1e4, 1.0, 0,
-                                   check=False)
-    torch.cuda.synchronize()
-    assert rc == 12 and torch.isnan(dq.float()).all()   # FLA_ERR_UNSUPPORTED
-    rc = fb.fla_swin_attn_rope_bwd(q, kk, v, z, z.clone(), lse, dq, torch.empty_like(kk),
-                                   torch.empty_like(v), None, 0, B, heads, H, W, 64, 20, 10, 0, 1e4, 1.0, 0,
-                                   check=False)
-    torch.cuda.synchronize()
-    assert rc == 0
-
-
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
 def test_multiscale_backward(dtype, pm):

@@ -43,6 +43,9 @@ def _compare(got, ref, f32):
 SHAPES = [  # B, heads, H, W, window, shift
     (2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 7, 16, 0),
     (1, 1, 9, 300, 16, 15), (1, 1, 1, 1, 1, 0), (1, 2, 40, 24, 32, 16),
+    # windows wider than the bf16 kernel's 32 x 32 cos / sin table: (cos, sin) per rotated
+    # piece; the second mixes 20 x 20 windows (table) with 40 x 40 ones (direct)
+    (1, 1, 40, 24, 40, 0), (1, 2, 64, 64, 40, 20),
 ]
 ROPES = [(10000.0, 1.0), (100.0, 0.5)]
 
@@ -102,7 +105,9 @@ def test_full_size_rope_sampled():
 
 # ---- RoPE training: forward with log-sum-exp, backward (gradients of the unrotated q, k, v)
 BWD_SHAPES = [(2, 2, 64, 64, 16, 8), (1, 3, 37, 29, 16, 8), (2, 2, 20, 13, 8, 3), (1, 1, 9, 300, 16, 15),
-              (1, 2, 40, 37, 20, 10), (1, 1, 40, 40, 32, 16)]   # the last two: windows over 256 tokens
+              # windows over 256 tokens; the last three also wider than 32 rows or columns
+              (1, 2, 40, 37, 20, 10), (1, 1, 40, 40, 32, 16), (1, 1, 40, 24, 40, 0), (1, 2, 64, 64, 40, 20),
+              (1, 1, 64, 64, 64, 0)]
 
 
 def _check_grad(name, got, ref, f32, bulk=True):
