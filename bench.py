@@ -429,6 +429,59 @@ def device_info(torch) -> dict:
     return info
 
 
+def parse_sclk(text: str):
+    """The current engine clock (MHz) from the text of pp_dpm_sclk: the line marked '*'."""
+    for line in text.splitlines():
+        if line.rstrip().endswith("*") and ":" in line:
+            try:
+                return int(line.split(":")[1].strip().lower().split("mhz")[0])
+            except ValueError:
+                return None
+    return None
+
+
+class ClockSampler:
+    """Samples the engine clock from sysfs every `period` seconds in a thread while a block
+    runs (`with sampler:`); `median()` of the samples, None when the clock is not readable
+    (no sysfs file, or several GPUs whose files cannot be told apart)."""
+
+    def __init__(self, period: float = 0.05):
+        import glob
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if len(paths) == 1 else None
+        self.period = period
+        self.samples = []
+
+    def _run(self):
+        while not self._stop.wait(self.period):
+            try:
+                with open(self.path) as f:
+                    mhz = parse_sclk(f.read())
+            except OSError:
+                mhz = None
+            if mhz is not None:
+                self.samples.append(mhz)
+
+    def __enter__(self):
+        import threading
+        self.samples = []
+        if self.path is not None:
+            self._stop = threading.Event()
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self.path is not None:
+            self._stop.set()
+            self._thread.join()
+        return False
+
+    def median(self):
+        xs = sorted(self.samples)
+        return xs[len(xs) // 2] if xs else None
+
+
 def percentiles(xs):
     xs = sorted(xs)
     pick = lambda f: xs[min(len(xs) - 1, int(f * len(xs)))]
@@ -541,9 +594,12 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int, mode: str, 
 
     fwd_us = mean_us(fwd, steps)
     fwd()
-    warm_us = mean_us(bwd, steps)
+    clk_warm, clk_cold = ClockSampler(), ClockSampler()
+    with clk_warm:
+        warm_us = mean_us(bwd, steps)
     p10, p50, p90 = percentiles(per_call_us(bwd, stream, 100))
-    cold = per_call_us(bwd, stream, max(steps // 5, 50), before=flush)
+    with clk_cold:
+        cold = per_call_us(bwd, stream, max(steps // 5, 50), before=flush)
     cold_us = statistics.mean(cold)
     c10, c50, c90 = percentiles(cold)
     assert torch.isfinite(dq[:, :64].float()).all() and torch.isfinite(dk[:, :64].float()).all()
@@ -559,7 +615,8 @@ def backward_leg(binding, synth, wl, qd, kd, vd, stream, steps: int, mode: str, 
             "alg_flops": flops, "alg_bytes": nbytes,
             "timing": {"warm_mean_us": round(warm_us, 3), "warm_p10_us": p10, "warm_p50_us": p50,
                        "warm_p90_us": p90, "cold_mean_us": round(cold_us, 3), "cold_p10_us": c10,
-                       "cold_p50_us": c50, "cold_p90_us": c90}}
+                       "cold_p50_us": c50, "cold_p90_us": c90,
+                       "sclk_mhz_p50": {"warm": clk_warm.median(), "cold": clk_cold.median()}}}
 
 
 def cycle_scan_leg(binding, synth, stream, steps: int, flush) -> dict:
@@ -753,19 +810,25 @@ def main() -> int:
     print("[bench] timing %d %s steps" % (args.steps, mode), file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    if mode == "cold":
-        cold = per_call_us(step, stream, args.steps, before=flush)
-        us = statistics.mean(cold)
-    else:
-        us = warm_mean(args.steps)
-    torch.cuda.synchronize()
+    clk_timed = ClockSampler()
+    with clk_timed:
+        if mode == "cold":
+            cold = per_call_us(step, stream, args.steps, before=flush)
+            us = statistics.mean(cold)
+        else:
+            us = warm_mean(args.steps)
+        torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    # the other mode, outside the timed region
-    if mode == "cold":
-        warm_us = warm_mean(max(args.steps, 1000))
-    else:
-        cold = per_call_us(step, stream, 100, before=flush)
-        warm_us = us
+    # the other mode, outside the timed region (warm: for about half a second, so that the
+    # clock samples cover it)
+    clk_other = ClockSampler()
+    with clk_other:
+        if mode == "cold":
+            warm_us = statistics.mean(warm_mean(1000) for _ in range(max(1, round(0.5e6 / (1000 * us)))))
+        else:
+            cold = per_call_us(step, stream, 100, before=flush)
+            warm_us = us
+    sclk = {mode: clk_timed.median(), ("warm" if mode == "cold" else "cold"): clk_other.median()}
     cold_us = statistics.mean(cold)
     tflops = flops / (us * 1e-6) / 1e12
     assert torch.isfinite(out[:, :64].float()).all()
@@ -810,7 +873,8 @@ def main() -> int:
                      "cold_p50_us": c50, "cold_p90_us": c90, "cold_calls": len(cold),
                      "launch_one_token_p50_us": l50,
                      "flush": "read-only sum over %d MiB before each cold call" % (FLUSH_BYTES >> 20),
-                     "settle_s": round(settle_s, 3), "settle_calls": settle_calls}
+                     "settle_s": round(settle_s, 3), "settle_calls": settle_calls,
+                     "sclk_mhz_p50": sclk}
     rec["stream_ceiling"] = stream_ceiling(torch, qd, kd, vd, out, stream, flush)
     rec["device"] = device_info(torch)
     rec["build"] = build_info(torch)

@@ -114,3 +114,19 @@ def test_cycle_summary_splits_cold_and_warm_calls_and_scales_counters(tmp_path):
     assert "| cycle_scan_outputs<32> | 1 | 40.00 | 1 | 30.00 | - | %.1f |" % (4000 * 1024 / 1e6) in text
     assert "| sum (one call) | | 74.00 | | 52.00 | | |" in text
     assert "Kernel source hash: %s" % bench.kernel_hash("cycle") in text
+
+
+def test_parse_sclk_takes_the_marked_level():
+    text = "0: 500Mhz \n1: 1888Mhz *\n2: 2400Mhz \n"
+    assert bench.parse_sclk(text) == 1888
+    assert bench.parse_sclk("0: 500Mhz \n1: 2400Mhz \n") is None
+    assert bench.parse_sclk("") is None
+
+
+def test_clock_sampler_without_sysfs_gives_none(monkeypatch):
+    import glob
+    monkeypatch.setattr(glob, "glob", lambda pattern: [])
+    s = bench.ClockSampler()
+    with s:
+        pass
+    assert s.median() is None
