@@ -33,8 +33,8 @@
  * failure without launching anything and without touching any output: FLA_ERR_SHAPE
  * (n_grids, then negative sizes), FLA_ERR_NULL, FLA_ERR_ALIGN, FLA_ERR_HEAD_DIM,
  * FLA_ERR_WINDOW, FLA_ERR_SHIFT, FLA_ERR_PAD_MODE, FLA_ERR_ROPE, FLA_ERR_TOO_LARGE,
- * FLA_ERR_UNSUPPORTED, FLA_ERR_WORKSPACE (or FLA_ERR_SCRATCH), FLA_ERR_ALIAS, FLA_ERR_ARCH,
- * FLA_ERR_LAUNCH.
+ * FLA_ERR_UNSUPPORTED (Cycle-scan only), FLA_ERR_WORKSPACE (or FLA_ERR_SCRATCH), FLA_ERR_ALIAS,
+ * FLA_ERR_ARCH, FLA_ERR_LAUNCH.
  * An empty problem (B, heads, Hgrid or Wgrid equal to 0) returns FLA_OK at once and
  * ignores the pointers.  Launches are asynchronous on `stream` (NULL = the null stream):
  * a fault during execution surfaces at the caller's next synchronisation, not here.  The
