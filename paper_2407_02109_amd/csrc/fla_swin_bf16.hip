@@ -35,8 +35,9 @@
 //
 // Optional prologue fusion of 2-D RoPE (Sec. 3.1): q in registers, and each K row in place in
 // LDS right after its write, are rotated by their token's grid coordinates, with the cos / sin
-// of the window's row and column positions in a per-workgroup LDS table, so a rotated copy
-// of q and k never goes through HBM.  The pad token has no position and is not rotated.
+// of the window's row and column positions in a per-workgroup LDS table (windows of at most
+// 32 x 32 tokens; wider ones evaluate them per rotated piece), so a rotated copy of q and k
+// never goes through HBM.  The pad token has no position and is not rotated.
 #include "fla_swin_device.h"
 
 namespace fla {
