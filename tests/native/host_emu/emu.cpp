@@ -26,8 +26,12 @@ hipError_t hipGetLastError() { return hipSuccess; }
 // every kernel the host build launches takes one argument struct; which one is told by the
 // caller (emu_kernel_args) before each API call
 int emu_kernel_args = 0;   // 0: SwinArgs, 1: SwinBwdArgs, 2: CycleArgs
+// nonzero: every launch fails as a real runtime's would on a bad configuration (the launch-failure
+// path of the C ABI)
+int emu_fail_launch = 0;
 
 hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, size_t, hipStream_t) {
+    if (emu_fail_launch) return hipErrorInvalidValue;
     std::barrier<> bar((std::ptrdiff_t)block.x);
     g_block_barrier = &bar;
     for (unsigned b = 0; b < grid.x; ++b) {

@@ -11,6 +11,7 @@
 #include "fla_swin.h"
 
 extern int emu_kernel_args;
+extern int emu_fail_launch;
 
 static float* alloc_random(size_t n, std::mt19937& g) {
     float* p = static_cast<float*>(std::aligned_alloc(16, ((n * 4 + 15) / 16) * 16));
@@ -65,8 +66,105 @@ static int run_cycle(int argc, char** argv) {
     return 0;
 }
 
+// Launch failure: every entry point must return FLA_ERR_LAUNCH and leave its outputs as they
+// were.  The bf16 launchers of this build always fail (the bf16 kernels are not part of it); for
+// the fp32 kernels and Cycle-scan the emulated runtime is told to fail every launch.
+static int run_launchfail() {
+    const int B = 1, heads = 2, H = 20, W = 13, k = 8, s = 3;
+    const size_t L = (size_t)H * W, rows = L + 1, tok = (size_t)heads * 64;
+    const int hw[2] = {H, W};
+    std::mt19937 g(99);
+    int bad = 0;
+    auto expect = [&](const char* what, int rc, const float* buf, const float* copy, size_t n) {
+        if (rc != FLA_ERR_LAUNCH) {
+            std::fprintf(stderr, "%s: status %d (%s), expected FLA_ERR_LAUNCH\n", what, rc, fla_status_string(rc));
+            ++bad;
+        }
+        if (std::memcmp(buf, copy, n * 4) != 0) {
+            std::fprintf(stderr, "%s: output changed\n", what);
+            ++bad;
+        }
+    };
+    for (int f32 = 0; f32 < 2; ++f32) {
+        emu_fail_launch = f32;
+        // fp32 sizes throughout: a bf16 call reads and writes half as many bytes
+        float* q = alloc_random(B * L * tok, g);
+        float* kk = alloc_random(B * rows * tok, g);
+        float* v = alloc_random(B * rows * tok, g);
+        float* dout = alloc_random(B * L * tok, g);
+        float* lse = alloc_random((size_t)B * heads * L, g);
+        float* out = alloc_random(B * L * tok, g);
+        float* dq = alloc_random(B * L * tok, g);
+        float* dk = alloc_random(B * rows * tok, g);
+        float* dv = alloc_random(B * rows * tok, g);
+        float* keep = alloc_random(B * rows * tok, g);
+        size_t nws = 0;
+        if (fla_swin_attn_bwd_workspace(B, heads, 1, hw, k, s, 1, &nws) != 0) return 1;
+        float* ws = alloc_random(nws / 4 + 1, g);
+        float* ws_copy = alloc_random(nws / 4 + 1, g);
+        std::memcpy(ws_copy, ws, nws);
+        for (int pm = 0; pm < 2; ++pm) {
+            std::memcpy(keep, out, B * L * tok * 4);
+            emu_kernel_args = 0;
+            const int rc = f32 ? fla_swin_attn_fwd_f32(q, kk, v, out, B, heads, H, W, 64, k, s, pm, nullptr)
+                               : fla_swin_attn_fwd(q, kk, v, out, B, heads, H, W, 64, k, s, pm, nullptr);
+            expect(f32 ? "forward fp32" : "forward bf16", rc, out, keep, B * L * tok);
+            std::memcpy(keep, lse, (size_t)B * heads * L * 4);
+            const int rl = f32 ? fla_swin_attn_fwd_lse_f32(q, kk, v, out, lse, B, heads, H, W, 64, k, s, pm, nullptr)
+                               : fla_swin_attn_fwd_lse(q, kk, v, out, lse, B, heads, H, W, 64, k, s, pm, nullptr);
+            expect(f32 ? "training forward fp32 (lse)" : "training forward bf16 (lse)", rl, lse, keep,
+                   (size_t)B * heads * L);
+            float* grads[3] = {dq, dk, dv};
+            const size_t sizes[3] = {B * L * tok, B * rows * tok, B * rows * tok};
+            float* copies[3];
+            for (int i = 0; i < 3; ++i) {
+                copies[i] = alloc_random(sizes[i], g);
+                std::memcpy(copies[i], grads[i], sizes[i] * 4);
+            }
+            emu_kernel_args = 1;
+            const int rb = f32 ? fla_swin_attn_bwd_f32(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W,
+                                                       64, k, s, pm, nullptr)
+                               : fla_swin_attn_bwd(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, H, W, 64,
+                                                   k, s, pm, nullptr);
+            const char* names[3] = {"backward dq", "backward dk", "backward dv"};
+            for (int i = 0; i < 3; ++i) {
+                expect(names[i], rb, grads[i], copies[i], sizes[i]);
+                std::free(copies[i]);
+            }
+            expect("backward workspace", rb, ws, ws_copy, nws / 4);
+        }
+        for (float* p : {q, kk, v, dout, lse, out, dq, dk, dv, keep, ws, ws_copy}) std::free(p);
+    }
+    // Cycle-scan (fp32 kernels of this build): the runtime fails the launch
+    emu_fail_launch = 1;
+    emu_kernel_args = 2;
+    {
+        const int Bc = 1, Lc = 40, d = 10, N = 4;
+        float* x = alloc_random((size_t)Bc * Lc * d, g);
+        float* dl = alloc_random((size_t)Bc * Lc * d, g);
+        float* A = alloc_random((size_t)d * N, g);
+        float* Bm = alloc_random((size_t)Bc * Lc * N, g);
+        float* Cm = alloc_random((size_t)Bc * Lc * N, g);
+        float* y = alloc_random((size_t)Bc * Lc * d, g);
+        float* y_copy = alloc_random((size_t)Bc * Lc * d, g);
+        std::memcpy(y_copy, y, (size_t)Bc * Lc * d * 4);
+        size_t nws = 0;
+        if (fla_cycle_scan_workspace(Bc, Lc, d, N, 3, &nws) != 0) return 1;
+        void* ws = std::aligned_alloc(16, ((nws + 15) / 16) * 16);
+        const int rc = fla_cycle_scan(x, dl, A, Bm, Cm, y, ws, nws, Bc, Lc, d, N, 3, nullptr);
+        expect("cycle scan", rc, y, y_copy, (size_t)Bc * Lc * d);
+        for (float* p : {x, dl, A, Bm, Cm, y, y_copy}) std::free(p);
+        std::free(ws);
+    }
+    emu_fail_launch = 0;
+    if (bad) return 1;
+    std::printf("ok\n");
+    return 0;
+}
+
 int main(int argc, char** argv) {
     if (argc > 1 && std::strcmp(argv[1], "cycle") == 0) return run_cycle(argc, argv);
+    if (argc > 1 && std::strcmp(argv[1], "launchfail") == 0) return run_launchfail();
     if (argc != 9) {
         std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
         return 2;

@@ -118,3 +118,12 @@ def test_cycle_scan_kernels_on_the_host(emu_binary, tmp_path, case):
     err = np.abs(y - ref).max() / max(1.0, np.abs(ref).max())
     assert err <= 1e-4, err
 
+
+
+def test_launch_failure_is_reported_and_leaves_outputs_untouched(emu_binary):
+    """FLA_ERR_LAUNCH: a launch that the runtime refuses (bf16 entry points, whose launchers this
+    build stubs out as failing, and the fp32 and Cycle-scan entry points with the emulated runtime
+    failing every launch) returns that status and leaves out, lse, dq, dk, dv, y and the workspace
+    as they were."""
+    r = subprocess.run([emu_binary, "launchfail"], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout[-2000:] + r.stderr[-4000:]
