@@ -4,7 +4,7 @@ The unmodified sources of the fp32 forward and backward kernels and of the C ABI
 geometry, workgroup decode, window rectangles, workspace layout, pad-token reduction) are
 compiled as host C++ against a small stand-in for the HIP runtime (tests/native/host_emu: a
 launch runs each block's work items as host threads with a barrier for __syncthreads), with
-AddressSanitizer and exact-size buffers.  A run must stay inside every buffer and reproduce
+AddressSanitizer, UndefinedBehaviorSanitizer (any report aborts the run) and exact-size buffers.  A run must stay inside every buffer and reproduce
 the fp64 oracle's output, log-sum-exp and gradients to fp32 accuracy.  No GPU is involved;
 the bf16 kernels (matrix-core builtins) are not part of this build."""
 import os
@@ -46,7 +46,7 @@ def emu_binary(tmp_path_factory):
     shutil.copy(os.path.join(CSRC, "fla_cycle_scan.h"), src / "fla_cycle_scan.h")
     shutil.copy(os.path.join(EMU, "fla_swin_device.h"), src / "fla_swin_device.h")
     exe = str(d / "run")
-    cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-pthread",
+    cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-pthread",
            "-I", EMU, "-I", str(src), "-I", os.path.join(ROOT, "include"),
            str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_cycle_scan.cpp"),
            str(src / "fla_swin_api.cpp"),
