@@ -173,10 +173,13 @@ def test_bf16_backward_wide_windows_multi_scale(pm):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("pm", [0, 1], ids=["mask", "kvtoken"])
-def test_multiscale_backward(dtype, pm):
-    grids = ((40, 36), (9, 9), (3, 20))
+@pytest.mark.parametrize("grids", [((40, 36), (9, 9), (3, 20)),
+                                   # the most grids one launch takes (8)
+                                   ((20, 13), (7, 9), (16, 16), (1, 1), (9, 30), (3, 3), (12, 5), (8, 8))],
+                         ids=["3grids", "8grids"])
+def test_multiscale_backward(dtype, pm, grids):
     _say("bwd ms %s %s pad_mode=%d" % (grids, dtype, pm))
-    wl = _wl(2, 2, 40, 36, 16, 8, dtype, pm, 21 + pm, grids=grids)
+    wl = _wl(2, 2, grids[0][0], grids[0][1], 16, 8, dtype, pm, 21 + pm, grids=grids)
     q, kk, v = (t.cuda() for t in synth.make_inputs(wl))
     dout = synth.make_grad(wl).cuda()
     _, lse, dq, dk, dv = _train(wl, q, kk, v, dout)

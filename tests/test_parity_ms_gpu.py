@@ -60,6 +60,8 @@ SHAPES = [  # (B, heads, grids, window, shift)
     (1, 1, [(17, 70), (3, 3), (40, 5)], 16, 8),
     (1, 2, [(9, 300), (30, 30)], 16, 15),
     (1, 1, [(24, 40), (12, 20)], 64, 0),   # windows larger than both grids: global per grid
+    # the most grids one launch takes (8): a 1x1 grid, grids smaller than the window, ragged ones
+    (1, 2, [(20, 13), (7, 9), (16, 16), (1, 1), (9, 30), (3, 3), (12, 5), (8, 8)], 8, 4),
 ]
 
 
