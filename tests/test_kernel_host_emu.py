@@ -98,6 +98,7 @@ CYCLE_CASES = [  # B, L, d, N, repeats
     (1, 65, 5, 1, 2),      # one state, three chunks, two copies
     (2, 33, 3, 16, 1),     # one copy: the plain scan
     (1, 3000, 8, 8, 4),    # chunks of 64 tokens, four copies
+    (2, 64, 1, 4, 5),      # one channel, two whole chunks, five copies
 ]
 
 

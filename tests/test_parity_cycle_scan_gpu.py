@@ -43,6 +43,7 @@ CASES = [  # B, L, d, N, repeats
     (3, 100, 130, 8, 2),    # three batch entries, three channel groups, two copies
     (1, 257, 64, 2, 1),     # one copy: the plain scan
     (1, 700, 64, 32, 4),    # four copies
+    (2, 64, 1, 4, 5),       # one channel (one live lane per wave), two whole chunks, five copies
 ]
 
 
