@@ -21,6 +21,8 @@ struct CycleArgs {
     int T;                // tokens per chunk
     int nch;              // chunks: ceil(L / T)
     int cgroups;          // groups of 64 channels: ceil(d / 64)
+    int seg;              // carry pass: segments of chunks per (batch entry, channel, state), 1 to 8
+                          // (set by launch_cycle_scan)
 };
 bool cycle_states_supported(int N);   // N in {1, 2, 4, 8, 16, 32}
 // Tokens per chunk: enough chunks to fill the chip at the sizes of an image layer, at

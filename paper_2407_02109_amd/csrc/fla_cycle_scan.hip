@@ -117,56 +117,84 @@ __global__ __launch_bounds__(64) void cycle_scan_chunks(CycleArgs c) {
 }
 
 // One thread per (batch entry, channel, state): the chunks' carries, in chunk order.
+// One workgroup holds every segment of cpw = 256 / seg (channel, state) pairs of one batch
+// entry: thread (segment s, pair j).  The chunks of a pair are split into seg consecutive
+// segments; each thread scans its segment from zero (its chunks' values come in batches of
+// kBatch loads issued before the recurrence, so one memory round trip per batch), the
+// segments' end states and Delta sums meet in LDS, every thread combines those before its own
+// (its carry in) and all of them (the state after one copy), and then runs over its segment
+// again writing E_c = r H_{c-1} + P(start -> chunk c) G.  A segment of one batch keeps its
+// values in registers for the second run.
 __global__ __launch_bounds__(256) void cycle_scan_carries(CycleArgs c) {
-    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    __shared__ float seg_h[256], seg_s[256];
+    const int S = c.seg;
+    const int cpw = 256 / S;
+    const int tid = (int)threadIdx.x;
+    const int j = tid % cpw, seg = tid / cpw;
     const long long per_b = (long long)c.d * c.N;
-    if (i >= (long long)c.B * per_b) return;
-    const int b = (int)(i / per_b);
-    const int cn = (int)(i - (long long)b * per_b);   // ch * N + n
+    const long long wg_per_b = (per_b + cpw - 1) / cpw;
+    const int b = (int)(blockIdx.x / wg_per_b);
+    const long long cn_ll = (long long)(blockIdx.x - b * wg_per_b) * cpw + j;
+    const bool live = cn_ll < per_b;
+    const int cn = live ? (int)cn_ll : (int)(per_b - 1);   // ch * N + n (past the end: a copy, not stored)
     const int ch = cn / c.N;
     const float a2 = c.A[cn] * kLog2e;
     const size_t hbase = (size_t)b * c.nch * per_b + cn;              // + chunk * d * N
     const size_t sbase = (size_t)b * c.nch * c.d + ch;                // + chunk * d
-    // the state after one copy, and the decay over it; the chunks' values come in batches of
-    // kBatch loads issued before the recurrence over them (one memory round trip per batch)
-    float H = 0.f, cum = 0.f;
-    for (int k0 = 0; k0 < c.nch; k0 += kBatch) {
-        float sv[kBatch], hv[kBatch];
+    const int cps = (c.nch + S - 1) / S;
+    const int k_begin = min(seg * cps, c.nch), k_end = min(k_begin + cps, c.nch);
+    const bool one_batch = k_end - k_begin <= kBatch;
+    float sv[kBatch], hv[kBatch];
+    auto load_batch = [&](int k0) {
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const int k = min(k0 + j, c.nch - 1);
-            sv[j] = c.ws_s[sbase + (size_t)k * c.d];
-            hv[j] = c.ws_h[hbase + (size_t)k * per_b];
+        for (int i = 0; i < kBatch; ++i) {
+            const int k = min(k0 + i, k_end - 1);
+            sv[i] = c.ws_s[sbase + (size_t)k * c.d];
+            hv[i] = c.ws_h[hbase + (size_t)k * per_b];
         }
+    };
+    // the segment from zero: its end state and the decay over it (as a sum of Delta)
+    float H = 0.f, cum = 0.f;
+    for (int k0 = k_begin; k0 < k_end; k0 += kBatch) {
+        load_batch(k0);
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j)
-            if (k0 + j < c.nch) {
-                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[j]), H, hv[j]);
-                cum += sv[j];
+        for (int i = 0; i < kBatch; ++i)
+            if (k0 + i < k_end) {
+                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[i]), H, hv[i]);
+                cum += sv[i];
             }
     }
-    const float PL = __builtin_amdgcn_exp2f(a2 * cum);
-    float g = 0.f;   // sum_{j=0}^{r-2} (r-1-j) PL^j, Horner from the top power
-    for (int j = c.repeats - 2; j >= 0; --j) g = __builtin_fmaf(g, PL, (float)(c.repeats - 1 - j));
-    const float G = g * H;
-    // E_c = r H_{c-1} + P(start -> chunk c) G, over the end states from zero
-    H = 0.f;
-    cum = 0.f;
-    const float r = (float)c.repeats;
-    for (int k0 = 0; k0 < c.nch; k0 += kBatch) {
-        float sv[kBatch], hv[kBatch];
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const int k = min(k0 + j, c.nch - 1);
-            sv[j] = c.ws_s[sbase + (size_t)k * c.d];
-            hv[j] = c.ws_h[hbase + (size_t)k * per_b];
+    seg_h[tid] = H;
+    seg_s[tid] = cum;
+    __syncthreads();
+    // the state entering this segment, and after the whole sequence (S_1) with its decay
+    float Hin = 0.f, cin = 0.f, Htot = 0.f, ctot = 0.f;
+    for (int s = 0; s < S; ++s) {
+        if (s == seg) {
+            Hin = Htot;
+            cin = ctot;
         }
+        const float cs = seg_s[s * cpw + j];
+        Htot = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cs), Htot, seg_h[s * cpw + j]);
+        ctot += cs;
+    }
+    const float PL = __builtin_amdgcn_exp2f(a2 * ctot);
+    float g = 0.f;   // sum_{i=0}^{r-2} (r-1-i) PL^i, Horner from the top power
+    for (int i = c.repeats - 2; i >= 0; --i) g = __builtin_fmaf(g, PL, (float)(c.repeats - 1 - i));
+    const float G = g * Htot;
+    // E_c = r H_{c-1} + P(start -> chunk c) G over the segment's chunks
+    H = Hin;
+    cum = cin;
+    const float r = (float)c.repeats;
+    for (int k0 = k_begin; k0 < k_end; k0 += kBatch) {
+        if (!one_batch) load_batch(k0);
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j)
-            if (k0 + j < c.nch) {
-                c.ws_h[hbase + (size_t)(k0 + j) * per_b] = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cum), G, r * H);
-                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[j]), H, hv[j]);
-                cum += sv[j];
+        for (int i = 0; i < kBatch; ++i)
+            if (k0 + i < k_end) {
+                if (live)
+                    c.ws_h[hbase + (size_t)(k0 + i) * per_b] = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * cum), G, r * H);
+                H = __builtin_fmaf(__builtin_amdgcn_exp2f(a2 * sv[i]), H, hv[i]);
+                cum += sv[i];
             }
     }
 }
@@ -227,12 +255,16 @@ __global__ __launch_bounds__(64) void cycle_scan_outputs(CycleArgs c) {
 template <int N>
 hipError_t launch_n(const CycleArgs& a, hipStream_t stream) {
     CycleArgs args = a;
+    // carry pass: up to 8 segments of at least kBatch chunks per (channel, state)
+    args.seg = 1;
+    while (args.seg < 8 && (long long)args.seg * kBatch < a.nch) args.seg *= 2;
     void* params[] = {&args};
     const long long scan_groups = (long long)a.B * a.nch * a.cgroups;
     hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&cycle_scan_chunks<N>), dim3((unsigned)scan_groups),
                                    dim3(64), params, 0, stream);
     if (e != hipSuccess) return e;
-    const long long carry_groups = ((long long)a.B * a.d * a.N + 255) / 256;
+    const long long per_wg = 256 / args.seg;
+    const long long carry_groups = (long long)a.B * (((long long)a.d * a.N + per_wg - 1) / per_wg);
     e = hipLaunchKernel(reinterpret_cast<const void*>(&cycle_scan_carries), dim3((unsigned)carry_groups), dim3(256),
                         params, 0, stream);
     if (e != hipSuccess) return e;

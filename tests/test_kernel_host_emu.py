@@ -99,6 +99,10 @@ CYCLE_CASES = [  # B, L, d, N, repeats
     (2, 33, 3, 16, 1),     # one copy: the plain scan
     (1, 3000, 8, 8, 4),    # chunks of 64 tokens, four copies
     (2, 64, 1, 4, 5),      # one channel, two whole chunks, five copies
+    # the carry pass in 2, 4 and 8 segments of chunks (36, 100 and 157 chunks of 256 tokens)
+    (1, 9000, 3, 4, 2),
+    (1, 25600, 1, 1, 3),
+    (2, 40000, 1, 2, 3),
 ]
 
 

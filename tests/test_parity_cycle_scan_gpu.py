@@ -44,6 +44,7 @@ CASES = [  # B, L, d, N, repeats
     (1, 257, 64, 2, 1),     # one copy: the plain scan
     (1, 700, 64, 32, 4),    # four copies
     (2, 64, 1, 4, 5),       # one channel (one live lane per wave), two whole chunks, five copies
+    (1, 25600, 40, 4, 3),   # 100 chunks of 256 tokens: the carry pass in four segments
 ]
 
 
