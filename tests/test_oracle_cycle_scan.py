@@ -191,7 +191,8 @@ def test_mutant_is_caught(name, monkeypatch):
     failed = []
     for pin in PINS:
         try:
-            pin(C)
+            with np.errstate(over="ignore", invalid="ignore"):   # a wrong decay sign overflows
+                pin(C)
         except AssertionError:
             failed.append(pin.__name__)
     assert failed, "mutant %s passed every pin" % name
