@@ -450,6 +450,7 @@ void swin_fwd_bf16_kernel(SwinArgs a) {
                 for (int u = 0; u < 4; ++u) r4[u] = (__bf16)(o[db][4 * rg + u] * inv);
                 *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * rg + 4 * h) = r4;
             }
+        asm volatile("" ::: "memory");   // staged rows are read back by other lanes of the wave
         const int part = lane & (TPR - 1);
         constexpr int rows = 64 / TPR;   // rows per store instruction
         for (int i = 0; i < QW / rows; ++i) {

@@ -1,7 +1,9 @@
-// The launch emulation behind hip_runtime.h (see there), a device that reports gfx950, and
-// stand-ins for the bf16 launchers (which the host build does not contain; it builds the fp32
-// attention kernels and the Cycle-scan kernels).
+// The launch emulation behind hip_runtime.h (see there), with the wave-level exchange that the
+// matrix-core and cross-lane builtins of amdgcn_host.h use; a device that reports gfx950; and
+// stand-ins for the bf16 backward launchers (which the host build does not contain: it builds
+// the bf16 forward, the fp32 attention kernels and the Cycle-scan kernels).
 #include <barrier>
+#include <memory>
 #include <thread>
 #include <vector>
 
@@ -11,6 +13,14 @@
 thread_local emu_index threadIdx, blockIdx;
 static std::barrier<>* g_block_barrier = nullptr;
 void __syncthreads() { g_block_barrier->arrive_and_wait(); }
+
+// waves of 64 work items: a barrier over each wave's lanes and 4 KB of exchange slots per wave
+constexpr unsigned kEmuMaxWaves = 8;
+static std::vector<std::unique_ptr<std::barrier<>>> g_wave_barriers;
+alignas(64) static unsigned char g_wave_slots[kEmuMaxWaves][4096];
+unsigned emu_lane_id() { return threadIdx.x & 63u; }
+void emu_wave_barrier() { g_wave_barriers[threadIdx.x >> 6]->arrive_and_wait(); }
+unsigned char* emu_wave_slots() { return g_wave_slots[threadIdx.x >> 6]; }
 
 hipError_t hipGetDevice(int* device) {
     *device = 0;
@@ -32,8 +42,13 @@ int emu_fail_launch = 0;
 
 hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, size_t, hipStream_t) {
     if (emu_fail_launch) return hipErrorInvalidValue;
+    const unsigned nw = (block.x + 63) / 64;
+    if (nw > kEmuMaxWaves) return hipErrorInvalidValue;
     std::barrier<> bar((std::ptrdiff_t)block.x);
     g_block_barrier = &bar;
+    g_wave_barriers.clear();
+    for (unsigned w = 0; w < nw; ++w)
+        g_wave_barriers.emplace_back(std::make_unique<std::barrier<>>((std::ptrdiff_t)std::min(64u, block.x - 64 * w)));
     for (unsigned b = 0; b < grid.x; ++b) {
         std::vector<std::thread> threads;
         threads.reserve(block.x);
@@ -53,11 +68,11 @@ hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, s
         for (auto& th : threads) th.join();
     }
     g_block_barrier = nullptr;
+    g_wave_barriers.clear();
     return hipSuccess;
 }
 
 namespace fla {
-hipError_t launch_swin_fwd_bf16(const SwinArgs&, hipStream_t) { return 1; }
 hipError_t launch_swin_bwd_bf16_window(const SwinBwdArgs&, hipStream_t) { return 1; }
 hipError_t launch_swin_bwd_bf16_blocks(const SwinBwdArgs&, hipStream_t) { return 1; }
 hipError_t scratch_address(void**) { return 1; }

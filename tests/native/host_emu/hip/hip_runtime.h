@@ -36,6 +36,12 @@ struct alignas(8) float2 {
     float x, y;
 };
 inline float2 make_float2(float a, float b) { return float2{a, b}; }
+struct alignas(16) uint4 {
+    unsigned x, y, z, w;
+};
+struct alignas(8) uint2 {
+    unsigned x, y;
+};
 
 typedef int hipError_t;
 constexpr hipError_t hipSuccess = 0;

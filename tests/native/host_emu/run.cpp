@@ -66,9 +66,77 @@ static int run_cycle(int argc, char** argv) {
     return 0;
 }
 
+static void dump_u16(const char* dir, const char* name, const uint16_t* p, size_t n) {
+    char path[1024];
+    std::snprintf(path, sizeof path, "%s/%s.bf16", dir, name);
+    FILE* f = std::fopen(path, "wb");
+    std::fwrite(p, 2, n, f);
+    std::fclose(f);
+}
+
+static uint16_t* alloc_bf16(size_t n, std::mt19937& g, bool random) {
+    uint16_t* p = static_cast<uint16_t*>(std::aligned_alloc(16, ((n * 2 + 15) / 16) * 16));
+    std::normal_distribution<float> d(0.f, 1.f);
+    for (size_t i = 0; i < n; ++i) {
+        const __bf16 x = random ? (__bf16)d(g) : (__bf16)NAN;
+        std::memcpy(p + i, &x, 2);
+    }
+    return p;
+}
+
+// The bf16 forward through the C ABI (its matrix-core kernel on the wave-level emulation):
+//   run bf16 KIND B heads GRIDS window shift pad_mode head_dim theta scale outdir
+// KIND plain, rope or ms; GRIDS "HxW", or "HxW,HxW,..." for ms.  Writes q, k, v, out (.bf16).
+static int run_bf16(int argc, char** argv) {
+    if (argc != 13) {
+        std::fprintf(stderr, "usage: run bf16 KIND B heads GRIDS window shift pad_mode head_dim theta scale outdir\n");
+        return 2;
+    }
+    const char* kind = argv[2];
+    const int B = std::atoi(argv[3]), heads = std::atoi(argv[4]);
+    int hw[16], ng = 0;
+    for (const char* p = argv[5]; *p && ng < 8;) {
+        char* e;
+        hw[2 * ng] = (int)std::strtol(p, &e, 10);
+        hw[2 * ng + 1] = (int)std::strtol(e + 1, &e, 10);
+        ++ng;
+        p = *e ? e + 1 : e;
+    }
+    const int k = std::atoi(argv[6]), s = std::atoi(argv[7]), pm = std::atoi(argv[8]), hd = std::atoi(argv[9]);
+    const float theta = (float)std::atof(argv[10]), scale = (float)std::atof(argv[11]);
+    const char* dir = argv[12];
+    size_t L = 0;
+    for (int i = 0; i < ng; ++i) L += (size_t)hw[2 * i] * hw[2 * i + 1];
+    const size_t rows = L + (pm ? 1 : 0), tok = (size_t)heads * hd;
+    std::mt19937 g(4321);
+    uint16_t* q = alloc_bf16(B * L * tok, g, true);
+    uint16_t* kk = alloc_bf16(B * rows * tok, g, true);
+    uint16_t* v = alloc_bf16(B * rows * tok, g, true);
+    uint16_t* out = alloc_bf16(B * L * tok, g, false);
+    emu_kernel_args = 0;
+    int rc;
+    if (std::strcmp(kind, "plain") == 0)
+        rc = fla_swin_attn_fwd(q, kk, v, out, B, heads, hw[0], hw[1], hd, k, s, pm, nullptr);
+    else if (std::strcmp(kind, "rope") == 0)
+        rc = fla_swin_attn_rope_fwd(q, kk, v, out, B, heads, hw[0], hw[1], hd, k, s, pm, theta, scale, nullptr);
+    else
+        rc = fla_swin_attn_ms_fwd(q, kk, v, out, B, heads, ng, hw, hd, k, s, pm, nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "bf16 forward: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    dump_u16(dir, "q", q, B * L * tok);
+    dump_u16(dir, "k", kk, B * rows * tok);
+    dump_u16(dir, "v", v, B * rows * tok);
+    dump_u16(dir, "out", out, B * L * tok);
+    for (uint16_t* p : {q, kk, v, out}) std::free(p);
+    std::printf("ok\n");
+    return 0;
+}
+
 // Launch failure: every entry point must return FLA_ERR_LAUNCH and leave its outputs as they
-// were.  The bf16 launchers of this build always fail (the bf16 kernels are not part of it); for
-// the fp32 kernels and Cycle-scan the emulated runtime is told to fail every launch.
+// were: the emulated runtime is told to fail every launch (the bf16 backward launchers of this
+// build, which does not contain those kernels, fail anyway).
 static int run_launchfail() {
     const int B = 1, heads = 2, H = 20, W = 13, k = 8, s = 3;
     const size_t L = (size_t)H * W, rows = L + 1, tok = (size_t)heads * 64;
@@ -86,7 +154,7 @@ static int run_launchfail() {
         }
     };
     for (int f32 = 0; f32 < 2; ++f32) {
-        emu_fail_launch = f32;
+        emu_fail_launch = 1;
         // fp32 sizes throughout: a bf16 call reads and writes half as many bytes
         float* q = alloc_random(B * L * tok, g);
         float* kk = alloc_random(B * rows * tok, g);
@@ -165,6 +233,7 @@ static int run_launchfail() {
 int main(int argc, char** argv) {
     if (argc > 1 && std::strcmp(argv[1], "cycle") == 0) return run_cycle(argc, argv);
     if (argc > 1 && std::strcmp(argv[1], "launchfail") == 0) return run_launchfail();
+    if (argc > 1 && std::strcmp(argv[1], "bf16") == 0) return run_bf16(argc, argv);
     if (argc != 9) {
         std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
         return 2;

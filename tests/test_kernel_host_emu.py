@@ -1,12 +1,16 @@
-"""The fp32 kernels and the C ABI, built for the CPU and run against the oracle.
+"""The kernels and the C ABI, built for the CPU and run against the oracle.
 
-The unmodified sources of the fp32 forward and backward kernels and of the C ABI (launch
-geometry, workgroup decode, window rectangles, workspace layout, pad-token reduction) are
-compiled as host C++ against a small stand-in for the HIP runtime (tests/native/host_emu: a
-launch runs each block's work items as host threads with a barrier for __syncthreads), with
-AddressSanitizer, UndefinedBehaviorSanitizer (any report aborts the run) and exact-size buffers.  A run must stay inside every buffer and reproduce
-the fp64 oracle's output, log-sum-exp and gradients to fp32 accuracy.  No GPU is involved;
-the bf16 kernels (matrix-core builtins) are not part of this build."""
+The sources of the fp32 forward and backward kernels, the bf16 forward kernel, the Cycle-scan
+kernels, the device header and the C ABI (launch geometry, workgroup decode, window rectangles,
+workspace layout, pad-token reduction) are compiled as host C++ against a small stand-in for
+the HIP runtime (tests/native/host_emu: a launch runs each block's work items as host threads
+with a barrier for __syncthreads; amdgcn_host.h gives the gfx950 builtins host definitions, the
+matrix-core product, the half-wave swap and the ballot exchanging their operands between the
+64 lanes of a wave), with AddressSanitizer, UndefinedBehaviorSanitizer (any report aborts the
+run) and exact-size buffers.  A run must stay inside every buffer and reproduce the fp64
+oracle's output, log-sum-exp and gradients (fp32: to fp32 accuracy; bf16: at the GPU tests'
+bounds).  No GPU is involved; the bf16 backward kernels (transposing LDS reads, loads that
+write LDS) are not part of this build."""
 import os
 import shutil
 import subprocess
@@ -36,19 +40,27 @@ def emu_binary(tmp_path_factory):
     d = tmp_path_factory.mktemp("host_emu")
     src = d / "src"
     src.mkdir()
-    # sources as they are; the stub device header sits next to them so that their quoted
-    # include finds it first
+    # sources as they are (the gfx950 builtins they use come from amdgcn_host.h, force-included)
     shutil.copy(os.path.join(CSRC, "fla_swin_bwd_f32.hip"), src / "fla_swin_bwd_f32.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_f32.hip"), src / "fla_swin_f32.cpp")
     shutil.copy(os.path.join(CSRC, "fla_cycle_scan.hip"), src / "fla_cycle_scan.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_api.cpp"), src / "fla_swin_api.cpp")
     shutil.copy(os.path.join(CSRC, "fla_swin_internal.h"), src / "fla_swin_internal.h")
     shutil.copy(os.path.join(CSRC, "fla_cycle_scan.h"), src / "fla_cycle_scan.h")
-    shutil.copy(os.path.join(EMU, "fla_swin_device.h"), src / "fla_swin_device.h")
+    shutil.copy(os.path.join(CSRC, "fla_swin_device.h"), src / "fla_swin_device.h")
+    # the bf16 forward as it is, except that its one intra-wave hand-off point (a compiler fence
+    # on the hardware, where the 64 lanes of a wave run in lockstep) becomes a barrier over the
+    # wave's lanes, which here run as separate threads
+    fwd = open(os.path.join(CSRC, "fla_swin_bf16.hip")).read()
+    fence = 'asm volatile("" ::: "memory");'
+    assert fwd.count(fence) == 1
+    (src / "fla_swin_bf16.cpp").write_text(fwd.replace(fence, "emu_wave_barrier();"))
     exe = str(d / "run")
     cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-pthread",
+           "-include", os.path.join(EMU, "amdgcn_host.h"),
            "-I", EMU, "-I", str(src), "-I", os.path.join(ROOT, "include"),
            str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_cycle_scan.cpp"),
+           str(src / "fla_swin_bf16.cpp"),
            str(src / "fla_swin_api.cpp"),
            os.path.join(EMU, "emu.cpp"), os.path.join(EMU, "run.cpp"), "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
@@ -132,3 +144,49 @@ def test_launch_failure_is_reported_and_leaves_outputs_untouched(emu_binary):
     as they were."""
     r = subprocess.run([emu_binary, "launchfail"], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout[-2000:] + r.stderr[-4000:]
+
+
+BF16_CASES = [  # kind, B, heads, grids, window, shift, pad_mode, head_dim, rope theta, rope scale
+    ("plain", 1, 2, "20x13", 8, 3, 0, 64, 0, 0),
+    ("plain", 1, 2, "20x13", 8, 3, 1, 64, 0, 0),     # KV-token mode: the pad token as key n
+    ("plain", 2, 1, "9x40", 16, 15, 1, 64, 0, 0),    # windows of a few rows, two batch entries
+    ("plain", 1, 1, "24x40", 32, 16, 0, 64, 0, 0),   # windows of up to 1024 tokens: query blocks, key chunks
+    ("plain", 1, 2, "17x11", 8, 4, 1, 32, 0, 0),     # head_dim 32
+    ("plain", 1, 1, "17x11", 8, 4, 0, 128, 0, 0),    # head_dim 128
+    ("rope", 1, 2, "20x13", 8, 3, 1, 64, 100.0, 0.5),      # the per-window cos / sin table
+    ("rope", 1, 1, "40x24", 40, 0, 0, 64, 10000.0, 1.0),   # a window wider than the table: per piece
+    ("ms", 1, 2, "20x13,7x9", 8, 4, 1, 64, 0, 0),
+    ("ms", 1, 1, "20x13,7x9,16x16,1x1,9x30,3x3,12x5,8x8", 8, 4, 1, 64, 0, 0),   # the most grids a launch takes
+]
+
+
+@pytest.mark.parametrize("case", BF16_CASES, ids=lambda c: "%s-%s-%d-%d-%d-d%d" % (c[0], c[3].replace(",", "+"), c[4],
+                                                                                  c[5], c[6], c[7]))
+def test_bf16_forward_on_the_host(emu_binary, tmp_path, case):
+    """The bf16 forward kernel (its source, with the matrix-core products, the half-wave swap
+    and the ballot emulated per wave) and the device header, built for the host with
+    AddressSanitizer and UndefinedBehaviorSanitizer on exact-size buffers, against the fp64
+    oracle at the GPU tests' bf16 bounds (max 2e-2, mean 2e-3)."""
+    kind, B, heads, grids, k, s, pm, d, theta, scale = case
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
+    r = subprocess.run([emu_binary, "bf16", kind, str(B), str(heads), grids, str(k), str(s), str(pm), str(d),
+                        str(theta), str(scale), str(tmp_path)], capture_output=True, text=True, timeout=900, env=env)
+    assert r.returncode == 0 and "ok" in r.stdout, r.stderr[-4000:]
+    glist = [tuple(int(x) for x in g.split("x")) for g in grids.split(",")]
+    L = sum(h * w for h, w in glist)
+    rows = L + (1 if pm else 0)
+
+    def ld(name, r_):
+        u = np.fromfile(str(tmp_path / (name + ".bf16")), dtype=np.uint16).astype(np.uint32) << 16
+        return u.view(np.float32).astype(np.float64).reshape(B, r_, heads, d)
+
+    q, kk, v, out = ld("q", L), ld("k", rows), ld("v", rows), ld("out", L)
+    assert np.isfinite(out).all(), "unwritten output rows"
+    if kind == "plain":
+        ref = O.swin_attention_textbook(q, kk, v, glist[0][0], glist[0][1], k, s, pm)
+    elif kind == "rope":
+        ref = O.swin_attention_rope(q, kk, v, glist[0][0], glist[0][1], k, s, pm, theta, scale)
+    else:
+        ref = O.swin_attention_ms(q, kk, v, glist, k, s, pm)
+    err = np.abs(out - ref)
+    assert err.max() <= 2e-2 and err.mean() <= 2e-3, (err.max(), err.mean())
