@@ -141,3 +141,61 @@ inline unsigned long long __builtin_amdgcn_ballot_w64(bool p) {
     emu_wave_barrier();
     return m;
 }
+
+// ---- used by the bf16 backward kernels
+
+typedef short emu_shortx4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read: lane i of each 16-lane group names a 4-element piece (row i / 4,
+// elements 4 (i % 4) .. + 3) of a 4 x 16 block of 16-bit elements and receives the block's
+// column i.
+inline emu_shortx4 __builtin_amdgcn_ds_read_tr16_b64_v4i16(__attribute__((address_space(3))) emu_shortx4* p) {
+    emu_shortx4* s = reinterpret_cast<emu_shortx4*>(emu_wave_slots());
+    const unsigned l = emu_lane_id();
+    emu_shortx4 mine;
+    std::memcpy(&mine, (const void*)(uintptr_t)p, 8);
+    s[l] = mine;
+    emu_wave_barrier();
+    const unsigned g = l & ~15u, i = l & 15u;
+    emu_shortx4 r;
+    for (int row = 0; row < 4; ++row) r[row] = s[g + 4 * row + i / 4][i % 4];
+    emu_wave_barrier();
+    return r;
+}
+
+// A buffer load that writes LDS: lane l's `size` bytes go to the LDS address base + l * size
+// (zeros outside the buffer's range), here at once.  The wave's wait for its loads is where the
+// rows its lanes wrote become visible to the whole wave: a barrier over the wave's lanes.
+inline void __builtin_amdgcn_raw_ptr_buffer_load_lds(__amdgpu_buffer_rsrc_t r, __attribute__((address_space(3))) void* lds,
+                                                    unsigned size, unsigned voff, unsigned soff, unsigned off,
+                                                    unsigned) {
+    unsigned char* dst = (unsigned char*)(uintptr_t)lds + (size_t)emu_lane_id() * size;
+    const unsigned long long o = (unsigned long long)voff + soff + off;
+    for (unsigned d = 0; d < size; d += 4) {
+        unsigned w = 0;
+        if (o + d + 4 <= r.bytes) std::memcpy(&w, r.base + o + d, 4);
+        std::memcpy(dst + d, &w, 4);
+    }
+}
+inline void __builtin_amdgcn_s_waitcnt(int) { emu_wave_barrier(); }
+
+inline int __builtin_amdgcn_readfirstlane(int x) {
+    int* s = reinterpret_cast<int*>(emu_wave_slots());
+    s[emu_lane_id()] = x;
+    emu_wave_barrier();
+    const int r = s[0];
+    emu_wave_barrier();
+    return r;
+}
+
+template <typename T>
+inline T __shfl_xor(T x, int mask, int = 64) {
+    static_assert(sizeof(T) == 4, "32-bit shuffles");
+    T* s = reinterpret_cast<T*>(emu_wave_slots());
+    const unsigned l = emu_lane_id();
+    s[l] = x;
+    emu_wave_barrier();
+    const T r = s[(l ^ (unsigned)mask) & 63u];
+    emu_wave_barrier();
+    return r;
+}

@@ -1,7 +1,5 @@
 // The launch emulation behind hip_runtime.h (see there), with the wave-level exchange that the
-// matrix-core and cross-lane builtins of amdgcn_host.h use; a device that reports gfx950; and
-// stand-ins for the bf16 backward launchers (which the host build does not contain: it builds
-// the bf16 forward, the fp32 attention kernels and the Cycle-scan kernels).
+// matrix-core and cross-lane builtins of amdgcn_host.h use, and a device that reports gfx950.
 #include <barrier>
 #include <memory>
 #include <thread>
@@ -15,7 +13,7 @@ static std::barrier<>* g_block_barrier = nullptr;
 void __syncthreads() { g_block_barrier->arrive_and_wait(); }
 
 // waves of 64 work items: a barrier over each wave's lanes and 4 KB of exchange slots per wave
-constexpr unsigned kEmuMaxWaves = 8;
+constexpr unsigned kEmuMaxWaves = 16;   // workgroups of up to 1024 work items
 static std::vector<std::unique_ptr<std::barrier<>>> g_wave_barriers;
 alignas(64) static unsigned char g_wave_slots[kEmuMaxWaves][4096];
 unsigned emu_lane_id() { return threadIdx.x & 63u; }
@@ -73,7 +71,6 @@ hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, s
 }
 
 namespace fla {
-hipError_t launch_swin_bwd_bf16_window(const SwinBwdArgs&, hipStream_t) { return 1; }
-hipError_t launch_swin_bwd_bf16_blocks(const SwinBwdArgs&, hipStream_t) { return 1; }
+// the static scratch of the allocation-free backward has no host counterpart
 hipError_t scratch_address(void**) { return 1; }
 }  // namespace fla

@@ -134,6 +134,82 @@ static int run_bf16(int argc, char** argv) {
     return 0;
 }
 
+// bf16 training (forward keeping the log-sum-exp, then the backward) through the C ABI:
+//   run bf16train KIND B heads GRIDS window shift pad_mode theta scale outdir
+// KIND plain, rope or ms; GRIDS as for bf16.  Writes q, k, v, dout, out, dq, dk, dv (.bf16) and
+// lse (.f32).
+static int run_bf16_train(int argc, char** argv) {
+    if (argc != 12) {
+        std::fprintf(stderr, "usage: run bf16train KIND B heads GRIDS window shift pad_mode theta scale outdir\n");
+        return 2;
+    }
+    const char* kind = argv[2];
+    const int B = std::atoi(argv[3]), heads = std::atoi(argv[4]);
+    int hw[16], ng = 0;
+    for (const char* p = argv[5]; *p && ng < 8;) {
+        char* e;
+        hw[2 * ng] = (int)std::strtol(p, &e, 10);
+        hw[2 * ng + 1] = (int)std::strtol(e + 1, &e, 10);
+        ++ng;
+        p = *e ? e + 1 : e;
+    }
+    const int k = std::atoi(argv[6]), s = std::atoi(argv[7]), pm = std::atoi(argv[8]);
+    const float theta = (float)std::atof(argv[9]), scale = (float)std::atof(argv[10]);
+    const char* dir = argv[11];
+    const int hd = 64;
+    size_t L = 0;
+    for (int i = 0; i < ng; ++i) L += (size_t)hw[2 * i] * hw[2 * i + 1];
+    const size_t rows = L + (pm ? 1 : 0), tok = (size_t)heads * hd;
+    std::mt19937 g(8765);
+    uint16_t* q = alloc_bf16(B * L * tok, g, true);
+    uint16_t* kk = alloc_bf16(B * rows * tok, g, true);
+    uint16_t* v = alloc_bf16(B * rows * tok, g, true);
+    uint16_t* dout = alloc_bf16(B * L * tok, g, true);
+    uint16_t* out = alloc_bf16(B * L * tok, g, false);
+    uint16_t* dq = alloc_bf16(B * L * tok, g, false);
+    uint16_t* dk = alloc_bf16(B * rows * tok, g, false);
+    uint16_t* dv = alloc_bf16(B * rows * tok, g, false);
+    float* lse = static_cast<float*>(std::aligned_alloc(16, (((size_t)B * heads * L * 4 + 15) / 16) * 16));
+    size_t nws = 0;
+    if (fla_swin_attn_bwd_workspace(B, heads, ng, hw, k, s, pm, &nws) != 0) return 1;
+    void* ws = nws ? std::aligned_alloc(16, ((nws + 15) / 16) * 16) : nullptr;
+    const bool rope = std::strcmp(kind, "rope") == 0, ms = std::strcmp(kind, "ms") == 0;
+    emu_kernel_args = 0;
+    int rc = rope ? fla_swin_attn_rope_fwd_lse(q, kk, v, out, lse, B, heads, hw[0], hw[1], hd, k, s, pm, theta, scale,
+                                               nullptr)
+             : ms ? fla_swin_attn_ms_fwd_lse(q, kk, v, out, lse, B, heads, ng, hw, hd, k, s, pm, nullptr)
+                  : fla_swin_attn_fwd_lse(q, kk, v, out, lse, B, heads, hw[0], hw[1], hd, k, s, pm, nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "bf16 training forward: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    emu_kernel_args = 1;
+    rc = rope ? fla_swin_attn_rope_bwd(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, hw[0], hw[1], hd, k, s,
+                                       pm, theta, scale, nullptr)
+         : ms ? fla_swin_attn_ms_bwd(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, ng, hw, hd, k, s, pm,
+                                     nullptr)
+              : fla_swin_attn_bwd(q, kk, v, out, dout, lse, dq, dk, dv, ws, nws, B, heads, hw[0], hw[1], hd, k, s, pm,
+                                  nullptr);
+    if (rc != 0) {
+        std::fprintf(stderr, "bf16 backward: %s\n", fla_status_string(rc));
+        return 1;
+    }
+    dump_u16(dir, "q", q, B * L * tok);
+    dump_u16(dir, "k", kk, B * rows * tok);
+    dump_u16(dir, "v", v, B * rows * tok);
+    dump_u16(dir, "dout", dout, B * L * tok);
+    dump_u16(dir, "out", out, B * L * tok);
+    dump_u16(dir, "dq", dq, B * L * tok);
+    dump_u16(dir, "dk", dk, B * rows * tok);
+    dump_u16(dir, "dv", dv, B * rows * tok);
+    dump(dir, "lse", lse, (size_t)B * heads * L);
+    for (uint16_t* p : {q, kk, v, dout, out, dq, dk, dv}) std::free(p);
+    std::free(lse);
+    std::free(ws);
+    std::printf("ok\n");
+    return 0;
+}
+
 // Launch failure: every entry point must return FLA_ERR_LAUNCH and leave its outputs as they
 // were: the emulated runtime is told to fail every launch (the bf16 backward launchers of this
 // build, which does not contain those kernels, fail anyway).
@@ -234,6 +310,7 @@ int main(int argc, char** argv) {
     if (argc > 1 && std::strcmp(argv[1], "cycle") == 0) return run_cycle(argc, argv);
     if (argc > 1 && std::strcmp(argv[1], "launchfail") == 0) return run_launchfail();
     if (argc > 1 && std::strcmp(argv[1], "bf16") == 0) return run_bf16(argc, argv);
+    if (argc > 1 && std::strcmp(argv[1], "bf16train") == 0) return run_bf16_train(argc, argv);
     if (argc != 9) {
         std::fprintf(stderr, "usage: run B heads H W window shift pad_mode outdir\n");
         return 2;

@@ -1,16 +1,14 @@
 """The kernels and the C ABI, built for the CPU and run against the oracle.
 
-The sources of the fp32 forward and backward kernels, the bf16 forward kernel, the Cycle-scan
-kernels, the device header and the C ABI (launch geometry, workgroup decode, window rectangles,
+The sources of the fp32 and bf16 forward and backward kernels, the Cycle-scan kernels, the device header and the C ABI (launch geometry, workgroup decode, window rectangles,
 workspace layout, pad-token reduction) are compiled as host C++ against a small stand-in for
 the HIP runtime (tests/native/host_emu: a launch runs each block's work items as host threads
 with a barrier for __syncthreads; amdgcn_host.h gives the gfx950 builtins host definitions, the
-matrix-core product, the half-wave swap and the ballot exchanging their operands between the
-64 lanes of a wave), with AddressSanitizer, UndefinedBehaviorSanitizer (any report aborts the
+matrix-core product, the transposing LDS read, the half-wave swap, the shuffles and the ballot
+exchanging their operands between the 64 lanes of a wave), with AddressSanitizer, UndefinedBehaviorSanitizer (any report aborts the
 run) and exact-size buffers.  A run must stay inside every buffer and reproduce the fp64
 oracle's output, log-sum-exp and gradients (fp32: to fp32 accuracy; bf16: at the GPU tests'
-bounds).  No GPU is involved; the bf16 backward kernels (transposing LDS reads, loads that
-write LDS) are not part of this build."""
+bounds).  No GPU is involved."""
 import os
 import shutil
 import subprocess
@@ -48,19 +46,21 @@ def emu_binary(tmp_path_factory):
     shutil.copy(os.path.join(CSRC, "fla_swin_internal.h"), src / "fla_swin_internal.h")
     shutil.copy(os.path.join(CSRC, "fla_cycle_scan.h"), src / "fla_cycle_scan.h")
     shutil.copy(os.path.join(CSRC, "fla_swin_device.h"), src / "fla_swin_device.h")
-    # the bf16 forward as it is, except that its one intra-wave hand-off point (a compiler fence
-    # on the hardware, where the 64 lanes of a wave run in lockstep) becomes a barrier over the
-    # wave's lanes, which here run as separate threads
-    fwd = open(os.path.join(CSRC, "fla_swin_bf16.hip")).read()
+    # the bf16 kernels as they are, except that their intra-wave hand-off points (compiler
+    # fences on the hardware, where the 64 lanes of a wave run in lockstep) become barriers over
+    # the wave's lanes, which here run as separate threads
     fence = 'asm volatile("" ::: "memory");'
-    assert fwd.count(fence) == 1
-    (src / "fla_swin_bf16.cpp").write_text(fwd.replace(fence, "emu_wave_barrier();"))
+    for name, fences in (("fla_swin_bf16", 1), ("fla_swin_bwd_bf16_window", 1), ("fla_swin_bwd_bf16_blocks", 3)):
+        text = open(os.path.join(CSRC, name + ".hip")).read()
+        assert text.count(fence) == fences, name
+        (src / (name + ".cpp")).write_text(text.replace(fence, "emu_wave_barrier();"))
     exe = str(d / "run")
     cmd = [cxx, "-std=c++20", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-pthread",
            "-include", os.path.join(EMU, "amdgcn_host.h"),
            "-I", EMU, "-I", str(src), "-I", os.path.join(ROOT, "include"),
            str(src / "fla_swin_bwd_f32.cpp"), str(src / "fla_swin_f32.cpp"), str(src / "fla_cycle_scan.cpp"),
-           str(src / "fla_swin_bf16.cpp"),
+           str(src / "fla_swin_bf16.cpp"), str(src / "fla_swin_bwd_bf16_window.cpp"),
+           str(src / "fla_swin_bwd_bf16_blocks.cpp"),
            str(src / "fla_swin_api.cpp"),
            os.path.join(EMU, "emu.cpp"), os.path.join(EMU, "run.cpp"), "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
@@ -114,7 +114,7 @@ CYCLE_CASES = [  # B, L, d, N, repeats
     # the carry pass in 2, 4 and 8 segments of chunks (36, 100 and 157 chunks of 256 tokens)
     (1, 9000, 3, 4, 2),
     (1, 25600, 1, 1, 3),
-    (2, 40000, 1, 2, 3),
+    (1, 40000, 1, 2, 3),
 ]
 
 
@@ -190,3 +190,62 @@ def test_bf16_forward_on_the_host(emu_binary, tmp_path, case):
         ref = O.swin_attention_ms(q, kk, v, glist, k, s, pm)
     err = np.abs(out - ref)
     assert err.max() <= 2e-2 and err.mean() <= 2e-3, (err.max(), err.mean())
+
+
+BF16_TRAIN_CASES = [  # kind, B, heads, grids, window, shift, pad_mode, rope theta, rope scale
+    ("plain", 1, 1, "13x11", 8, 3, 0, 0, 0),      # one-window kernel
+    ("plain", 2, 1, "13x11", 8, 3, 1, 0, 0),      # one-window kernel, pad token, its gradient's reduction
+    ("plain", 1, 1, "24x20", 20, 10, 0, 0, 0),    # windows of up to 400 tokens: key- and query-role blocks
+    ("plain", 1, 1, "24x20", 20, 10, 1, 0, 0),    # the same with the pad token
+    ("rope", 1, 1, "13x11", 8, 3, 1, 100.0, 0.5),
+    ("rope", 1, 1, "24x20", 20, 10, 1, 100.0, 0.5),   # the block kernel's RoPE + pad instance (spills to scratch)
+    ("rope", 1, 1, "33x12", 33, 0, 0, 10000.0, 1.0),  # a window taller than the forward's cos / sin table
+    ("ms", 1, 1, "20x13,7x9,3x20", 8, 4, 1, 0, 0),
+]
+
+
+@pytest.mark.parametrize("case", BF16_TRAIN_CASES, ids=lambda c: "%s-%s-%d-%d-%d" % (c[0], c[3].replace(",", "+"),
+                                                                                     c[4], c[5], c[6]))
+def test_bf16_training_on_the_host(emu_binary, tmp_path, case):
+    """The bf16 training forward and backward (one-window and block kernels, the pad-gradient
+    reduction) on the host emulation with AddressSanitizer and UndefinedBehaviorSanitizer,
+    against the fp64 oracle's gradients at the GPU tests' bounds (max 2e-2, mean 2e-3 of the
+    largest reference gradient) and its log-sum-exp."""
+    kind, B, heads, grids, k, s, pm, theta, scale = case
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
+    r = subprocess.run([emu_binary, "bf16train", kind, str(B), str(heads), grids, str(k), str(s), str(pm),
+                        str(theta), str(scale), str(tmp_path)], capture_output=True, text=True, timeout=1200, env=env)
+    assert r.returncode == 0 and "ok" in r.stdout, r.stderr[-4000:]
+    glist = [tuple(int(x) for x in g.split("x")) for g in grids.split(",")]
+    L = sum(h * w for h, w in glist)
+    rows = L + (1 if pm else 0)
+
+    def ld(name, r_):
+        u = np.fromfile(str(tmp_path / (name + ".bf16")), dtype=np.uint16).astype(np.uint32) << 16
+        return u.view(np.float32).astype(np.float64).reshape(B, r_, heads, 64)
+
+    q, kk, v, dout = ld("q", L), ld("k", rows), ld("v", rows), ld("dout", L)
+    lse = np.fromfile(str(tmp_path / "lse.f32"), dtype=np.float32).astype(np.float64).reshape(B, heads, L)
+    H, W = glist[0]
+    if kind == "plain":
+        refs = O.swin_attention_bwd(q, kk, v, dout, H, W, k, s, pm)
+        ref_lse = O.swin_attention_lse(q, kk, v, H, W, k, s, pm)
+    elif kind == "rope":
+        refs = O.swin_attention_rope_bwd(q, kk, v, dout, H, W, k, s, pm, theta, scale)
+        ref_lse = O.swin_attention_rope_lse(q, kk, v, H, W, k, s, pm, theta, scale)
+    else:
+        refs = O.swin_attention_ms_bwd(q, kk, v, dout, glist, k, s, pm)
+        ref_lse = O.swin_attention_ms_lse(q, kk, v, glist, k, s, pm)
+    # the log-sum-exp: the forward's bound, plus for RoPE the bf16 rounding of the rotated q, k
+    # (2 * 2^-9 relative per logit: a rotation keeps norms)
+    bound = 4e-3
+    if kind == "rope":
+        qn = np.linalg.norm(q, axis=-1).transpose(0, 2, 1)
+        kmax = np.linalg.norm(kk, axis=-1).max(axis=1)[:, :, None]
+        bound = 4e-3 + 2.0 * 2.0 ** -9 * 0.125 * qn * kmax
+    assert (np.abs(lse - ref_lse) <= bound).all()
+    for name, got, ref in zip(("dq", "dk", "dv"), (ld("dq", L), ld("dk", rows), ld("dv", rows)), refs):
+        assert np.isfinite(got).all(), name
+        M = np.abs(ref).max()
+        err = np.abs(got - ref)
+        assert err.max() <= 2e-2 * M and err.mean() <= 2e-3 * M, (name, err.max() / M, err.mean() / M)
