@@ -115,6 +115,7 @@ CYCLE_CASES = [  # B, L, d, N, repeats
     (1, 9000, 3, 4, 2),
     (1, 25600, 1, 1, 3),
     (1, 40000, 1, 2, 3),
+    (1, 70000, 1, 1, 2),   # 274 chunks: 8 segments of 35, two load batches each (the second run reloads)
 ]
 
 

@@ -45,6 +45,7 @@ CASES = [  # B, L, d, N, repeats
     (1, 700, 64, 32, 4),    # four copies
     (2, 64, 1, 4, 5),       # one channel (one live lane per wave), two whole chunks, five copies
     (1, 25600, 40, 4, 3),   # 100 chunks of 256 tokens: the carry pass in four segments
+    (1, 70000, 40, 2, 2),   # 274 chunks: eight segments of two load batches each
 ]
 
 
