@@ -71,6 +71,10 @@ hipError_t hipLaunchKernel(const void* fn, dim3 grid, dim3 block, void** args, s
 }
 
 namespace fla {
-// the static scratch of the allocation-free backward has no host counterpart
-hipError_t scratch_address(void**) { return 1; }
+// the static device array of the allocation-free backward: a host array of the same size
+hipError_t scratch_address(void** ptr) {
+    alignas(256) static unsigned char scratch[kScratchBytes];
+    *ptr = scratch;
+    return hipSuccess;
+}
 }  // namespace fla

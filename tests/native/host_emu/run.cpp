@@ -74,6 +74,11 @@ static void dump_u16(const char* dir, const char* name, const uint16_t* p, size_
     std::fclose(f);
 }
 
+static std::mt19937& g_rng() {
+    static std::mt19937 r(2468);
+    return r;
+}
+
 static uint16_t* alloc_bf16(size_t n, std::mt19937& g, bool random) {
     uint16_t* p = static_cast<uint16_t*>(std::aligned_alloc(16, ((n * 2 + 15) / 16) * 16));
     std::normal_distribution<float> d(0.f, 1.f);
@@ -193,6 +198,28 @@ static int run_bf16_train(int argc, char** argv) {
     if (rc != 0) {
         std::fprintf(stderr, "bf16 backward: %s\n", fla_status_string(rc));
         return 1;
+    }
+    if (std::strcmp(kind, "plain") == 0) {
+        // the allocation-free backward (its workspace in the library's static array) gives the
+        // same bits, twice in a row
+        uint16_t* g[3] = {alloc_bf16(B * L * tok, g_rng(), false), alloc_bf16(B * rows * tok, g_rng(), false),
+                          alloc_bf16(B * rows * tok, g_rng(), false)};
+        const uint16_t* want[3] = {dq, dk, dv};
+        const size_t n[3] = {B * L * tok, B * rows * tok, B * rows * tok};
+        for (int rep = 0; rep < 2; ++rep) {
+            rc = fla_swin_attn_bwd_noalloc(q, kk, v, out, dout, lse, g[0], g[1], g[2], B, heads, hw[0], hw[1], hd, k,
+                                           s, pm, nullptr);
+            if (rc != 0) {
+                std::fprintf(stderr, "allocation-free backward: %s\n", fla_status_string(rc));
+                return 1;
+            }
+            for (int i = 0; i < 3; ++i)
+                if (std::memcmp(g[i], want[i], n[i] * 2) != 0) {
+                    std::fprintf(stderr, "allocation-free backward differs (gradient %d, call %d)\n", i, rep);
+                    return 1;
+                }
+        }
+        for (uint16_t* p : g) std::free(p);
     }
     dump_u16(dir, "q", q, B * L * tok);
     dump_u16(dir, "k", kk, B * rows * tok);

@@ -211,7 +211,8 @@ def test_bf16_training_on_the_host(emu_binary, tmp_path, case):
     """The bf16 training forward and backward (one-window and block kernels, the pad-gradient
     reduction) on the host emulation with AddressSanitizer and UndefinedBehaviorSanitizer,
     against the fp64 oracle's gradients at the GPU tests' bounds (max 2e-2, mean 2e-3 of the
-    largest reference gradient) and its log-sum-exp."""
+    largest reference gradient) and its log-sum-exp.  For the plain cases the driver also runs
+    the allocation-free backward twice and requires the same bits as the workspace call."""
     kind, B, heads, grids, k, s, pm, theta, scale = case
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
     r = subprocess.run([emu_binary, "bf16train", kind, str(B), str(heads), grids, str(k), str(s), str(pm),
